@@ -1,0 +1,471 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself:
+hand-worked examples (tests/golden), closed forms, invariants, special cases
+that reduce to a library routine, and brute force on tiny inputs."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _rand(shape, seed, scale=1.0):
+    g = np.random.default_rng(seed)
+    return (g.standard_normal(shape) * scale).astype(np.float32)
+
+
+# ----------------------------------------------------------------------------- score
+
+def test_score_worked_examples():
+    for case in _golden("score_worked.json")["cases"]:
+        G, W, d = case["G"], case["W"], case["d"]
+        q = np.array(case["q"], dtype=np.float32)[None, None]          # [B=1][L=1][Hq=G][W][d]
+        k = np.array(case["k"], dtype=np.float32)[None, None]          # [L][Hkv=1][T][d]
+        N = k.shape[2]
+        s = oracle.score(q, k, [0, N], Hkv=1)
+        # inputs pass through float32 (ln 2, ln 3 round at ~3e-8 relative)
+        np.testing.assert_allclose(s[0, 0], case["expect"], rtol=1e-7, atol=0, err_msg=case["name"])
+
+
+def test_score_rows_sum_to_GW():
+    # every window row is a probability distribution, so a unit's scores add up to G*W
+    B, L, Hq, Hkv, W, d = 2, 2, 6, 2, 5, 16
+    lens = [37, 21]
+    cu = [0, 37, 58]
+    q = _rand((B, L, Hq, W, d), 1)
+    k = _rand((L, Hkv, cu[-1], d), 2)
+    s = oracle.score(q, k, cu, Hkv)
+    G = Hq // Hkv
+    for l in range(L):
+        for h in range(Hkv):
+            for b in range(B):
+                tot = s[l, h, cu[b]:cu[b + 1]].sum()
+                assert abs(tot - G * W) <= 1e-9 * G * W
+            assert (s[l, h] >= 0).all()
+
+
+def test_score_equal_keys_closed_form():
+    # all keys equal: row at position p spreads 1/(p+1) over keys 0..p
+    B, L, Hq, Hkv, W, d, N = 1, 1, 4, 2, 7, 8, 19
+    q = _rand((B, L, Hq, W, d), 3)
+    row = _rand((d,), 4)
+    k = np.broadcast_to(row, (L, Hkv, N, d)).copy()
+    s = oracle.score(q, k, [0, N], Hkv)
+    G = Hq // Hkv
+    pos = np.arange(N - W, N)
+    expect = np.array([G * sum(1.0 / (p + 1) for p in pos if p >= j) for j in range(N)])
+    for h in range(Hkv):
+        np.testing.assert_allclose(s[0, h], expect, rtol=1e-12)
+
+
+def test_score_causal_and_window_match_torch_softmax():
+    # special case reducing to a library routine: the window rows are the last W rows
+    # of the full causal attention-probability matrix (torch.softmax in fp64)
+    B, L, Hq, Hkv, d = 2, 2, 8, 2, 32
+    W = 6
+    lens = [29, 40]
+    cu = [0, 29, 69]
+    G = Hq // Hkv
+    q = _rand((B, L, Hq, W, d), 5)
+    k = _rand((L, Hkv, cu[-1], d), 6)
+    s = oracle.score(q, k, cu, Hkv)
+    for b in range(B):
+        N = lens[b]
+        for l in range(L):
+            # full query matrix: random rows for non-window positions, the window rows at the end
+            qfull = torch.from_numpy(_rand((Hq, N, d), 100 + b * 10 + l)).double()
+            qfull[:, N - W:] = torch.from_numpy(q[b, l]).double()
+            kk = torch.from_numpy(k[l, :, cu[b]:cu[b + 1]]).double()
+            kk = kk.repeat_interleave(G, dim=0)                      # q head g reads KV head g // G
+            logits = qfull @ kk.transpose(1, 2) / math.sqrt(d)
+            causal = torch.ones(N, N, dtype=torch.bool).tril()
+            p = torch.softmax(logits.masked_fill(~causal, float("-inf")), dim=-1)
+            colsum = p[:, N - W:].sum(dim=1)                         # [Hq][N]
+            expect = colsum.view(Hkv, G, N).sum(dim=1).numpy()
+            np.testing.assert_allclose(s[l, :, cu[b]:cu[b + 1]], expect, rtol=1e-10, atol=1e-14)
+
+
+def test_score_window_equals_prompt_reduces_to_full_causal():
+    B, L, Hq, Hkv, d, N = 1, 1, 2, 1, 8, 12
+    q = _rand((B, L, Hq, N, d), 7)
+    k = _rand((L, Hkv, N, d), 8)
+    s = oracle.score(q, k, [0, N], Hkv)
+    qq = torch.from_numpy(q[0, 0]).double()
+    kk = torch.from_numpy(k[0, 0]).double()
+    causal = torch.ones(N, N, dtype=torch.bool).tril()
+    p = torch.softmax((qq @ kk.T / math.sqrt(d)).masked_fill(~causal, float("-inf")), dim=-1)
+    np.testing.assert_allclose(s[0, 0], p.sum(dim=(0, 1)).numpy(), rtol=1e-10)
+
+
+def test_score_aligned_heavy_key_takes_almost_all_mass():
+    B, L, Hq, Hkv, W, d, N = 1, 1, 4, 1, 8, 16, 64
+    q = np.zeros((B, L, Hq, W, d), dtype=np.float32)
+    q[..., 0] = 10.0
+    k = _rand((L, Hkv, N, d), 9, 0.01)
+    k[0, 0, 20, 0] = 10.0                  # before the window: every row sees it
+    s = oracle.score(q, k, [0, N], Hkv)
+    assert s[0, 0, 20] > 4 * 8 * (1 - 1e-6)
+    assert s[0, 0, 20] <= 4 * 8
+
+
+def test_score_last_key_only_seen_by_last_row():
+    B, L, Hq, Hkv, W, d, N = 1, 1, 1, 1, 4, 8, 30
+    q = _rand((B, L, Hq, W, d), 10)
+    k = _rand((L, Hkv, N, d), 11)
+    s = oracle.score(q, k, [0, N], Hkv)
+    z = k[0, 0].astype(np.float64) @ q[0, 0, 0, W - 1].astype(np.float64) / math.sqrt(d)
+    p_last = np.exp(z[-1] - z.max()) / np.exp(z - z.max()).sum()
+    np.testing.assert_allclose(s[0, 0, -1], p_last, rtol=1e-12)
+
+
+def test_score_shared_layer_source():
+    # a layer stride of 0 rows means every layer reads the same K
+    B, L, Hq, Hkv, W, d, N = 1, 3, 2, 1, 3, 8, 10
+    q = _rand((B, L, Hq, W, d), 12)
+    k1 = _rand((1, Hkv, N, d), 13)
+    s_shared = oracle.score(q, k1, [0, N], Hkv, k_layer_rows=0)
+    k3 = np.repeat(k1, L, axis=0)
+    s_full = oracle.score(q, k3, [0, N], Hkv)
+    np.testing.assert_array_equal(s_shared, s_full)
+
+
+def test_score_rejects_window_longer_than_prompt():
+    q = _rand((1, 1, 1, 5, 4), 1)
+    k = _rand((1, 1, 4, 4), 2)
+    with pytest.raises(ValueError):
+        oracle.score(q, k, [0, 4], 1)
+
+
+# ----------------------------------------------------------------------------- topk
+
+def _brute_topk(s, k):
+    s = np.asarray(s, dtype=np.float32)
+    key = np.where(np.isnan(s), -np.inf, s).astype(np.float64)
+    nan = np.isnan(s)
+    # lexsort: last key is primary -> (nan last, -score, index)
+    order = np.lexsort((np.arange(len(s)), -key, nan))
+    return np.sort(order[:k])
+
+
+def test_topk_worked_example():
+    g = _golden("topk_worked.json")
+    s = np.array([float(x) for x in g["scores"]], dtype=np.float32)
+    N = len(s)
+    for kk, expect in g["expect"].items():
+        kk = int(kk)
+        out = oracle.topk(s[None, None], [0, N], [0, kk])
+        np.testing.assert_array_equal(out[0, 0], expect)
+
+
+@pytest.mark.parametrize("levels", [0, 3, 50])
+def test_topk_brute_force(levels):
+    g = np.random.default_rng(levels)
+    lens = [1, 15, 16, 17, 200]
+    cu = np.cumsum([0] + lens)
+    L, Hkv = 2, 3
+    s = g.random((L, Hkv, cu[-1])).astype(np.float32)
+    if levels:
+        s = (np.floor(s * levels) / levels).astype(np.float32)
+    ks = [1, 7, 16, 1, 50]
+    ck = np.cumsum([0] + ks)
+    out = oracle.topk(s, cu, ck)
+    for l in range(L):
+        for h in range(Hkv):
+            for b in range(len(lens)):
+                row = s[l, h, cu[b]:cu[b + 1]]
+                got = out[l, h, ck[b]:ck[b + 1]]
+                np.testing.assert_array_equal(got, _brute_topk(row, ks[b]))
+                # invariants: k distinct ascending, selected >= unselected, ties go low
+                assert len(set(got.tolist())) == ks[b] and (np.diff(got) > 0).all()
+                mask = np.zeros(len(row), bool)
+                mask[got] = True
+                if (~mask).any():
+                    assert row[mask].min() >= row[~mask].max()
+                    thr = row[mask].min()
+                    tied_sel = np.nonzero(mask & (row == thr))[0]
+                    tied_unsel = np.nonzero(~mask & (row == thr))[0]
+                    if len(tied_unsel):
+                        assert tied_sel.max() < tied_unsel.min()
+
+
+def test_topk_all_equal_is_address_prefix():
+    # equal scores select the first k tokens in address order (the paper's partial-transfer baseline)
+    N, k = 100, 13
+    s = np.full((1, 1, N), 0.25, dtype=np.float32)
+    out = oracle.topk(s, [0, N], [0, k])
+    np.testing.assert_array_equal(out[0, 0], np.arange(k))
+
+
+def test_topk_full_budget_selects_everything():
+    N = 33
+    s = np.random.default_rng(0).random((1, 2, N)).astype(np.float32)
+    out = oracle.topk(s, [0, N], [0, N])
+    np.testing.assert_array_equal(out[0, 0], np.arange(N))
+    np.testing.assert_array_equal(out[0, 1], np.arange(N))
+
+
+def test_topk_rejects_k_above_n():
+    s = np.zeros((1, 1, 4), dtype=np.float32)
+    with pytest.raises(ValueError):
+        oracle.topk(s, [0, 4], [0, 5])
+
+
+# ----------------------------------------------------------------------------- pack
+
+def test_pack_worked_example():
+    g = _golden("pack_worked.json")
+    k = np.array(g["k"], dtype=np.float32)[None, None]
+    v = np.array(g["v"], dtype=np.float32)[None, None]
+    idx = np.array(g["idx"], dtype=np.int32)[None, None]
+    buf = oracle.pack(k, v, idx, [0, 4], [0, 2])
+    S, d = 2, 2
+    kr = buf[:S * d * 4].view(np.float32).reshape(S, d)
+    vr = buf[S * d * 4:2 * S * d * 4].view(np.float32).reshape(S, d)
+    ir = buf[2 * S * d * 4:].view(np.int32)
+    np.testing.assert_array_equal(kr, g["expect_k_rows"])
+    np.testing.assert_array_equal(vr, g["expect_v_rows"])
+    np.testing.assert_array_equal(ir, g["expect_idx"])
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.uint16])
+def test_pack_slots_are_source_rows(dtype):
+    g = np.random.default_rng(1)
+    L, Hkv, d = 3, 2, 8
+    lens = [10, 3, 25]
+    cu = np.cumsum([0] + lens)
+    ks = [4, 3, 1]
+    ck = np.cumsum([0] + ks)
+    T = cu[-1]
+    if dtype == np.uint16:
+        k = g.integers(0, 65535, (L, Hkv, T, d), dtype=np.uint16)
+        v = g.integers(0, 65535, (L, Hkv, T, d), dtype=np.uint16)
+    else:
+        k = g.standard_normal((L, Hkv, T, d)).astype(np.float32)
+        v = g.standard_normal((L, Hkv, T, d)).astype(np.float32)
+    idx = np.zeros((L, Hkv, ck[-1]), dtype=np.int32)
+    for l in range(L):
+        for h in range(Hkv):
+            for b in range(3):
+                idx[l, h, ck[b]:ck[b + 1]] = np.sort(g.choice(lens[b], ks[b], replace=False))
+    buf = oracle.pack(k, v, idx, cu, ck)
+    S = L * Hkv * ck[-1]
+    rb = d * k.dtype.itemsize
+    kr = buf[:S * rb].view(k.dtype).reshape(L, Hkv, ck[-1], d)
+    vr = buf[S * rb:2 * S * rb].view(k.dtype).reshape(L, Hkv, ck[-1], d)
+    ir = buf[2 * S * rb:].view(np.int32).reshape(L, Hkv, ck[-1])
+    for l in range(L):
+        for h in range(Hkv):
+            for b in range(3):
+                for i in range(ks[b]):
+                    s = ck[b] + i
+                    t = idx[l, h, s]
+                    assert kr[l, h, s].tobytes() == k[l, h, cu[b] + t].tobytes()
+                    assert vr[l, h, s].tobytes() == v[l, h, cu[b] + t].tobytes()
+    np.testing.assert_array_equal(ir, idx)
+
+
+def test_pack_full_selection_is_concatenation():
+    # k = N with idx = 0..N-1 reproduces the source: the full-transfer baseline
+    g = np.random.default_rng(2)
+    L, Hkv, N, d = 2, 2, 9, 4
+    k = g.standard_normal((L, Hkv, N, d)).astype(np.float32)
+    v = g.standard_normal((L, Hkv, N, d)).astype(np.float32)
+    idx = np.broadcast_to(np.arange(N, dtype=np.int32), (L, Hkv, N)).copy()
+    buf = oracle.pack(k, v, idx, [0, N], [0, N])
+    S = L * Hkv * N
+    assert buf[:S * d * 4].tobytes() == k.tobytes()
+    assert buf[S * d * 4:2 * S * d * 4].tobytes() == v.tobytes()
+
+
+def test_pack_invalid_index_gives_zero_row():
+    k = np.ones((1, 1, 4, 2), dtype=np.float32)
+    idx = np.array([[[4, -1, 2]]], dtype=np.int32)
+    buf = oracle.pack(k, k, idx, [0, 4], [0, 3])
+    kr = buf[:3 * 8].view(np.float32).reshape(3, 2)
+    np.testing.assert_array_equal(kr, [[0, 0], [0, 0], [1, 1]])
+
+
+# ----------------------------------------------------------------------------- split (Algorithm 1)
+
+def _split_inputs(rows):
+    masks = [np.array(r["mask"], np.int8) for r in rows]
+    idxs = [np.array(r["kv_index"], np.int32) for r in rows]
+    row_off = np.cumsum([0] + [len(i) for i in idxs]).astype(np.int32)
+    mask_off = np.cumsum([0] + [len(m) for m in masks])[:-1].astype(np.int64)
+    mask_len = np.array([len(m) for m in masks], np.int32)
+    return row_off, np.concatenate(idxs), np.concatenate(masks), mask_off, mask_len
+
+
+@pytest.mark.parametrize("reorder", [0, 1])
+def test_split_worked_example(reorder):
+    rows = _golden("split_worked.json")["rows"]
+    row_off, ix, m, mo, ml = _split_inputs(rows)
+    out, loc, rem, nl, nr = oracle.split(row_off, ix, m, mo, ml, reorder)
+    for r, row in enumerate(rows):
+        o = row_off[r]
+        assert nl[r] == len(row["local"]) and nr[r] == len(row["remote"])
+        np.testing.assert_array_equal(loc[o:o + nl[r]], row["local"])
+        np.testing.assert_array_equal(rem[o:o + nr[r]], row["remote"])
+        if reorder:
+            np.testing.assert_array_equal(out[o:row_off[r + 1]], row["reordered"])
+
+
+def test_split_brute_force_and_invariants():
+    g = np.random.default_rng(3)
+    rows, N = 40, 64
+    n = g.integers(0, 30, rows)
+    row_off = np.cumsum([0] + list(n)).astype(np.int32)
+    mask = g.integers(0, 3, rows * N).astype(np.int8)
+    mask[g.random(rows * N) < 0.02] = 7                  # invalid codes count as pads
+    mo = (np.arange(rows) * N).astype(np.int64)
+    ml = np.full(rows, N, np.int32)
+    ix = np.concatenate([g.integers(-2, N + 2, k) for k in n]).astype(np.int32)
+    out, loc, rem, nl, nr = oracle.split(row_off, ix, mask, mo, ml, 1)
+    for r in range(rows):
+        seg = ix[row_off[r]:row_off[r + 1]]
+        valid = (seg >= 0) & (seg < N)
+        m = np.where(valid, mask[r * N + np.clip(seg, 0, N - 1)], 0)
+        m = np.where((m == 1) | (m == 2), m, 0)
+        o = row_off[r]
+        np.testing.assert_array_equal(loc[o:o + nl[r]], seg[m == 1])
+        np.testing.assert_array_equal(rem[o:o + nr[r]], seg[m == 2])
+        order = np.argsort(-m, kind="stable")
+        np.testing.assert_array_equal(out[o:row_off[r + 1]], seg[order])
+        assert nl[r] + nr[r] + (m == 0).sum() == len(seg)
+        assert (loc[o + nl[r]:row_off[r + 1]] == -1).all()
+
+
+def test_split_all_local_and_all_remote():
+    N = 10
+    ix = np.arange(N, dtype=np.int32)
+    for code, want_local in ((1, True), (2, False)):
+        mask = np.full(N, code, np.int8)
+        _, loc, rem, nl, nr = oracle.split([0, N], ix, mask, [0], [N], 0)
+        if want_local:
+            assert nl[0] == N and nr[0] == 0
+        else:
+            assert nl[0] == 0 and nr[0] == N
+
+
+# ----------------------------------------------------------------------------- fetch
+
+def test_fetch_paged_destination_brute_force():
+    g = np.random.default_rng(4)
+    d, P, rows = 4, 4, 5
+    src_rows = 100
+    ks = g.standard_normal((src_rows, d)).astype(np.float32)
+    vs = g.standard_normal((src_rows, d)).astype(np.float32)
+    n = g.integers(0, 9, rows)
+    row_off = np.cumsum([0] + list(n)).astype(np.int32)
+    index = g.integers(0, 20, row_off[-1]).astype(np.int32)
+    n_valid = np.minimum(n, g.integers(0, 9, rows)).astype(np.int32)
+    src_base = (np.arange(rows) * 20).astype(np.int64)
+    max_pages = 5
+    pool_rows = 128
+    pages = g.permutation(pool_rows // P)[:rows * max_pages].reshape(rows, max_pages) * P
+    dst_start = g.integers(0, 6, rows).astype(np.int32)
+    kp = np.zeros((pool_rows, d), np.float32)
+    vp = np.zeros((pool_rows, d), np.float32)
+    oracle.fetch(row_off, index, n_valid, src_base, ks, vs, pages, P, dst_start, kp, vp)
+    ek = np.zeros_like(kp)
+    ev = np.zeros_like(vp)
+    for r in range(rows):
+        for i in range(n_valid[r]):
+            t = index[row_off[r] + i]
+            lr = dst_start[r] + i
+            dst = pages[r, lr // P] + lr % P
+            ek[dst] = ks[src_base[r] + t]
+            ev[dst] = vs[src_base[r] + t]
+    np.testing.assert_array_equal(kp, ek)
+    np.testing.assert_array_equal(vp, ev)
+
+
+def test_fetch_identity_index_and_bounds():
+    d = 2
+    ks = np.arange(20, dtype=np.float32).reshape(10, d)
+    kp = np.zeros((4, d), np.float32)
+    vp = np.zeros((4, d), np.float32)
+    # 6 entries starting at logical row 0 of a 1-page (4-row) destination: entries 4,5 fall off the table
+    oracle.fetch([0, 6], None, None, [3], ks, ks, [[0]], 4, [0], kp, vp)
+    np.testing.assert_array_equal(kp, ks[3:7])
+
+
+# ----------------------------------------------------------------------------- decode attention
+
+def test_decode_worked_example():
+    g = _golden("decode_worked.json")
+    q = np.array(g["q"], np.float32)[None]                      # [B=1][Hq=2][d]
+    pt = np.array(g["page_table"], np.int32)[None, None]       # [B][Hkv=1][pages]
+    o = oracle.decode_attn(q, np.array(g["pool_k"], np.float32), np.array(g["pool_v"], np.float32),
+                           pt, np.array([[g["n_rows"]]], np.int32), 1, scale=g["scale"])
+    np.testing.assert_allclose(o[0], g["expect"], rtol=1e-7, atol=1e-12)
+
+
+def _dense_case(seed, B=2, Hq=8, Hkv=2, d=16, N=37, P=4):
+    g = np.random.default_rng(seed)
+    q = g.standard_normal((B, Hq, d)).astype(np.float32)
+    kd = g.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    vd = g.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    npg = (N + P - 1) // P
+    # scatter the dense rows into a pool through shuffled pages
+    pages = g.permutation(B * Hkv * npg).reshape(B, Hkv, npg)
+    kp = np.zeros((B * Hkv * npg * P, d), np.float32)
+    vp = np.zeros_like(kp)
+    for b in range(B):
+        for h in range(Hkv):
+            for i in range(N):
+                r = pages[b, h, i // P] * P + i % P
+                kp[r] = kd[b, h, i]
+                vp[r] = vd[b, h, i]
+    return q, kd, vd, kp, vp, (pages * P).astype(np.int32), np.full((B, Hkv), N, np.int32)
+
+
+def test_decode_full_selection_equals_dense_sdpa():
+    q, kd, vd, kp, vp, pt, nr = _dense_case(5)
+    o = oracle.decode_attn(q, kp, vp, pt, nr, 4)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q).double()[:, :, None], torch.from_numpy(kd).double(),
+        torch.from_numpy(vd).double(), enable_gqa=True)[:, :, 0]
+    np.testing.assert_allclose(o, ref.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_decode_page_order_does_not_matter():
+    q, kd, vd, kp, vp, pt, nr = _dense_case(6, N=32)           # whole pages only
+    o1 = oracle.decode_attn(q, kp, vp, pt, nr, 4)
+    g = np.random.default_rng(0)
+    pt2 = pt.copy()
+    for b in range(pt.shape[0]):
+        for h in range(pt.shape[1]):
+            pt2[b, h] = pt[b, h][g.permutation(pt.shape[2])]
+    o2 = oracle.decode_attn(q, kp, vp, pt2, nr, 4)
+    np.testing.assert_allclose(o1, o2, rtol=1e-12, atol=1e-12)
+
+
+def test_decode_single_row_returns_its_value_and_equal_keys_average():
+    g = np.random.default_rng(7)
+    d = 8
+    kp = g.standard_normal((10, d)).astype(np.float32)
+    vp = g.standard_normal((10, d)).astype(np.float32)
+    q = g.standard_normal((1, 1, d)).astype(np.float32)
+    o = oracle.decode_attn(q, kp, vp, np.array([[[6]]], np.int32), np.array([[1]], np.int32), 1)
+    np.testing.assert_allclose(o[0, 0], vp[6], rtol=0, atol=0)
+    kp[:] = kp[0]
+    o = oracle.decode_attn(q, kp, vp, np.array([[[2, 5, 7]]], np.int32), np.array([[3]], np.int32), 1)
+    np.testing.assert_allclose(o[0, 0], vp[[2, 5, 7]].astype(np.float64).mean(0), rtol=1e-12, atol=1e-14)
+
+
+def test_decode_empty_set_is_zero():
+    q = np.ones((1, 2, 4), np.float32)
+    o = oracle.decode_attn(q, np.ones((4, 4), np.float32), np.ones((4, 4), np.float32),
+                           np.zeros((1, 1, 1), np.int32), np.zeros((1, 1), np.int32), 4)
+    assert (o == 0).all()
