@@ -1,0 +1,271 @@
+"""Benchmark of the selective KV-transfer hot path on one MI355X.
+
+One step = one pass of the whole path over one request of the Llama-3-8B-shaped
+workload (32 layers, 32 q heads / 8 KV heads, d = 128, bf16, 8192-token prompt,
+64-query score window, 10% budget, 128 decode steps):
+
+  prefill side   sg_score -> sg_topk -> sg_pack (transfer buffer in HBM)
+  decode side    128 x [ sg_split (Algorithm 1 on the step's KV index)
+                         -> sg_decode_attn over the selected rows of all 32
+                            layers, batched as 32 sequences ]
+
+Inputs are generated on the GPU before timing.  The decode reads rotate over
+several replicas of the transfer buffer so the working set exceeds the 256 MB
+last-level cache (a real decode step streams the model weights between layers).
+
+Prints one JSON line.  ``value`` is select+pack throughput: bytes of the KV
+cache (K and V of every layer and head) turned into a transfer buffer per
+second of score + top-k + pack time.  The decode rate is reported as
+``decode_tokens_per_s``; the roofline object covers the dominant kernel
+(sparse decode attention).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+_ROOT = os.path.dirname(os.path.abspath(__file__))
+if _ROOT not in sys.path:
+    sys.path.insert(0, _ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="llama8b_8k")
+    p.add_argument("--decode-steps", type=int, default=None, help="decode steps per step (default: workload's)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-layers", type=int, default=2, help="layers of the workload the oracle is timed on")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus_requested": args.gpus}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from datagen import inputs
+    from datagen.configs import get
+    from paper_2607_28150_amd import smartgen as sg
+
+    if not os.path.exists(sg.LIB_PATH):
+        from paper_2607_28150_amd import build as hip_build
+        hip_build.build()
+    sg.load()
+    assert torch.cuda.is_available(), "bench needs a GPU"
+    dev = "cuda"
+    cfg = get(args.workload)
+    assert cfg.B == 1 and cfg.extra_bp == 0, "the bench step covers single-request workloads without extras"
+    nsteps_dec = cfg.steps if args.decode_steps is None else args.decode_steps
+    L, Hq, Hkv, d, W, G = cfg.L, cfg.Hq, cfg.Hkv, cfg.d, cfg.W, cfg.G
+
+    # ------------------------------------------------------------- inputs (resident in HBM)
+    t0 = time.time()
+    pre = inputs.make_prefill(cfg, device=dev)
+    lens, T = pre["seqlens"], pre["T"]
+    N = lens[0]
+    bud = inputs.make_budget(cfg, lens)
+    K_total = bud["K_total"]
+    cus = torch.tensor(pre["cu_seqlens"], dtype=torch.int32, device=dev)
+    cuk = torch.tensor(bud["cu_k"], dtype=torch.int32, device=dev)
+    qdec = torch.stack([inputs.decode_queries(cfg, s, device=dev, mu=pre["mu"])[0] for s in range(nsteps_dec)])
+    qdec = qdec.contiguous()                                           # [steps][L][Hq][d]
+    esize = 2 if cfg.dtype == "bf16" else 4
+    S = L * Hkv * K_total
+    nbytes = sg.pack_bytes(pre["k"].dtype, L, Hkv, d, K_total)
+    reps = max(2, math.ceil(640e6 / nbytes))
+    bufs = [torch.empty(nbytes, dtype=torch.uint8, device=dev) for _ in range(reps)]
+    scores = torch.empty((L, Hkv, T), device=dev)
+    idx = torch.empty((L, Hkv, K_total), dtype=torch.int32, device=dev)
+    ws_score = torch.empty(sg.score_workspace_size(1, L, Hq, Hkv, d, W, N), dtype=torch.uint8, device=dev)
+    P = cfg.page_size
+    npg = (K_total + P - 1) // P
+    units = L * Hkv
+    # decode: sequence = layer; unit (l, h) rows are slots (l*Hkv + h)*K_total + i of the K / V regions
+    page_table = (torch.arange(units, device=dev)[:, None] * K_total
+                  + torch.arange(npg, device=dev)[None, :] * P).to(torch.int32).view(L, Hkv, npg).contiguous()
+    n_rows = torch.full((L, Hkv), K_total, dtype=torch.int32, device=dev)
+    ws_dec = torch.zeros(max(sg.decode_workspace_size(L, Hq, Hkv, d, npg, P), 16), dtype=torch.uint8, device=dev)
+    out = torch.empty((L, Hq, d), device=dev)
+    pools = []
+    for b in bufs:
+        kp = b[: S * d * esize].view(pre["k"].dtype).view(S, d)
+        vp = b[S * d * esize: 2 * S * d * esize].view(pre["k"].dtype).view(S, d)
+        pools.append((kp, vp))
+    # Algorithm 1 inputs: every selected row is local (mask 1) in this workload
+    split_rows = units
+    row_off = (torch.arange(split_rows + 1, device=dev) * K_total).to(torch.int32)
+    mask = torch.ones((units, N), dtype=torch.int8, device=dev)
+    mask_off = (torch.arange(units, device=dev, dtype=torch.int64) * N)
+    mask_len = torch.full((units,), N, dtype=torch.int32, device=dev)
+    sp_local = torch.empty(S, dtype=torch.int32, device=dev)
+    sp_remote = torch.empty(S, dtype=torch.int32, device=dev)
+    sp_order = torch.empty(S, dtype=torch.int32, device=dev)
+    sp_nl = torch.empty(split_rows, dtype=torch.int32, device=dev)
+    sp_nr = torch.empty(split_rows, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    # timed ops of one step: score, topk, pack, then per decode step split and decode
+    def step(r, rec):
+        e = [ev() for _ in range(4)]
+        e[0].record()
+        sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score)
+        e[1].record()
+        sg.sg_topk(scores, cus, T, N, cuk, K_total, idx)
+        e[2].record()
+        sg.sg_pack(pre["k"], pre["v"], idx, cus, T, cuk, K_total, K_total, bufs[r % reps])
+        e[3].record()
+        dec = []
+        for s in range(nsteps_dec):
+            kp, vp = pools[(r + s) % reps]
+            a, b_, c = ev(), ev(), ev()
+            a.record()
+            sg.sg_split(row_off, idx.view(-1), mask.view(-1), mask_off, mask_len, 1, sp_local, sp_remote, sp_nl,
+                        sp_nr, out_index=sp_order)
+            b_.record()
+            sg.sg_decode_attn(qdec[s], kp, vp, page_table, n_rows, P, out, ws=ws_dec)
+            c.record()
+            dec.append((a, b_, c))
+        if rec is not None:
+            rec.append((e, dec))
+
+    # every replica holds a packed buffer before timing
+    for r in range(reps):
+        step(r, None)
+    for w in range(args.warmup):
+        step(w, None)
+    torch.cuda.synchronize()
+
+    recs = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        step(k, recs)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+
+    # ------------------------------------------------------------- per-op times
+    def ms(a, b):
+        return a.elapsed_time(b)
+    t_score = np.mean([ms(e[0], e[1]) for e, _ in recs])
+    t_topk = np.mean([ms(e[1], e[2]) for e, _ in recs])
+    t_pack = np.mean([ms(e[2], e[3]) for e, _ in recs])
+    t_split = np.mean([ms(a, b_) for _, dec in recs for a, b_, _c in dec])
+    t_dec = np.mean([ms(b_, c) for _, dec in recs for _a, b_, c in dec])
+    ms_per_step = wall * 1e3 / args.steps
+
+    kv_bytes = 2 * L * Hkv * T * d * esize                       # the whole KV cache
+    sel_ms = t_score + t_topk + t_pack
+    value = kv_bytes / (sel_ms * 1e-3) / 1e9
+    score_flops = 2.0 * d * G * (W * N - W * (W - 1) / 2) * units
+    pack_bytes_alg = 2 * S * d * esize * 2 + S * 4 * 2          # rows read + written, index read + written
+    dec_bytes = (2 * S * d * esize + L * Hq * d * esize + L * Hq * d * 4 + page_table.numel() * 4
+                 + n_rows.numel() * 4)
+    dec_gbs = dec_bytes / (t_dec * 1e-3) / 1e9
+    tokens_per_s = 1.0 / (t_dec * 1e-3)                          # one token of one request per decode step
+    peak_mfma = BF16_MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else FP32_MFMA_PEAK_TFLOPS
+    ops = {
+        "score": {"ms": round(t_score, 4), "tflops": round(score_flops / (t_score * 1e-3) / 1e12, 2),
+                  "frac_mfma_peak": round(score_flops / (t_score * 1e-3) / 1e12 / peak_mfma, 4),
+                  "gflop_algorithmic": round(score_flops / 1e9, 2)},
+        "topk": {"ms": round(t_topk, 4),
+                 "gbs": round((scores.numel() * 4 + idx.numel() * 4) / (t_topk * 1e-3) / 1e9, 1)},
+        "pack": {"ms": round(t_pack, 4), "gbs": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9, 1),
+                 "frac_hbm_peak": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                 "mb_algorithmic": round(pack_bytes_alg / 1e6, 2)},
+        "split": {"ms": round(t_split, 4)},
+        "decode_attn": {"ms": round(t_dec, 4), "gbs": round(dec_gbs, 1),
+                        "frac_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4),
+                        "mb_algorithmic": round(dec_bytes / 1e6, 2)},
+    }
+    line = {
+        "metric": "select+pack GB/s and sparse decode-attn tokens/s; % of MI355X HBM/MFMA peak",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
+                   "prompt": N, "score_window": W, "budget_bp": cfg.budget_bp, "k": K_total,
+                   "decode_steps": nsteps_dec, "page_size": P, "transfer_replicas": reps},
+        "decode_tokens_per_s": round(tokens_per_s, 1),
+        "roofline": {"kernel": "sg_decode_attn", "bound": "hbm", "achieved": round(dec_gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": dec_bytes, "avg_launch_ms": round(t_dec, 5)},
+        "ops": ops,
+        "setup_s": round(setup_s, 2),
+    }
+
+    # ------------------------------------------------------------- oracle on the host cores
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, pre, bud, args.cpu_layers)
+        if line["cpu_baseline"].get("value"):
+            line["gpu_over_cpu"] = round(value / line["cpu_baseline"]["value"], 1)
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(cfg, pre, bud, layers):
+    """The oracle's select+pack (score, top-k, pack) timed on a bounded sample:
+    the first ``layers`` layers of the same request, all KV heads."""
+    import numpy as np
+
+    import oracle
+    if not os.path.exists(oracle.LIB_PATH):
+        from oracle import build as ob
+        ob.build()
+    layers = max(1, min(layers, cfg.L))
+    q = pre["q_win"][:, :layers].float().cpu().numpy()
+    k = pre["k"][:layers].float().cpu().numpy()
+    kraw = pre["k"][:layers].cpu().contiguous().view(__import__("torch").int16).numpy().view(np.uint16)
+    vraw = pre["v"][:layers].cpu().contiguous().view(__import__("torch").int16).numpy().view(np.uint16)
+    units = layers * cfg.Hkv
+    threads = oracle.threads()
+    t0 = time.perf_counter()
+    s = oracle.score(q, k, pre["cu_seqlens"], cfg.Hkv)
+    idx = oracle.topk(s.astype(np.float32), pre["cu_seqlens"], bud["cu_k"])
+    oracle.pack(kraw, vraw, idx, pre["cu_seqlens"], bud["cu_k"])
+    dt = time.perf_counter() - t0
+    esize = 2 if cfg.dtype == "bf16" else 4
+    kv_bytes = 2 * units * pre["T"] * cfg.d * esize
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    cpu = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": round(kv_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": min(threads, units),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"score+topk+pack of layers 0..{layers - 1} ({units} of {cfg.L * cfg.Hkv} units), "
+                      f"same request, fp64 C oracle with OpenMP over units",
+            "cpu_model": cpu, "host": platform.node()}
+
+
+if __name__ == "__main__":
+    main()

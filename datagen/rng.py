@@ -84,10 +84,10 @@ def normal(key: int, count: int, device="cpu", start: int = 0) -> torch.Tensor:
 
 def choice_without_replacement(key: int, lo: int, hi: int, n: int, device="cpu") -> torch.Tensor:
     """``n`` distinct integers drawn uniformly from ``[lo, hi)``, ascending."""
-    if n > hi - lo:
-        raise ValueError("cannot draw more distinct values than the range holds")
     if n == 0:
         return torch.empty(0, dtype=torch.int64, device=device)
+    if n > hi - lo:
+        raise ValueError("cannot draw more distinct values than the range holds")
     r = raw64(key, hi - lo, device)
     # the n smallest random keys pick a uniform n-subset; ties have
     # probability ~2^-64 and are broken by position (stable sort)

@@ -1,0 +1,224 @@
+/*
+ * smartgen.h — C ABI of the MI355X (gfx950) selective KV-cache transfer hot
+ * path of SmartGen (arXiv 2607.28150):
+ *
+ *   sg_score        per-token importance of every (layer, KV head) from a window
+ *                   of prefill attention                     (Section 4.1)
+ *   sg_topk         budgeted exact top-k per (request, layer, KV head)
+ *                                                           (Section 2.3)
+ *   sg_pack         gather of the selected K/V rows into one transfer buffer
+ *                                                           (Sections 4.1, 4.2)
+ *   sg_split        mask-based KV index splitting and reordering (Algorithm 1)
+ *   sg_fetch        copy of indexed rows into paged destination slots
+ *                   (parallel on-demand transfer, Section 4.2; non-GDR mode,
+ *                   Section 4.4)
+ *   sg_decode_attn  decode attention over a partial KV set addressed through a
+ *                   page table (Section 2.1; order invariance, Section 4.2)
+ *
+ * Conventions for every call:
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
+ *     call is asynchronous on it; nothing is synchronised.
+ *   - Pointers are caller-owned.  "device" pointers must be readable/writable by
+ *     the GPU: device memory, or pinned host memory allocated with
+ *     hipHostMalloc (device-accessible through the same address).  The library
+ *     never allocates or frees memory; scratch comes from a caller workspace
+ *     sized by the matching *_workspace_size call.
+ *   - Scalars are checked on the host before anything is enqueued; a failing
+ *     check returns a negative sg_status, enqueues nothing, and leaves a
+ *     description in sg_last_error() (thread-local).  Device-resident metadata
+ *     (offsets, indices, page tables) cannot be checked on the host: kernels
+ *     clamp every access to the sizes passed here, so a bad entry never reads
+ *     or writes outside the arrays; the documented fallback for each call says
+ *     what such an entry produces.
+ *   - A unit is one (request b, layer l, KV head h).  q head g belongs to KV
+ *     head g / G with G = Hq / Hkv (consecutive grouping).
+ *   - Varlen batching: cu_seqlens[B+1] (device int32) are the token offsets of
+ *     the requests inside T = sum N_b; cu_k[B+1] (device int32) the offsets of
+ *     their selected rows inside K_total = sum k_b.
+ *   - Element types: SG_F32 (float) or SG_BF16 (bfloat16 stored as uint16).
+ *     Head dimension d must be 64 or 128.  Rows are d elements, contiguous;
+ *     row starts must be 16-byte aligned (true for d in {64, 128}).
+ */
+#ifndef SMARTGEN_H
+#define SMARTGEN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { SG_F32 = 0, SG_BF16 = 1 } sg_dtype;
+
+typedef enum {
+    SG_OK = 0,
+    SG_EINVAL = -1,        /* an argument is out of its documented range */
+    SG_EUNSUPPORTED = -2,  /* a valid but unimplemented combination (e.g. d = 96) */
+    SG_EWORKSPACE = -3,    /* workspace or destination smaller than required */
+    SG_EHIP = -4,          /* the HIP runtime reported an error on launch */
+    SG_EINTERNAL = -5
+} sg_status;
+
+int sg_version(void);                    /* major*10000 + minor*100 + patch */
+const char *sg_status_str(int status);   /* static string for a status code */
+const char *sg_last_error(void);         /* detail of this thread's last failure */
+
+/* ---------------------------------------------------------------- sg_score
+ * Importance of every cached token (Section 4.1 defines importance as how often
+ * attention-magnitude selection picks an entry; this computes its soft,
+ * prefill-time form).  For unit (b, l, h) with prompt length N = N_b and the
+ * last W prompt positions p_w = N - W + w as queries:
+ *
+ *   scores[l][h][cu_seqlens[b] + j] =
+ *       sum over q heads g of group h, sum over w < W, of
+ *       softmax_j( q_win[b][l][g][w] . K[l][h][j] / sqrt(d) ),  causal (j <= p_w)
+ *
+ * so each unit's scores add up to G * W.
+ *
+ *   q_win   device, dtype, [B][L][Hq][W][d]: window queries (rows p_w).
+ *   k       device, dtype, rows of d; unit (l, h, b) token j is row
+ *           l * k_layer_rows + h * T + cu_seqlens[b] + j.  k_layer_rows is
+ *           Hkv * T for a per-layer cache, 0 for one source shared by layers.
+ *   lse_in  device float [B][L][Hq][W] or NULL: natural-log log-sum-exp of
+ *           each window row's scaled causal logits (what a prefill flash
+ *           attention produces).  When given, the row statistics pass is
+ *           skipped and these values are trusted.
+ *   scores  device float [L][Hkv][T] (output).
+ *   max_seqlen  host upper bound of every N_b (sizes the launch).
+ *   ws      device workspace of at least sg_score_workspace_size(...) bytes.
+ * Requirements: W >= 1, W <= N_b for every request (a request with N_b < W gets
+ * all-zero scores), G * W <= 512, Hq % Hkv == 0.
+ */
+size_t sg_score_workspace_size(int B, int L, int Hq, int Hkv, int d, int W, int max_seqlen);
+int sg_score(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
+             const int32_t *cu_seqlens, int64_t T, int max_seqlen,
+             const void *q_win, const void *k, int64_t k_layer_rows,
+             const float *lse_in, float *scores, void *ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------- sg_topk
+ * Exact top-k of every unit row (Section 2.3: each head of each request keeps
+ * its own top-k entries, the KV index of shape BH x k).  Order: larger score
+ * first; equal scores by lower token index; -0 equals +0; NaN ranks below every
+ * number.  The k_b = cu_k[b+1] - cu_k[b] chosen token ids (request-local,
+ * 0 <= id < N_b) are written in ascending order to
+ * idx[l][h][cu_k[b] .. cu_k[b+1]).
+ *
+ *   scores  device float [L][Hkv][T].
+ *   idx     device int32 [L][Hkv][K_total] (output).
+ *   max_seqlen  host bound of every N_b; must be <= 65536.
+ * A request with k_b > N_b or k_b < 0 (device metadata) gets idx = -1 in its
+ * segment.
+ */
+int sg_topk(void *stream, int B, int L, int Hkv, const int32_t *cu_seqlens, int64_t T,
+            int max_seqlen, const int32_t *cu_k, int64_t K_total,
+            const float *scores, int32_t *idx);
+
+/* ---------------------------------------------------------------- sg_pack
+ * Gathers the selected K and V rows of every unit into one contiguous transfer
+ * buffer (the block push of proactive transfer, Section 4.1; a row of selected
+ * entries is BH x k x d, Section 4.2).  Layout of dst, S = L * Hkv * K_total:
+ *
+ *   [ K rows: S x d x esize | V rows: S x d x esize | idx: S x int32 ]
+ *
+ * slot s = (l * Hkv + h) * K_total + cu_k[b] + i holds the i-th selected row of
+ * unit (b, l, h): source row l * kv_layer_rows + h * T + cu_seqlens[b] + idx[s].
+ * The index table is idx verbatim.  An index outside [0, N_b) yields a zero row.
+ *
+ *   k, v    device, dtype, addressed as for sg_score (same layer stride).
+ *   idx     device int32 [L][Hkv][K_total].
+ *   dst     device memory or pinned host memory (then the kernel writes over
+ *           the host link); 16-byte aligned; dst_bytes >= sg_pack_bytes(...).
+ *   max_k   host bound of every k_b: it only sizes the launch (any k_b is
+ *           covered), so a tight bound gives the best grid.
+ */
+size_t sg_pack_bytes(sg_dtype dt, int L, int Hkv, int d, int64_t K_total);
+int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,
+            const int32_t *cu_seqlens, int64_t T, const int32_t *cu_k, int64_t K_total,
+            int max_k, const void *k, const void *v, int64_t kv_layer_rows, const int32_t *idx,
+            void *dst, size_t dst_bytes);
+
+/* ---------------------------------------------------------------- sg_split
+ * Algorithm 1: KV index splitting and (optional) reordering.  Row r holds
+ * kv_index[row_off[r] .. row_off[r+1]); its int8 mask row starts at
+ * mask[mask_off[r]] and has mask_len[r] entries (0 pad, 1 local, 2 remote;
+ * Section 4.2).  The paper shares one mask value across heads; a per-head
+ * mask is the general case and is what mask_off addresses.
+ *
+ *   (1) m_i = mask[kv_index_i] (an index outside [0, mask_len[r]) or a value
+ *       other than 1 and 2 counts as 0);
+ *   (4)(5) if reorder: out_index row = kv_index row stably sorted by m
+ *       descending (remote entries first, then local, then pads);
+ *   (2) local = entries with m == 1, (3) remote = entries with m == 2, both in
+ *       row order, written from the start of the row's segment;
+ *       n_local[r], n_remote[r] count them; the rest of each segment is -1.
+ *
+ *   row_off device int32 [rows+1]; total = row_off[rows] (host copy).
+ *   kv_index, out_index, local, remote: device int32 [total]; out_index may be
+ *   NULL when reorder == 0.  mask: device int8 of mask_bytes entries; mask_off:
+ *   device int64 [rows]; mask_len: device int32 [rows]; n_local, n_remote:
+ *   device int32 [rows].  A mask entry outside [0, mask_bytes) counts as 0.
+ */
+int sg_split(void *stream, int rows, const int32_t *row_off, int64_t total,
+             const int32_t *kv_index, const int8_t *mask, int64_t mask_bytes,
+             const int64_t *mask_off, const int32_t *mask_len, int reorder, int32_t *out_index,
+             int32_t *local, int32_t *remote, int32_t *n_local, int32_t *n_remote);
+
+/* ---------------------------------------------------------------- sg_fetch
+ * Copies indexed K/V rows into paged destination slots: the remote lane of
+ * parallel on-demand transfer (Section 4.2) with the source in pinned host
+ * memory standing in for the prefill node (non-GDR mode, Section 4.4), and the
+ * placement of received rows into the decode-side pool.
+ *
+ * Row r copies its first n_r entries, n_r = n_valid[r] (or the whole segment
+ * row_off[r+1] - row_off[r] when n_valid is NULL).  Entry i reads source row
+ * src_row_base[r] + index[row_off[r] + i] (+ i when index is NULL) of k_src /
+ * v_src and writes logical row L = dst_start[r] + i of the row's destination,
+ * i.e. pool row page_table[r * max_pages + L / page_size] + L % page_size of
+ * k_pool / v_pool.  Entries whose source row is outside [0, src_rows), whose
+ * page is outside the table or whose pool row is outside [0, pool_rows) are
+ * skipped.
+ *
+ *   k_src, v_src  device or pinned host (device-accessible), dtype rows of d.
+ *   row_off device int32 [rows+1], total = row_off[rows] (host copy); index
+ *   (device int32 [total]) and n_valid (device int32 [rows]) may be NULL;
+ *   src_row_base device int64 [rows]; page_table device int32
+ *   [rows][max_pages]; dst_start device int32 [rows].
+ */
+int sg_fetch(void *stream, sg_dtype dt, int d, int rows, const int32_t *row_off, int64_t total,
+             const int32_t *index, const int32_t *n_valid,
+             const int64_t *src_row_base, int64_t src_rows,
+             const void *k_src, const void *v_src,
+             const int32_t *page_table, int page_size, int max_pages, const int32_t *dst_start,
+             void *k_pool, void *v_pool, int64_t pool_rows);
+
+/* ---------------------------------------------------------------- sg_decode_attn
+ * Decode attention over a partial KV set (Section 2.1; Section 4.2 notes that
+ * the order of entries does not change the result).  For sequence b and q head
+ * g (KV head h = g / G):
+ *
+ *   n = min(n_rows[b][h], max_pages * page_size); logical row i lives at pool
+ *   row page_table[b][h][i / page_size] + i % page_size;
+ *   out[b][g] = sum_i softmax_i(scale * q[b][g] . k_i) * v_i      (fp32)
+ *
+ * No causal mask (a decode query sees every row of its set).  Rows whose pool
+ * index is outside [0, pool_rows) are left out; an empty set gives zeros.
+ *
+ *   q       device, dtype, [B][Hq][d].
+ *   k_pool, v_pool  device, dtype, [pool_rows][d].
+ *   page_table device int32 [B][Hkv][max_pages]; n_rows device int32 [B][Hkv].
+ *   out     device float [B][Hq][d] (output).
+ *   ws      device workspace >= sg_decode_attn_workspace_size(...) bytes.
+ * Batching layers of one step is B' = L * B independent sequences.
+ * Requirements: 1 <= G <= 16, page_size >= 1.
+ */
+size_t sg_decode_attn_workspace_size(int B, int Hq, int Hkv, int d, int max_pages, int page_size);
+int sg_decode_attn(void *stream, sg_dtype dt, int B, int Hq, int Hkv, int d, float scale,
+                   const void *q, const void *k_pool, const void *v_pool, int64_t pool_rows,
+                   const int32_t *page_table, const int32_t *n_rows, int page_size, int max_pages,
+                   float *out, void *ws, size_t ws_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SMARTGEN_H */

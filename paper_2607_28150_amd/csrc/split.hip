@@ -1,0 +1,107 @@
+// sg_split: Algorithm 1 (KV index splitting and reordering), one wavefront
+// per row of the KV index.
+//
+// The row is walked in 64-entry chunks.  Each lane gathers the mask value of
+// its entry (operator 1); three ballots give, for every lane, how many earlier
+// lanes carry each mask value, so the stable partitions (operators 2, 3) and
+// the stable descending sort by mask value (operators 4, 5) are all prefix
+// popcounts plus a running per-value count.  A first pass counts the remote
+// entries, which fixes where the local entries start in the reordered row.
+#include "sg_internal.h"
+
+namespace sg {
+
+constexpr int SPLIT_WAVES = 4;
+
+__device__ __forceinline__ int gather_mask(const int8_t *__restrict__ mask, int64_t moff, int32_t mlen,
+                                           int64_t mask_bytes, int32_t t) {
+    int m = 0;
+    if (t >= 0 && t < mlen && moff + t < mask_bytes) m = mask[moff + t];
+    return (m == 1 || m == 2) ? m : 0;
+}
+
+__global__ __launch_bounds__(64 * SPLIT_WAVES) void split_kernel(
+    int rows, const int32_t *__restrict__ row_off, int64_t total, const int32_t *__restrict__ kv_index,
+    const int8_t *__restrict__ mask, int64_t mask_bytes, const int64_t *__restrict__ mask_off,
+    const int32_t *__restrict__ mask_len, int reorder, int32_t *__restrict__ out_index,
+    int32_t *__restrict__ local, int32_t *__restrict__ remote, int32_t *__restrict__ n_local,
+    int32_t *__restrict__ n_remote) {
+    const int r = blockIdx.x * SPLIT_WAVES + threadIdx.x / 64;
+    if (r >= rows) return;
+    const int lane = threadIdx.x % 64;
+    int64_t o = row_off[r], e = row_off[r + 1];
+    if (o < 0 || e < o || e > total) {  // bad device metadata: empty row
+        if (lane == 0) { n_local[r] = 0; n_remote[r] = 0; }
+        return;
+    }
+    const int64_t n = e - o;
+    const int64_t moff = mask_off[r];
+    const int32_t mlen = moff >= 0 ? mask_len[r] : 0;   // a negative offset makes every entry a pad
+    const uint64_t lt = lanemask_lt();
+
+    // pass 1: count remote entries (the start of the local block in the reordered row)
+    int64_t n2 = 0, n1 = 0;
+    for (int64_t c = 0; c < n; c += 64) {
+        const int64_t i = c + lane;
+        const int m = i < n ? gather_mask(mask, moff, mlen, mask_bytes, kv_index[o + i]) : 0;
+        n2 += __popcll(__ballot(m == 2));
+        n1 += __popcll(__ballot(m == 1));
+    }
+    // pass 2: write the partitions
+    int64_t c2 = 0, c1 = 0, c0 = 0;
+    for (int64_t c = 0; c < n; c += 64) {
+        const int64_t i = c + lane;
+        int32_t t = -1;
+        int m = 0;
+        if (i < n) {
+            t = kv_index[o + i];
+            m = gather_mask(mask, moff, mlen, mask_bytes, t);
+        }
+        const uint64_t b2 = __ballot(i < n && m == 2);
+        const uint64_t b1 = __ballot(i < n && m == 1);
+        const uint64_t b0 = __ballot(i < n && m == 0);
+        if (i < n) {
+            if (m == 2) {
+                const int64_t p = c2 + __popcll(b2 & lt);
+                remote[o + p] = t;
+                if (reorder) out_index[o + p] = t;
+            } else if (m == 1) {
+                const int64_t p = c1 + __popcll(b1 & lt);
+                local[o + p] = t;
+                if (reorder) out_index[o + n2 + p] = t;
+            } else if (reorder) {
+                out_index[o + n2 + n1 + c0 + __popcll(b0 & lt)] = t;
+            }
+        }
+        c2 += __popcll(b2);
+        c1 += __popcll(b1);
+        c0 += __popcll(b0);
+    }
+    // unused tails of the compacted outputs
+    for (int64_t i = n1 + lane; i < n; i += 64) local[o + i] = -1;
+    for (int64_t i = n2 + lane; i < n; i += 64) remote[o + i] = -1;
+    if (lane == 0) {
+        n_local[r] = (int32_t)n1;
+        n_remote[r] = (int32_t)n2;
+    }
+}
+
+}  // namespace sg
+
+using namespace sg;
+
+extern "C" int sg_split(void *stream, int rows, const int32_t *row_off, int64_t total,
+                        const int32_t *kv_index, const int8_t *mask, int64_t mask_bytes,
+                        const int64_t *mask_off, const int32_t *mask_len, int reorder, int32_t *out_index, int32_t *local,
+                        int32_t *remote, int32_t *n_local, int32_t *n_remote) {
+    SG_REQUIRE(rows >= 0 && total >= 0 && mask_bytes >= 0, SG_EINVAL, "sg_split: negative size");
+    if (rows == 0) return SG_OK;
+    SG_REQUIRE(row_off && n_local && n_remote && mask_off && mask_len, SG_EINVAL, "sg_split: null pointer");
+    SG_REQUIRE(total == 0 || (kv_index && mask && local && remote), SG_EINVAL, "sg_split: null pointer");
+    SG_REQUIRE(!reorder || total == 0 || out_index, SG_EINVAL, "sg_split: reorder needs out_index");
+    const int blocks = (int)ceil_div(rows, SPLIT_WAVES);
+    split_kernel<<<blocks, 64 * SPLIT_WAVES, 0, as_stream(stream)>>>(
+        rows, row_off, total, kv_index, mask, mask_bytes, mask_off, mask_len, reorder ? 1 : 0, out_index, local, remote,
+        n_local, n_remote);
+    return launch_status("sg_split");
+}

@@ -1,0 +1,259 @@
+"""ctypes binding of libsmartgen.so (the C ABI declared in include/smartgen.h).
+
+Argument marshalling only: every function takes torch tensors (device memory or
+pinned host memory), checks dtypes/shapes that the C call cannot see, passes
+raw pointers and the current HIP stream, and raises ``SmartgenError`` on a
+non-zero status.  All computation runs in the library's HIP kernels.  There is
+no fallback: if the library is missing or fails to load, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsmartgen.so")
+
+SG_F32, SG_BF16 = 0, 1
+SG_OK, SG_EINVAL, SG_EUNSUPPORTED, SG_EWORKSPACE, SG_EHIP, SG_EINTERNAL = 0, -1, -2, -3, -4, -5
+
+EXPORTS = [
+    "sg_version", "sg_status_str", "sg_last_error",
+    "sg_score_workspace_size", "sg_score",
+    "sg_topk",
+    "sg_pack_bytes", "sg_pack",
+    "sg_split",
+    "sg_fetch",
+    "sg_decode_attn_workspace_size", "sg_decode_attn",
+]
+
+
+class SmartgenError(RuntimeError):
+    def __init__(self, fn: str, status: int, detail: str):
+        super().__init__(f"{fn} failed with status {status}: {detail}")
+        self.status = status
+
+
+_lib = None
+_vp, _i, _l, _sz, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+
+
+def load() -> ctypes.CDLL:
+    """Load libsmartgen.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_28150_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    lib.sg_version.restype = _i
+    lib.sg_status_str.argtypes = [_i]
+    lib.sg_status_str.restype = ctypes.c_char_p
+    lib.sg_last_error.restype = ctypes.c_char_p
+    lib.sg_score_workspace_size.argtypes = [_i] * 7
+    lib.sg_score_workspace_size.restype = _sz
+    lib.sg_score.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _l, _i, _vp, _vp, _l, _vp, _vp, _vp, _sz]
+    lib.sg_topk.argtypes = [_vp, _i, _i, _i, _vp, _l, _i, _vp, _l, _vp, _vp]
+    lib.sg_pack_bytes.argtypes = [_i, _i, _i, _i, _l]
+    lib.sg_pack_bytes.restype = _sz
+    lib.sg_pack.argtypes = [_vp, _i, _i, _i, _i, _i, _vp, _l, _vp, _l, _i, _vp, _vp, _l, _vp, _vp, _sz]
+    lib.sg_split.argtypes = [_vp, _i, _vp, _l, _vp, _vp, _l, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp]
+    lib.sg_fetch.argtypes = [_vp, _i, _i, _i, _vp, _l, _vp, _vp, _vp, _l, _vp, _vp, _vp, _i, _i, _vp, _vp, _vp, _l]
+    lib.sg_decode_attn_workspace_size.argtypes = [_i] * 6
+    lib.sg_decode_attn_workspace_size.restype = _sz
+    lib.sg_decode_attn.argtypes = [_vp, _i, _i, _i, _i, _i, _f, _vp, _vp, _vp, _l, _vp, _vp, _i, _i, _vp, _vp, _sz]
+    for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn"):
+        getattr(lib, f).restype = _i
+    _lib = lib
+    return lib
+
+
+def version() -> int:
+    return load().sg_version()
+
+
+def _check(fn: str, rc: int) -> None:
+    if rc != SG_OK:
+        raise SmartgenError(fn, rc, load().sg_last_error().decode())
+
+
+_hip = None
+
+
+def _hip_runtime():
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipHostGetDevicePointer.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_uint]
+        _hip.hipHostGetDevicePointer.restype = ctypes.c_int
+    return _hip
+
+
+def _ptr(t):
+    """Device-usable address of a tensor: device memory as is, pinned host memory
+    through hipHostGetDevicePointer (pageable host memory is refused)."""
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous")
+    if t.is_cuda or t.numel() == 0:
+        return ctypes.c_void_p(t.data_ptr())
+    if not t.is_pinned():
+        raise ValueError("host tensors passed to the library must be pinned (pin_memory=True)")
+    dptr = ctypes.c_void_p()
+    rc = _hip_runtime().hipHostGetDevicePointer(ctypes.byref(dptr), ctypes.c_void_p(t.data_ptr()), 0)
+    if rc != 0 or not dptr.value:
+        raise RuntimeError(f"hipHostGetDevicePointer failed ({rc}) for a pinned tensor")
+    return dptr
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return SG_F32
+    if t.dtype == torch.bfloat16:
+        return SG_BF16
+    raise TypeError(f"unsupported element type {t.dtype}")
+
+
+def _need(cond: bool, msg: str) -> None:
+    if not cond:
+        raise ValueError(msg)
+
+
+# ------------------------------------------------------------------------ score
+
+def score_workspace_size(B, L, Hq, Hkv, d, W, max_seqlen) -> int:
+    return int(load().sg_score_workspace_size(B, L, Hq, Hkv, d, W, max_seqlen))
+
+
+def sg_score(q_win, k, cu_seqlens, T, max_seqlen, Hkv, scores, ws=None, lse_in=None, k_layer_rows=None,
+             stream=None):
+    """scores[L][Hkv][T] (float32, written) from q_win [B][L][Hq][W][d] and k rows."""
+    B, L, Hq, W, d = q_win.shape
+    _need(k.dtype == q_win.dtype, "q_win and k must share a dtype")
+    _need(scores.dtype == torch.float32 and scores.numel() >= L * Hkv * T, "scores must be float32 [L][Hkv][T]")
+    _need(cu_seqlens.dtype == torch.int32 and cu_seqlens.numel() == B + 1, "cu_seqlens must be int32 [B+1]")
+    if k_layer_rows is None:
+        k_layer_rows = 0 if (k.dim() == 4 and k.shape[0] == 1 and L > 1) else Hkv * T
+    _need(k.numel() >= ((L - 1) * k_layer_rows + Hkv * T) * d, "k is smaller than its layout needs")
+    _need(lse_in is None or (lse_in.dtype == torch.float32 and lse_in.numel() >= B * L * Hq * W),
+          "lse_in must be float32 [B][L][Hq][W]")
+    rc = load().sg_score(_stream(stream), _dtype_code(q_win), B, L, Hq, Hkv, d, W, _ptr(cu_seqlens), int(T),
+                         int(max_seqlen), _ptr(q_win), _ptr(k), int(k_layer_rows), _ptr(lse_in), _ptr(scores),
+                         _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size())
+    _check("sg_score", rc)
+    return scores
+
+
+# ------------------------------------------------------------------------ topk
+
+def sg_topk(scores, cu_seqlens, T, max_seqlen, cu_k, K_total, idx, B=None, stream=None):
+    L, Hkv = scores.shape[0], scores.shape[1]
+    B = cu_seqlens.numel() - 1 if B is None else B
+    _need(scores.dtype == torch.float32 and scores.numel() >= L * Hkv * T, "scores must be float32 [L][Hkv][T]")
+    _need(cu_seqlens.numel() >= B + 1 and cu_k.numel() >= B + 1, "cu_seqlens and cu_k need B+1 entries")
+    _need(idx.dtype == torch.int32 and idx.numel() >= L * Hkv * K_total, "idx must be int32 [L][Hkv][K_total]")
+    rc = load().sg_topk(_stream(stream), B, L, Hkv, _ptr(cu_seqlens), int(T), int(max_seqlen), _ptr(cu_k),
+                        int(K_total), _ptr(scores), _ptr(idx))
+    _check("sg_topk", rc)
+    return idx
+
+
+# ------------------------------------------------------------------------ pack
+
+def pack_bytes(dtype: torch.dtype, L, Hkv, d, K_total) -> int:
+    code = SG_F32 if dtype == torch.float32 else SG_BF16
+    return int(load().sg_pack_bytes(code, L, Hkv, d, int(K_total)))
+
+
+def sg_pack(k, v, idx, cu_seqlens, T, cu_k, K_total, max_k, dst, L=None, Hkv=None, kv_layer_rows=None,
+            stream=None):
+    """Writes [K rows | V rows | idx] of every unit into ``dst`` (uint8, device or pinned host)."""
+    _need(k.dtype == v.dtype, "k and v must share a dtype")
+    L = idx.shape[0] if L is None else L
+    Hkv = idx.shape[1] if Hkv is None else Hkv
+    d = k.shape[-1]
+    B = cu_seqlens.numel() - 1
+    if kv_layer_rows is None:
+        kv_layer_rows = 0 if (k.dim() == 4 and k.shape[0] == 1 and L > 1) else Hkv * T
+    rows_needed = ((L - 1) * kv_layer_rows + Hkv * T) * d
+    _need(k.numel() >= rows_needed and v.numel() >= rows_needed, "k / v smaller than their layout needs")
+    _need(idx.dtype == torch.int32 and idx.numel() >= L * Hkv * K_total, "idx must be int32 [L][Hkv][K_total]")
+    _need(cu_k.numel() == B + 1, "cu_k must have B+1 entries")
+    rc = load().sg_pack(_stream(stream), _dtype_code(k), B, L, Hkv, d, _ptr(cu_seqlens), int(T), _ptr(cu_k),
+                        int(K_total), int(max_k), _ptr(k), _ptr(v), int(kv_layer_rows), _ptr(idx), _ptr(dst),
+                        dst.numel() * dst.element_size())
+    _check("sg_pack", rc)
+    return dst
+
+
+# ------------------------------------------------------------------------ split
+
+def sg_split(row_off, kv_index, mask, mask_off, mask_len, reorder, local, remote, n_local, n_remote,
+             out_index=None, stream=None):
+    rows = row_off.numel() - 1
+    total = kv_index.numel()
+    _need(mask.dtype == torch.int8, "mask must be int8")
+    for t in (mask_off, mask_len, n_local, n_remote):
+        _need(t.numel() >= rows, "per-row arrays need one entry per row")
+    for t in (local, remote) + ((out_index,) if out_index is not None else ()):
+        _need(t.numel() >= total, "outputs need one entry per index")
+    rc = load().sg_split(_stream(stream), rows, _ptr(row_off), int(total), _ptr(kv_index), _ptr(mask),
+                         mask.numel(), _ptr(mask_off), _ptr(mask_len), int(bool(reorder)), _ptr(out_index),
+                         _ptr(local), _ptr(remote), _ptr(n_local), _ptr(n_remote))
+    _check("sg_split", rc)
+
+
+# ------------------------------------------------------------------------ fetch
+
+def sg_fetch(row_off, total, index, n_valid, src_row_base, k_src, v_src, page_table, page_size, dst_start,
+             k_pool, v_pool, stream=None):
+    rows = row_off.numel() - 1
+    d = k_src.shape[-1]
+    _need(k_pool.dtype == k_src.dtype and v_pool.dtype == v_src.dtype, "pool and source dtypes differ")
+    max_pages = page_table.shape[-1]
+    src_rows = k_src.numel() // d
+    pool_rows = k_pool.numel() // d
+    _need(v_src.numel() >= src_rows * d and v_pool.numel() >= pool_rows * d, "v arrays smaller than k arrays")
+    _need(page_table.numel() >= rows * max_pages, "page_table must be [rows][max_pages]")
+    _need(src_row_base.dtype == torch.int64 and src_row_base.numel() >= rows, "src_row_base must be int64 [rows]")
+    _need(dst_start.numel() >= rows and (n_valid is None or n_valid.numel() >= rows), "per-row arrays too short")
+    _need(index is None or index.numel() >= total, "index shorter than total")
+    rc = load().sg_fetch(_stream(stream), _dtype_code(k_src), d, rows, _ptr(row_off), int(total), _ptr(index),
+                         _ptr(n_valid), _ptr(src_row_base), src_rows, _ptr(k_src), _ptr(v_src), _ptr(page_table),
+                         int(page_size), int(max_pages), _ptr(dst_start), _ptr(k_pool), _ptr(v_pool), pool_rows)
+    _check("sg_fetch", rc)
+
+
+# ------------------------------------------------------------------------ decode attention
+
+def decode_workspace_size(B, Hq, Hkv, d, max_pages, page_size) -> int:
+    return int(load().sg_decode_attn_workspace_size(B, Hq, Hkv, d, max_pages, page_size))
+
+
+def sg_decode_attn(q, k_pool, v_pool, page_table, n_rows, page_size, out, ws=None, scale=None, stream=None):
+    """out[B][Hq][d] (float32) = attention of q [B][Hq][d] over the paged partial set."""
+    B, Hq, d = q.shape
+    Hkv, max_pages = page_table.shape[1], page_table.shape[2]
+    _need(k_pool.dtype == q.dtype and v_pool.dtype == q.dtype, "q and pools must share a dtype")
+    _need(out.dtype == torch.float32 and out.numel() >= B * Hq * d, "out must be float32 [B][Hq][d]")
+    if scale is None:
+        scale = d ** -0.5
+    pool_rows = k_pool.numel() // d
+    _need(v_pool.numel() >= pool_rows * d, "v_pool smaller than k_pool")
+    _need(page_table.shape[0] == B and n_rows.numel() >= B * Hkv, "page_table [B][Hkv][max_pages], n_rows [B][Hkv]")
+    _need(Hq % Hkv == 0, "Hq must be a multiple of Hkv")
+    rc = load().sg_decode_attn(_stream(stream), _dtype_code(q), B, Hq, Hkv, d, float(scale), _ptr(q), _ptr(k_pool),
+                               _ptr(v_pool), pool_rows, _ptr(page_table), _ptr(n_rows), int(page_size),
+                               int(max_pages), _ptr(out), _ptr(ws),
+                               0 if ws is None else ws.numel() * ws.element_size())
+    _check("sg_decode_attn", rc)
+    return out

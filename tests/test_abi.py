@@ -1,0 +1,104 @@
+"""The C ABI: the library loads, exports every function include/smartgen.h
+declares, and rejects bad scalar arguments on the host (no GPU needed: the
+checks run before anything is enqueued)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_28150_amd import smartgen
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(sg_[a-z0-9_]+)\s*\(", text))
+    return names
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(smartgen.LIB_PATH):
+        from paper_2607_28150_amd import build
+        build.build()
+    return smartgen.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    declared = _declared()
+    assert {"sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn"} <= declared
+    for name in declared:
+        assert hasattr(lib, name), f"{name} declared but not exported"
+    assert set(smartgen.EXPORTS) == declared
+
+
+def test_version_and_status_strings(lib):
+    assert smartgen.version() == 100
+    assert lib.sg_status_str(0) == b"ok"
+    assert lib.sg_status_str(-3).startswith(b"workspace")
+
+
+def test_sizes(lib):
+    # [K | V | idx] of 2 layers x 8 heads x 819 rows of 128 bf16
+    S = 2 * 8 * 819
+    assert smartgen.pack_bytes(__import__("torch").bfloat16, 2, 8, 128, 819) == 2 * S * 256 + 4 * S
+    assert smartgen.score_workspace_size(1, 1, 8, 8, 64, 32, 2048) == 8 * 4 * 32 * 8 + 8 * 32 * 4
+    assert smartgen.decode_workspace_size(1, 32, 8, 128, 1, 16) == 0          # one split: no workspace
+    assert smartgen.decode_workspace_size(2, 32, 8, 128, 64, 16) == 2 * 8 * 4 * 4 * 130 * 4
+
+
+P = ctypes.c_void_p(16)   # never dereferenced: every call below fails validation first
+
+
+def _err(lib):
+    return lib.sg_last_error().decode()
+
+
+def test_score_rejections(lib):
+    rc = lib.sg_score(None, 1, 1, 1, 8, 8, 96, 32, P, 100, 100, P, P, 0, None, P, P, 1 << 20)
+    assert rc == smartgen.SG_EUNSUPPORTED and "head dimension" in _err(lib)
+    rc = lib.sg_score(None, 1, 1, 1, 6, 4, 64, 32, P, 100, 100, P, P, 0, None, P, P, 1 << 20)
+    assert rc == smartgen.SG_EINVAL
+    rc = lib.sg_score(None, 1, 1, 1, 64, 8, 128, 65, P, 100, 100, P, P, 0, None, P, P, 1 << 20)
+    assert rc == smartgen.SG_EUNSUPPORTED and "G*W" in _err(lib)
+    rc = lib.sg_score(None, 1, 1, 1, 8, 8, 64, 32, P, 4096, 4096, P, P, 0, None, P, P, 16)
+    assert rc == smartgen.SG_EWORKSPACE
+    rc = lib.sg_score(None, 7, 1, 1, 8, 8, 64, 32, P, 100, 100, P, P, 0, None, P, P, 1 << 20)
+    assert rc == smartgen.SG_EINVAL and "dtype" in _err(lib)
+
+
+def test_topk_rejections(lib):
+    rc = lib.sg_topk(None, 1, 1, 1, P, 100000, 70000, P, 100, P, P)
+    assert rc == smartgen.SG_EUNSUPPORTED
+    rc = lib.sg_topk(None, 0, 1, 1, P, 100, 100, P, 10, P, P)
+    assert rc == smartgen.SG_EINVAL
+    assert lib.sg_topk(None, 1, 1, 1, P, 100, 100, P, 0, P, P) == smartgen.SG_OK   # nothing to select
+
+
+def test_pack_rejections(lib):
+    rc = lib.sg_pack(None, 1, 1, 1, 1, 128, P, 100, P, 10, 10, P, P, 100, P, P, 100)
+    assert rc == smartgen.SG_EWORKSPACE
+    rc = lib.sg_pack(None, 1, 1, 1, 1, 80, P, 100, P, 10, 10, P, P, 100, P, P, 1 << 20)
+    assert rc == smartgen.SG_EUNSUPPORTED
+    rc = lib.sg_pack(None, 1, 1, 1, 1, 128, P, 100, P, 10, 10, ctypes.c_void_p(18), P, 100, P, P, 1 << 20)
+    assert rc == smartgen.SG_EINVAL and "aligned" in _err(lib)
+
+
+def test_split_fetch_decode_rejections(lib):
+    assert lib.sg_split(None, -1, P, 0, P, P, 0, P, P, 0, None, P, P, P, P) == smartgen.SG_EINVAL
+    assert lib.sg_split(None, 2, P, 5, P, P, 10, P, P, 1, None, P, P, P, P) == smartgen.SG_EINVAL
+    assert lib.sg_fetch(None, 1, 128, 1, P, 5, P, None, P, 10, P, P, P, 0, 1, P, P, P, 10) == smartgen.SG_EINVAL
+    rc = lib.sg_decode_attn(None, 1, 1, 6, 4, 128, 0.1, P, P, P, 10, P, P, 16, 4, P, None, 0)
+    assert rc == smartgen.SG_EINVAL
+    rc = lib.sg_decode_attn(None, 1, 1, 8, 8, 128, -1.0, P, P, P, 10, P, P, 16, 4, P, None, 0)
+    assert rc == smartgen.SG_EINVAL
+    rc = lib.sg_decode_attn(None, 1, 2, 32, 8, 128, 0.1, P, P, P, 10, P, P, 16, 64, P, None, 0)
+    assert rc == smartgen.SG_EWORKSPACE
+    rc = lib.sg_decode_attn(None, 1, 1, 24, 8, 128, 0.1, P, P, P, 10, P, P, 16, 4, P, None, 0)
+    assert rc == smartgen.SG_EUNSUPPORTED       # group size 3
