@@ -46,7 +46,8 @@ def parse():
     p.add_argument("--workload", default="llama8b_8k")
     p.add_argument("--decode-steps", type=int, default=None, help="decode steps per step (default: workload's)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-layers", type=int, default=2, help="layers of the workload the oracle is timed on")
+    p.add_argument("--cpu-layers", type=int, default=0, help="layers the oracle is timed on (0 = all)")
+    p.add_argument("--cpu-seconds", type=float, default=10.0, help="repeat the oracle sample to at least this long")
     return p.parse_args()
 
 
@@ -123,29 +124,30 @@ def main():
     setup_s = time.time() - t0
 
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    # timed ops of one step: score, topk, pack, then per decode step split and decode
-    def step(r, rec):
-        e = [ev() for _ in range(4)]
-        e[0].record()
+    decode = sg.DecodeCall(qdec[0], pools[0][0], pools[0][1], page_table, n_rows, P, out, ws=ws_dec)
+    ev_pool = [[ev() for _ in range(5 + nsteps_dec + 1)] for _ in range(args.steps)]
+
+    # one step: score, top-k, pack; Algorithm 1 on the step's KV index (the
+    # selected set, all local in this workload, so once per request); then the
+    # decode steps, each one attention launch over all layers
+    def step(r, e):
+        if e is None:
+            e = [None] * (6 + nsteps_dec)
+        rec = lambda i: e[i].record() if e[i] is not None else None  # noqa: E731
+        rec(0)
         sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score)
-        e[1].record()
+        rec(1)
         sg.sg_topk(scores, cus, T, N, cuk, K_total, idx)
-        e[2].record()
+        rec(2)
         sg.sg_pack(pre["k"], pre["v"], idx, cus, T, cuk, K_total, K_total, bufs[r % reps])
-        e[3].record()
-        dec = []
+        rec(3)
+        sg.sg_split(row_off, idx.view(-1), mask.view(-1), mask_off, mask_len, 1, sp_local, sp_remote, sp_nl,
+                    sp_nr, out_index=sp_order)
+        rec(4)
         for s in range(nsteps_dec):
             kp, vp = pools[(r + s) % reps]
-            a, b_, c = ev(), ev(), ev()
-            a.record()
-            sg.sg_split(row_off, idx.view(-1), mask.view(-1), mask_off, mask_len, 1, sp_local, sp_remote, sp_nl,
-                        sp_nr, out_index=sp_order)
-            b_.record()
-            sg.sg_decode_attn(qdec[s], kp, vp, page_table, n_rows, P, out, ws=ws_dec)
-            c.record()
-            dec.append((a, b_, c))
-        if rec is not None:
-            rec.append((e, dec))
+            decode(qdec[s], kp, vp, out)
+            rec(5 + s)
 
     # every replica holds a packed buffer before timing
     for r in range(reps):
@@ -154,22 +156,21 @@ def main():
         step(w, None)
     torch.cuda.synchronize()
 
-    recs = []
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k in range(args.steps):
-        step(k, recs)
+        step(k, ev_pool[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
 
-    # ------------------------------------------------------------- per-op times
+    # ------------------------------------------------------------- per-op times (HIP events on the launch stream)
     def ms(a, b):
         return a.elapsed_time(b)
-    t_score = np.mean([ms(e[0], e[1]) for e, _ in recs])
-    t_topk = np.mean([ms(e[1], e[2]) for e, _ in recs])
-    t_pack = np.mean([ms(e[2], e[3]) for e, _ in recs])
-    t_split = np.mean([ms(a, b_) for _, dec in recs for a, b_, _c in dec])
-    t_dec = np.mean([ms(b_, c) for _, dec in recs for _a, b_, c in dec])
+    t_score = np.mean([ms(e[0], e[1]) for e in ev_pool])
+    t_topk = np.mean([ms(e[1], e[2]) for e in ev_pool])
+    t_pack = np.mean([ms(e[2], e[3]) for e in ev_pool])
+    t_split = np.mean([ms(e[3], e[4]) for e in ev_pool])
+    t_dec = np.mean([ms(e[4 + s], e[5 + s]) for e in ev_pool for s in range(nsteps_dec)])
     ms_per_step = wall * 1e3 / args.steps
 
     kv_bytes = 2 * L * Hkv * T * d * esize                       # the whole KV cache
@@ -222,15 +223,16 @@ def main():
 
     # ------------------------------------------------------------- oracle on the host cores
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, pre, bud, args.cpu_layers)
+        line["cpu_baseline"] = cpu_baseline(cfg, pre, bud, args.cpu_layers or cfg.L, args.cpu_seconds)
         if line["cpu_baseline"].get("value"):
             line["gpu_over_cpu"] = round(value / line["cpu_baseline"]["value"], 1)
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(cfg, pre, bud, layers):
+def cpu_baseline(cfg, pre, bud, layers, min_seconds):
     """The oracle's select+pack (score, top-k, pack) timed on a bounded sample:
-    the first ``layers`` layers of the same request, all KV heads."""
+    the first ``layers`` layers of the same request, all KV heads, repeated
+    until at least ``min_seconds`` have passed."""
     import numpy as np
 
     import oracle
@@ -244,11 +246,16 @@ def cpu_baseline(cfg, pre, bud, layers):
     vraw = pre["v"][:layers].cpu().contiguous().view(__import__("torch").int16).numpy().view(np.uint16)
     units = layers * cfg.Hkv
     threads = oracle.threads()
+    reps = 0
     t0 = time.perf_counter()
-    s = oracle.score(q, k, pre["cu_seqlens"], cfg.Hkv)
-    idx = oracle.topk(s.astype(np.float32), pre["cu_seqlens"], bud["cu_k"])
-    oracle.pack(kraw, vraw, idx, pre["cu_seqlens"], bud["cu_k"])
-    dt = time.perf_counter() - t0
+    while True:
+        s = oracle.score(q, k, pre["cu_seqlens"], cfg.Hkv)
+        idx = oracle.topk(s.astype(np.float32), pre["cu_seqlens"], bud["cu_k"])
+        oracle.pack(kraw, vraw, idx, pre["cu_seqlens"], bud["cu_k"])
+        reps += 1
+        if time.perf_counter() - t0 >= min_seconds:
+            break
+    dt = (time.perf_counter() - t0) / reps
     esize = 2 if cfg.dtype == "bf16" else 4
     kv_bytes = 2 * units * pre["T"] * cfg.d * esize
     cpu = "unknown"
@@ -261,9 +268,9 @@ def cpu_baseline(cfg, pre, bud, layers):
     except OSError:
         pass
     return {"value": round(kv_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": min(threads, units),
-            "kind": "oracle", "seconds": round(dt, 2),
+            "kind": "oracle", "seconds_per_pass": round(dt, 3), "passes": reps,
             "sample": f"score+topk+pack of layers 0..{layers - 1} ({units} of {cfg.L * cfg.Hkv} units), "
-                      f"same request, fp64 C oracle with OpenMP over units",
+                      f"same request, fp64 C oracle with OpenMP over units, repeated {reps}x",
             "cpu_model": cpu, "host": platform.node()}
 
 

@@ -1,0 +1,124 @@
+// Shared pieces of the score kernels: MFMA operand fragments, the K-tile
+// stager and the query-fragment loader (gfx950).
+#pragma once
+
+#include "sg_internal.h"
+
+namespace sg {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int SC_TK = 64;          // keys per tile
+constexpr int SC_TPC = 8;          // tiles per chunk
+constexpr int SC_CHUNK = SC_TK * SC_TPC;
+constexpr int SC_MAXR = 512;       // rows per unit (G * W): at most 8 wavefronts
+constexpr float SC_LOG2E = 1.4426950408889634f;
+constexpr float SC_LN2 = 0.6931471805599453f;
+
+template <typename T, int D>
+struct Frag;
+
+template <int D>
+struct Frag<uint16_t, D> {  // bfloat16 operands, K = 32 per instruction
+    static constexpr int KSTEPS = D / 32;
+    static constexpr int ROWB = D * 2 + 16;  // padded LDS row bytes
+    using A = bf16x8;
+    __device__ static A zero() { return A{}; }
+    __device__ static A load_global(const uint16_t *row, int ks, int lane) {
+        return *reinterpret_cast<const A *>(row + ks * 32 + 8 * (lane / 16));
+    }
+    __device__ static A load_lds(const char *tile, int key, int ks, int lane) {
+        return *reinterpret_cast<const A *>(tile + key * ROWB + (ks * 32 + 8 * (lane / 16)) * 2);
+    }
+    __device__ static f32x4 mma(const A &a, const A &b, const f32x4 &c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <int D>
+struct Frag<float, D> {  // fp32 operands, K = 4 per instruction
+    static constexpr int KSTEPS = D / 4;
+    static constexpr int ROWB = D * 4 + 16;
+    using A = float;
+    __device__ static A zero() { return 0.f; }
+    __device__ static A load_global(const float *row, int ks, int lane) { return row[ks * 4 + lane / 16]; }
+    __device__ static A load_lds(const char *tile, int key, int ks, int lane) {
+        return *reinterpret_cast<const float *>(tile + key * ROWB + (ks * 4 + lane / 16) * 4);
+    }
+    __device__ static f32x4 mma(const A &a, const A &b, const f32x4 &c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+};
+
+struct UnitGeom {
+    int b, l, h;
+    int64_t s0, N;
+};
+
+__device__ __forceinline__ UnitGeom unit_geom(int64_t u, int B, int Hkv, const int32_t *cu_seqlens, int64_t T) {
+    UnitGeom g;
+    g.b = (int)(u % B);
+    const int64_t lh = u / B;
+    g.l = (int)(lh / Hkv);
+    g.h = (int)(lh % Hkv);
+    const int64_t s0 = cu_seqlens[g.b], s1 = cu_seqlens[g.b + 1];
+    g.s0 = s0;
+    g.N = (s0 >= 0 && s1 >= s0 && s1 <= T) ? s1 - s0 : 0;
+    return g;
+}
+
+// Stage one 64-key tile of K (rows [key0, key0+64) of the unit) into LDS.
+template <typename T, int D>
+__device__ __forceinline__ void stage_tile(char *tile, const T *kunit, int64_t key0, int64_t N) {
+    constexpr int ESZ = sizeof(T);
+    constexpr int VPR = D * ESZ / 16;  // 16-byte vectors per key row
+    for (int i = threadIdx.x; i < SC_TK * VPR; i += blockDim.x) {
+        const int key = i / VPR, v = i % VPR;
+        v4u x = v4u{0u, 0u, 0u, 0u};
+        if (key0 + key < N) x = reinterpret_cast<const v4u *>(kunit + (key0 + key) * D)[v];
+        *reinterpret_cast<v4u *>(tile + key * Frag<T, D>::ROWB + v * 16) = x;
+    }
+}
+
+// acc[rb][kb] = Q(rows of row-block rb) . K(tile keys of key-block kb)
+template <typename T, int D>
+__device__ __forceinline__ void tile_mma(const typename Frag<T, D>::A (&qa)[4][Frag<T, D>::KSTEPS],
+                                         const char *tile, int lane, f32x4 (&acc)[4][4]) {
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) acc[rb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < Frag<T, D>::KSTEPS; ++ks) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            const auto bf = Frag<T, D>::load_lds(tile, kb * 16 + lane % 16, ks, lane);
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) acc[rb][kb] = Frag<T, D>::mma(qa[rb][ks], bf, acc[rb][kb]);
+        }
+    }
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void load_q(const T *qunit, int R, int wave, int lane,
+                                       typename Frag<T, D>::A (&qa)[4][Frag<T, D>::KSTEPS]) {
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+        const int r = wave * 64 + rb * 16 + lane % 16;
+#pragma unroll
+        for (int ks = 0; ks < Frag<T, D>::KSTEPS; ++ks)
+            qa[rb][ks] = r < R ? Frag<T, D>::load_global(qunit + (int64_t)r * D, ks, lane) : Frag<T, D>::zero();
+    }
+}
+
+
+// dispatcher of the single-pass (fused) score kernel; returns SG_EUNSUPPORTED
+// when the fused path cannot run for these sizes (the caller then falls back
+// to the two-pass kernels)
+size_t score_fused_workspace(int B, int L, int Hq, int Hkv, int W, int max_seqlen);
+int launch_score_fused(hipStream_t s, sg_dtype dt, int d, int B, int L, int Hq, int Hkv, int W,
+                       const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *q_win, const void *k,
+                       int64_t k_layer_rows, float *scores, void *ws, size_t ws_bytes);
+
+}  // namespace sg

@@ -257,3 +257,35 @@ def sg_decode_attn(q, k_pool, v_pool, page_table, n_rows, page_size, out, ws=Non
                                0 if ws is None else ws.numel() * ws.element_size())
     _check("sg_decode_attn", rc)
     return out
+
+
+class DecodeCall:
+    """A prepared sg_decode_attn call for a fixed geometry: per call only the
+    query, the pools and the output change.  Cuts host overhead in decode loops
+    (the same marshalling as sg_decode_attn, done once)."""
+
+    def __init__(self, q, k_pool, v_pool, page_table, n_rows, page_size, out, ws=None, scale=None, stream=None):
+        sg_decode_attn(q, k_pool, v_pool, page_table, n_rows, page_size, out, ws=ws, scale=scale, stream=stream)
+        B, Hq, d = q.shape
+        self._lib = load()
+        self._keep = (page_table, n_rows, ws)
+        self._dt = _dtype_code(q)
+        self._shape = (B, Hq, page_table.shape[1], d)
+        self._scale = float(d ** -0.5 if scale is None else scale)
+        self._pt, self._nr = _ptr(page_table), _ptr(n_rows)
+        self._geom = (int(page_size), int(page_table.shape[2]))
+        self._ws = _ptr(ws)
+        self._wsb = 0 if ws is None else ws.numel() * ws.element_size()
+        self._stream = _stream(stream)
+        self._pool_rows = k_pool.numel() // d
+        self._numel = (q.numel(), k_pool.numel(), out.numel())
+
+    def __call__(self, q, k_pool, v_pool, out):
+        _need(q.numel() == self._numel[0] and k_pool.numel() == self._numel[1] and out.numel() == self._numel[2]
+              and v_pool.numel() == self._numel[1], "prepared decode call used with other shapes")
+        B, Hq, Hkv, d = self._shape
+        rc = self._lib.sg_decode_attn(self._stream, self._dt, B, Hq, Hkv, d, self._scale, q.data_ptr(),
+                                      k_pool.data_ptr(), v_pool.data_ptr(), self._pool_rows, self._pt, self._nr,
+                                      self._geom[0], self._geom[1], out.data_ptr(), self._ws, self._wsb)
+        _check("sg_decode_attn", rc)
+

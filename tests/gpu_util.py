@@ -32,7 +32,7 @@ def assert_scores_close(gpu: np.ndarray, ref: np.ndarray, rtol=1e-3, floor=1e-30
     """|g - o| <= rtol * |o| + floor, element by element (scores are sums of positive terms)."""
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
-    bad = np.abs(gpu - ref) > rtol * np.abs(ref) + floor
+    bad = ~(np.abs(gpu - ref) <= rtol * np.abs(ref) + floor)     # NaN counts as a mismatch
     if bad.any():
         i = np.argwhere(bad)[:5]
         raise AssertionError(f"{int(bad.sum())} scores out of tolerance; first {i.tolist()}: "

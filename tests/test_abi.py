@@ -50,7 +50,7 @@ def test_sizes(lib):
     assert smartgen.pack_bytes(__import__("torch").bfloat16, 2, 8, 128, 819) == 2 * S * 256 + 4 * S
     assert smartgen.score_workspace_size(1, 1, 8, 8, 64, 32, 2048) == 8 * 4 * 32 * 8 + 8 * 32 * 4
     assert smartgen.decode_workspace_size(1, 32, 8, 128, 1, 16) == 0          # one split: no workspace
-    assert smartgen.decode_workspace_size(2, 32, 8, 128, 64, 16) == 2 * 8 * 4 * 4 * 130 * 4
+    assert smartgen.decode_workspace_size(2, 32, 8, 128, 64, 16) == 2 * 8 * 4 * 4 * 130 * 4   # <= 4 splits of 256 rows
 
 
 P = ctypes.c_void_p(16)   # never dereferenced: every call below fails validation first

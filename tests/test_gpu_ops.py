@@ -220,6 +220,8 @@ def _paged_set(g, B, Hkv, d, nmax, P, td, empty_some=True):
     ("f32", 64, 1, 204, 16, 2),
     ("f32", 128, 2, 1000, 1, 2),
     ("bf16", 128, 4, 256, 16, 4),              # exactly one split
+    ("bf16", 128, 4, 819, 16, 128),            # >= 256 units: one split, several tiles per wavefront
+    ("bf16", 128, 8, 1700, 16, 128),
 ])
 def test_decode_parity(gpu_lib, dtype, d, G, nmax, P, B):
     g = np.random.default_rng(nmax + G + d + P)
