@@ -10,7 +10,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int SC_TK = 64;          // keys per tile
-constexpr int SC_TPC = 8;          // tiles per chunk
+constexpr int SC_TPC = 16;         // tiles per chunk
 constexpr int SC_CHUNK = SC_TK * SC_TPC;
 constexpr int SC_MAXR = 512;       // rows per unit (G * W): at most 8 wavefronts
 constexpr float SC_LOG2E = 1.4426950408889634f;
@@ -51,6 +51,24 @@ struct Frag<float, D> {  // fp32 operands, K = 4 per instruction
     }
 };
 
+// Workgroup -> (unit, chunk).  Workgroups are dealt to the 8 XCDs round-robin
+// by their linear id; this mapping gives the chunks of one unit consecutive
+// slots on one XCD, so the unit's queries are fetched into that XCD's L2 once.
+__device__ __forceinline__ void unit_chunk(int64_t units, int nchunk, int64_t &u, int &c) {
+    const int64_t id = blockIdx.x;
+    const int64_t total = units * nchunk;
+    const int64_t full = total / 8 * 8;        // ids in the XCD-interleaved part
+    if (id < full) {
+        const int64_t xcd = id % 8, j = id / 8;          // j-th workgroup of this XCD
+        const int64_t lin = xcd * (full / 8) + j;       // contiguous range per XCD
+        u = lin / nchunk;
+        c = (int)(lin % nchunk);
+    } else {
+        u = id / nchunk;
+        c = (int)(id % nchunk);
+    }
+}
+
 struct UnitGeom {
     int b, l, h;
     int64_t s0, N;
@@ -81,16 +99,19 @@ __device__ __forceinline__ void stage_tile(char *tile, const T *kunit, int64_t k
     }
 }
 
-// acc[rb][kb] = Q(rows of row-block rb) . K(tile keys of key-block kb)
+// acc[rb][kb] = Q(rows of row-block rb) . K(tile keys of key-block kb); the
+// first k-step multiplies with a zero accumulator operand (no separate clear)
 template <typename T, int D>
 __device__ __forceinline__ void tile_mma(const typename Frag<T, D>::A (&qa)[4][Frag<T, D>::KSTEPS],
                                          const char *tile, int lane, f32x4 (&acc)[4][4]) {
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+    for (int kb = 0; kb < 4; ++kb) {
+        const auto bf = Frag<T, D>::load_lds(tile, kb * 16 + lane % 16, 0, lane);
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) acc[rb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int rb = 0; rb < 4; ++rb) acc[rb][kb] = Frag<T, D>::mma(qa[rb][0], bf, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
 #pragma unroll
-    for (int ks = 0; ks < Frag<T, D>::KSTEPS; ++ks) {
+    for (int ks = 1; ks < Frag<T, D>::KSTEPS; ++ks) {
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
             const auto bf = Frag<T, D>::load_lds(tile, kb * 16 + lane % 16, ks, lane);
@@ -112,13 +133,5 @@ __device__ __forceinline__ void load_q(const T *qunit, int R, int wave, int lane
     }
 }
 
-
-// dispatcher of the single-pass (fused) score kernel; returns SG_EUNSUPPORTED
-// when the fused path cannot run for these sizes (the caller then falls back
-// to the two-pass kernels)
-size_t score_fused_workspace(int B, int L, int Hq, int Hkv, int W, int max_seqlen);
-int launch_score_fused(hipStream_t s, sg_dtype dt, int d, int B, int L, int Hq, int Hkv, int W,
-                       const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *q_win, const void *k,
-                       int64_t k_layer_rows, float *scores, void *ws, size_t ws_bytes);
 
 }  // namespace sg
