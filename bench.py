@@ -34,6 +34,10 @@ if _ROOT not in sys.path:
     sys.path.insert(0, _ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# the counter summary that gives the decode kernel's measured HBM traffic, and
+# the sources whose hash it records (a changed kernel makes the figure stale)
+TRAFFIC_SUMMARY = os.path.join(_ROOT, "profiles", "all_kernels.llama8b_8k.hbm_traffic.md")
+TRAFFIC_SOURCES = ("paper_2607_28150_amd/csrc/decode_attn.hip", "paper_2607_28150_amd/csrc/sg_internal.h")
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 
@@ -48,6 +52,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-layers", type=int, default=0, help="layers the oracle is timed on (0 = all)")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="repeat the oracle sample to at least this long")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run a plain device copy of MIB MiB three times (counter calibration) and exit")
     return p.parse_args()
 
 
@@ -60,6 +66,17 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        a = torch.ones(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}), flush=True)
+        return
 
     from datagen import inputs
     from datagen.configs import get
@@ -125,14 +142,16 @@ def main():
 
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     decode = sg.DecodeCall(qdec[0], pools[0][0], pools[0][1], page_table, n_rows, P, out, ws=ws_dec)
-    ev_pool = [[ev() for _ in range(5 + nsteps_dec + 1)] for _ in range(args.steps)]
+    ev_pool = [[ev() for _ in range(6)] for _ in range(args.steps)]
 
     # one step: score, top-k, pack; Algorithm 1 on the step's KV index (the
     # selected set, all local in this workload, so once per request); then the
-    # decode steps, each one attention launch over all layers
+    # decode steps, each one attention launch over all layers.  The decode
+    # launches run back to back between two events (an event between every
+    # launch would add its own marker to each measured interval).
     def step(r, e):
         if e is None:
-            e = [None] * (6 + nsteps_dec)
+            e = [None] * 6
         rec = lambda i: e[i].record() if e[i] is not None else None  # noqa: E731
         rec(0)
         sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score)
@@ -147,7 +166,7 @@ def main():
         for s in range(nsteps_dec):
             kp, vp = pools[(r + s) % reps]
             decode(qdec[s], kp, vp, out)
-            rec(5 + s)
+        rec(5)
 
     # every replica holds a packed buffer before timing
     for r in range(reps):
@@ -170,7 +189,7 @@ def main():
     t_topk = np.mean([ms(e[1], e[2]) for e in ev_pool])
     t_pack = np.mean([ms(e[2], e[3]) for e in ev_pool])
     t_split = np.mean([ms(e[3], e[4]) for e in ev_pool])
-    t_dec = np.mean([ms(e[4 + s], e[5 + s]) for e in ev_pool for s in range(nsteps_dec)])
+    t_dec = np.mean([ms(e[4], e[5]) for e in ev_pool]) / nsteps_dec
     ms_per_step = wall * 1e3 / args.steps
 
     kv_bytes = 2 * L * Hkv * T * d * esize                       # the whole KV cache
@@ -216,7 +235,8 @@ def main():
         "decode_tokens_per_s": round(tokens_per_s, 1),
         "roofline": {"kernel": "sg_decode_attn", "bound": "hbm", "achieved": round(dec_gbs, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_launch": dec_bytes, "avg_launch_ms": round(t_dec, 5)},
+                     "traffic": measured_traffic(), "bytes_per_launch": dec_bytes,
+                     "avg_launch_ms": round(t_dec, 5)},
         "ops": ops,
         "setup_s": round(setup_s, 2),
     }
@@ -227,6 +247,32 @@ def main():
         if line["cpu_baseline"].get("value"):
             line["gpu_over_cpu"] = round(value / line["cpu_baseline"]["value"], 1)
     print(json.dumps(line), flush=True)
+
+
+def sources_sha256(paths) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(_ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy's reading), or None
+    when the summary is missing or the kernel sources changed since."""
+    import re
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            text = f.read()
+    except OSError:
+        return None
+    h = re.search(r"^kernel_sources_sha256:\s*([0-9a-f]{64})\s*$", text, re.M)
+    t = re.search(r"^traffic_bytes_per_launch:\s*([0-9]+)\s*$", text, re.M)
+    if not h or not t or h.group(1) != sources_sha256(TRAFFIC_SOURCES):
+        return None
+    return int(t.group(1))
 
 
 def cpu_baseline(cfg, pre, bud, layers, min_seconds):

@@ -6,7 +6,7 @@
 // the causal limit j <= position(row).  The row normaliser (log-sum-exp) is
 // needed before any column can be summed, so the contraction runs twice:
 //
-//   A  stats  : per (unit, 512-key chunk) the per-row (max, sum exp) of the
+//   A  stats  : per (unit, 1024-key chunk) the per-row (max, sum exp) of the
 //               chunk's logits;
 //   B  merge  : per unit, merge the chunk statistics into each row's LSE;
 //   C  colsum : recompute the logits, p = exp(z - LSE), and sum p over the R
