@@ -6,306 +6,489 @@
 // the causal limit j <= position(row).  The row normaliser (log-sum-exp) is
 // needed before any column can be summed, so the contraction runs twice:
 //
-//   A  stats  : per (unit, 1024-key chunk) the per-row (max, sum exp) of the
-//               chunk's logits;
-//   B  merge  : per unit, merge the chunk statistics into each row's LSE;
-//   C  colsum : recompute the logits, p = exp(z - LSE), and sum p over the R
-//               rows for every key of the chunk.
+//   stats  : per (unit, 2048-key chunk) the per-row (reference, sum exp) of
+//            the chunk's logits;
+//   colsum : merge the chunk statistics into each row's LSE, recompute the
+//            logits, p = exp(z - LSE), and sum p over the R rows for every key.
 //
 // When the caller passes the LSE (a prefill flash attention produces it) only
-// C runs.  A and C share one tile engine: a workgroup of ceil(R/64)
-// wavefronts keeps its 64 query rows per wavefront in registers as MFMA A
-// fragments; 64-key tiles of K are staged through LDS (rows padded by 16
-// bytes so the 16 lanes reading one fragment column hit distinct banks) and
-// every wavefront multiplies its rows against the tile with
-// v_mfma_f32_16x16x32_bf16 (bf16) or v_mfma_f32_16x16x4_f32 (fp32), fp32
-// accumulation.  Exponentials use exp2 with log2(e)/sqrt(d) folded into one
-// multiply.  All reductions run in a fixed order: results are deterministic.
+// colsum runs.
+//
+// Both passes use one engine.  A workgroup owns one (unit, chunk) and has one
+// wavefront per 64 query rows; each wavefront keeps its rows in registers as
+// MFMA operand fragments.  The chunk's keys stream through LDS in tiles of 128
+// (bf16) or 64 (fp32) keys, double buffered: direct global->LDS loads of the
+// next tile run while every wavefront multiplies its rows against the current
+// one with v_mfma_f32_32x32x16_bf16 (bf16) or v_mfma_f32_16x16x4_f32 (fp32),
+// fp32 accumulation; one workgroup barrier per tile.  Within a tile the
+// (key block, row block) products are software pipelined: the MFMAs of the
+// next block and the LDS reads of the block after are issued next to the
+// exponentials of the current one.
+//
+//   stats computes C = K Q^T: a lane's results of a block belong to one query
+//   row, so the row's (reference, sum) stays in the lane.  Terms are summed
+//   against the current reference (initially 0); only when a block's terms
+//   grow past 2^64 of it, or the sum stays below 2^-60 of it (and on the
+//   masked tiles at the end of the prompt), the row takes a new reference from
+//   the block's exact max.
+//   colsum computes C = Q K^T: a lane's results of a block belong to one key;
+//   the wavefronts' partial column sums meet in LDS once per tile.
+//
+// Exponentials use exp2 with log2(e)/sqrt(d) folded into one multiply.  All
+// reductions run in a fixed order: results are deterministic.
+#include <algorithm>
+#include <type_traits>
+
 #include "score_common.h"
 
 namespace sg {
 
-// Double-buffered staging of 64-key K tiles: the next tile's vectors are
-// loaded into registers while the current tile is multiplied, then written
-// to the other LDS buffer; one workgroup barrier per tile.
-template <typename T, int D, int NW>
-struct Stager {
-    static constexpr int VPR = D * (int)sizeof(T) / 16;      // 16-byte vectors per key row
-    static constexpr int NV = SC_TK * VPR;                   // vectors per tile
-    static constexpr int PF = (NV + 64 * NW - 1) / (64 * NW);
-    v4u r[PF];
-    __device__ __forceinline__ void load(const T *kunit, int key0, int N) {
+template <typename T, int D>
+using TA = typename MT<T, D>::A;
+template <typename T, int D>
+using TC = typename MT<T, D>::C;
+
+// The wavefront's 64 query rows (rows >= R are zero) as operand fragments.
+template <typename T, int D>
+struct QFrags {
+    static constexpr int NRB = 64 / MT<T, D>::BM;     // row blocks per wavefront
+    TA<T, D> f[NRB][MT<T, D>::KS];
+    __device__ __forceinline__ void load(const T *qunit, int R, int wave, int lane) {
+        using M = MT<T, D>;
 #pragma unroll
-        for (int j = 0; j < PF; ++j) {
-            const int i = (int)threadIdx.x + j * 64 * NW;
-            r[j] = v4u{0u, 0u, 0u, 0u};
-            if (i < NV && key0 + i / VPR < N)
-                r[j] = reinterpret_cast<const v4u *>(kunit + (int64_t)(key0 + i / VPR) * D)[i % VPR];
-        }
-    }
-    __device__ __forceinline__ void store(char *tile) const {
+        for (int rb = 0; rb < NRB; ++rb) {
+            const int row = wave * 64 + rb * M::BM + lane % M::BM;
+            const T *p = qunit + (int64_t)min(row, R - 1) * D;
 #pragma unroll
-        for (int j = 0; j < PF; ++j) {
-            const int i = (int)threadIdx.x + j * 64 * NW;
-            if (i < NV) *reinterpret_cast<v4u *>(tile + (i / VPR) * Frag<T, D>::ROWB + (i % VPR) * 16) = r[j];
+            for (int ks = 0; ks < M::KS; ++ks) {
+                const TA<T, D> x = M::load_global(p, ks, lane);
+                f[rb][ks] = row < R ? x : TA<T, D>{};
+            }
         }
     }
 };
 
-// The two passes share one tile engine.  For every 64-key tile of the
-// workgroup's key chunk it produces acc[rb][kb] = Q(rows of row-block rb) .
-// K(keys of key-block kb) for the wavefront's 64 rows and hands it to
-// `on_tile(acc, key0, full, t)`; `full` means every row may see every key of
-// the tile (no causal or end-of-prompt masking needed).  After the tile's
-// workgroup barrier it calls `after_barrier(key0, t)`.
-template <typename T, int D, int NW, typename OnTile, typename After>
-__device__ __forceinline__ void for_each_tile(const T *kunit, int N, int W, int key_begin, int key_end,
-                                              char *tiles, const typename Frag<T, D>::A (&qa)[4][Frag<T, D>::KSTEPS],
-                                              int lane, OnTile &&on_tile, After &&after_barrier) {
-    constexpr int TB = SC_TK * Frag<T, D>::ROWB;
-    Stager<T, D, NW> st;
-    st.load(kunit, key_begin, N);
-    st.store(tiles);
-    __syncthreads();
-    int buf = 0, t = 0;
-    for (int key0 = key_begin; key0 < key_end; key0 += SC_TK, ++t) {
-        const bool more = key0 + SC_TK < key_end;
-        if (more) st.load(kunit, key0 + SC_TK, N);
-        f32x4 acc[4][4];
-        tile_mma<T, D>(qa, tiles + buf * TB, lane, acc);
-        on_tile(acc, key0, key0 + SC_TK - 1 <= N - W, t);
-        if (more) st.store(tiles + (buf ^ 1) * TB);
-        __syncthreads();
-        after_barrier(key0, t);
-        buf ^= 1;
+// One (key block, row block) product over the whole contraction.  KEY_ROWS:
+// C[key][row] (stats), else C[row][key] (colsum).
+template <typename T, int D, bool KEY_ROWS>
+__device__ __forceinline__ TC<T, D> block_mma(const TA<T, D> (&kf)[MT<T, D>::KS], const TA<T, D> (&qf)[MT<T, D>::KS]) {
+    using M = MT<T, D>;
+    TC<T, D> acc = KEY_ROWS ? M::mma(kf[0], qf[0], M::zero()) : M::mma(qf[0], kf[0], M::zero());
+#pragma unroll
+    for (int ks = 1; ks < M::KS; ++ks) acc = KEY_ROWS ? M::mma(kf[ks], qf[ks], acc) : M::mma(qf[ks], kf[ks], acc);
+    return acc;
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void load_kf(const char *buf, int kb, int lane, TA<T, D> (&kf)[MT<T, D>::KS]) {
+#pragma unroll
+    for (int ks = 0; ks < MT<T, D>::KS; ++ks) kf[ks] = KTile<T, D>::frag(buf, kb, ks, lane);
+}
+
+// One block product, accumulated onto c0, whose key fragments are refilled,
+// right behind each MFMA that reads them, with key block `next` of the tile
+// (when next >= 0).
+template <typename T, int D, bool KEY_ROWS>
+__device__ __forceinline__ TC<T, D> block_mma_refill(const char *buf, int next, int lane, const TC<T, D> &c0,
+                                                     TA<T, D> (&kf)[MT<T, D>::KS],
+                                                     const TA<T, D> (&qf)[MT<T, D>::KS]) {
+    using M = MT<T, D>;
+    TC<T, D> acc = c0;
+#pragma unroll
+    for (int ks = 0; ks < M::KS; ++ks) {
+        acc = KEY_ROWS ? M::mma(kf[ks], qf[ks], acc) : M::mma(qf[ks], kf[ks], acc);
+        if (next >= 0) kf[ks] = KTile<T, D>::frag(buf, next, ks, lane);
+    }
+    return acc;
+}
+
+// All (key block, row block) products of the tile in `buf`, key block major.
+// Software pipelined: step b issues the MFMAs of block b + 1 and then hands
+// block b to valu(acc, kb, rb).  One set of key fragments: the last block of
+// a key block refills them with the next key block's behind its own MFMAs.
+// Scheduling barriers keep the compiler from hoisting later loads, and group
+// barriers interleave each MFMA with a share of the vector work.
+template <typename T, int D, bool KEY_ROWS, typename F>
+__device__ __forceinline__ void tile_sweep(const char *buf, const QFrags<T, D> &q,
+                                           const TC<T, D> (&c0)[QFrags<T, D>::NRB], int lane, F &&valu) {
+    constexpr int NKB = KTile<T, D>::NKB, NRB = QFrags<T, D>::NRB, NB = NKB * NRB;
+    // a block's vector work is about 3 instructions per output value
+    constexpr int VALU_PER_MFMA = (3 * MT<T, D>::NV + MT<T, D>::KS - 1) / MT<T, D>::KS;
+    TA<T, D> kf[MT<T, D>::KS];
+    load_kf<T, D>(buf, 0, lane, kf);
+    TC<T, D> acc = block_mma_refill<T, D, KEY_ROWS>(buf, NRB == 1 && NKB > 1 ? 1 : -1, lane, c0[0], kf, q.f[0]), nacc;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (b + 1 < NB) {
+            const int nkb = (b + 1) / NRB, nrb = (b + 1) % NRB;
+            const int refill = nrb == NRB - 1 && nkb + 1 < NKB ? nkb + 1 : -1;
+            nacc = block_mma_refill<T, D, KEY_ROWS>(buf, refill, lane, c0[nrb], kf, q.f[nrb]);
+        }
+        valu(acc, b / NRB, b % NRB);
+        // issue order of the step: each MFMA of block b + 1 followed by a share
+        // of block b's vector work, so the two overlap
+        if (b + 1 < NB) {
+#pragma unroll
+            for (int i = 0; i < MT<T, D>::KS; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x002, VALU_PER_MFMA, 0);    // VALU
+            }
+        }
+        acc = nacc;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// The same products without pipelining, for the few tiles at the end of a
+// prompt (keeps their masking work from raising the register needs of the
+// main loop).
+template <typename T, int D, bool KEY_ROWS, typename F>
+__device__ __forceinline__ void tile_sweep_plain(const char *buf, const QFrags<T, D> &q,
+                                                 const TC<T, D> (&c0)[QFrags<T, D>::NRB], int lane, F &&valu) {
+    constexpr int NKB = KTile<T, D>::NKB, NRB = QFrags<T, D>::NRB;
+#pragma unroll 1
+    for (int kb = 0; kb < NKB; ++kb) {
+        TA<T, D> kf[MT<T, D>::KS];
+        load_kf<T, D>(buf, kb, lane, kf);
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+            TC<T, D> acc = block_mma_refill<T, D, KEY_ROWS>(buf, -1, lane, c0[rb], kf, q.f[rb]);
+            valu(acc, kb, rb);
+        }
     }
 }
 
-// ---------------------------------------------------------------- pass A: row statistics per chunk
+// Tiles [0, nfull) of a chunk lie wholly before the first window position, so
+// every row sees every key of them; the rest need the causal mask.
+__device__ __forceinline__ int full_tiles(int key_begin, int ntile, int tk, int N, int W) {
+    const int span = N - W + 1 - key_begin;            // keys key_begin .. N - W are seen by every row
+    return max(0, min(ntile, span >= 0 ? span / tk : 0));
+}
+
+// ---------------------------------------------------------------- stats pass
+
+// Exact update of the blocks whose bit (kb * NRB + rb) is set in `sel`.  The
+// state (m, s) of a row means: the sum of 2^x over the keys seen so far is
+// s * 2^m, with any reference m.  The new reference is the larger of the
+// state's magnitude m + log2(s) and the block's max over its visible keys
+// (all keys unless MASK), so neither the state nor the block's terms can
+// overflow or lose precision.
+template <typename T, int D, bool MASK>
+struct StatsExact {
+    static constexpr int NRB = QFrags<T, D>::NRB;
+    float (&m)[NRB];
+    float (&s)[NRB];
+    unsigned sel;
+    int lane, wave, key0, N, W, R;
+    float c2;
+    __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
+        using M = MT<T, D>;
+        if (MASK) {
+            const int row = wave * 64 + rb * M::BM + lane % M::BM;
+            const int pos = row < R ? N - W + row % W : -1;
+#pragma unroll
+            for (int v = 0; v < M::NV; ++v) acc[v] = key0 + kb * M::BM + M::crow(v, lane) <= pos ? acc[v] : -INFINITY;
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < M::NV; ++v) mx = fmaxf(mx, acc[v]);
+        const float eff = s[rb] > 0.f ? m[rb] + __log2f(s[rb]) : -INFINITY;
+        const float mn = fmaxf(eff, mx * c2);
+        const float ref = mn == -INFINITY ? 0.f : mn;
+        float t = 0.f;
+#pragma unroll
+        for (int v = 0; v < M::NV; ++v) t += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, -ref));
+        const float sn = fmaf(s[rb], __builtin_amdgcn_exp2f(m[rb] - ref), t);
+        const bool take = (sel >> (kb * NRB + rb)) & 1u;
+        s[rb] = take ? sn : s[rb];
+        m[rb] = take ? ref : m[rb];
+    }
+};
+
+// Fast update against the current reference.  A block whose terms sum past
+// 2^64 of it, or after which the row's sum is still below 2^-60 of it, is left
+// untouched and reported in `need` (then the exact update takes it).
+template <typename T, int D>
+struct StatsFast {
+    static constexpr int NRB = QFrags<T, D>::NRB;
+    const float (&m)[NRB];
+    float (&s)[NRB];
+    unsigned &need;
+    float c2;
+    __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
+        using M = MT<T, D>;
+        const float nm = -m[rb];
+        float t[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int v = 0; v < M::NV; ++v) t[v % 4] += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, nm));
+        const float tt = (t[0] + t[1]) + (t[2] + t[3]);
+        const float sn = s[rb] + tt;
+        const bool bad = !(tt <= 0x1p64f) || !(sn >= 0x1p-60f);     // also inf and NaN
+        need |= (unsigned)bad << (kb * NRB + rb);
+        s[rb] = bad ? s[rb] : sn;
+    }
+};
+
 template <typename T, int D, int NW>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void score_stats_kernel(int B, int L, int Hq, int Hkv, int W,
-                                                               const int32_t *__restrict__ cu_seqlens, int64_t T_,
-                                                               const T *__restrict__ q_win, const T *__restrict__ k,
-                                                               int64_t k_layer_rows, float c2, int nchunk,
-                                                               float2 *__restrict__ part) {
-    __shared__ __attribute__((aligned(16))) char tiles[2 * SC_TK * Frag<T, D>::ROWB];
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void score_stats_kernel(
+    int B, int L, int Hq, int Hkv, int W, const int32_t *__restrict__ cu_seqlens, int64_t T_,
+    const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, float c2, int nchunk, int chunk_keys,
+    float2 *__restrict__ part) {
+    using M = MT<T, D>;
+    using KT = KTile<T, D>;
+    constexpr int NRB = QFrags<T, D>::NRB;
+    // two tile buffers as separate objects: the compiler can then tell that the
+    // direct loads into one never alias the fragment reads from the other
+    __shared__ __attribute__((aligned(16))) char kbA[KT::BYTES];
+    __shared__ __attribute__((aligned(16))) char kbB[KT::BYTES];
     int64_t u;
     int chunk;
     unit_chunk((int64_t)L * Hkv * B, nchunk, u, chunk);
     const UnitGeom g = unit_geom(u, B, Hkv, cu_seqlens, T_);
     const int G = Hq / Hkv, R = G * W;
     const int N = (int)g.N;
-    const int key_begin = chunk * SC_CHUNK;
+    const int key_begin = chunk * chunk_keys;
     if (N < W || key_begin >= N) return;
     const int lane = threadIdx.x % 64;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const T *qunit = q_win + (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * W * D;
     const T *kunit = k + ((int64_t)g.l * k_layer_rows + (int64_t)g.h * T_ + g.s0) * D;
-    typename Frag<T, D>::A qa[4][Frag<T, D>::KSTEPS];
-    load_q<T, D>(qunit, R, wave, lane, qa);
+    const int key_end = min(N, key_begin + chunk_keys);
+    const int ntile = (int)ceil_div(key_end - key_begin, KT::TK);
+    KT::template load<NW>(kbA, kunit, key_begin, N, wave, lane);
+    QFrags<T, D> q;
+    q.load(qunit, R, wave, lane);
 
-    // running (max, sum) of this lane's 16 rows (rb*16 + 4*(lane/16) + i) over its key columns, log2 units
-    float m[4][4], s[4][4];
+    TC<T, D> zero[NRB];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+    for (int rb = 0; rb < NRB; ++rb) zero[rb] = M::zero();
+    // (reference, sum) of row wave * 64 + rb * BM + lane % BM over this lane's keys, log2 units
+    float m[NRB], s[NRB];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) { m[rb][i] = -INFINITY; s[rb][i] = 0.f; }
-    const int key_end = min(N, key_begin + SC_CHUNK);
-    for_each_tile<T, D, NW>(kunit, N, W, key_begin, key_end, tiles, qa, lane,
-                            [&](f32x4 (&acc)[4][4], int key0, bool full, int) {
-        if (!full) {   // causal / end-of-prompt masking (the last tiles of a prompt only)
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int r = wave * 64 + rb * 16 + 4 * (lane / 16) + i;
-                    const int pos = r < R ? N - W + (r % W) : -1;
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb)
-                        if (key0 + kb * 16 + lane % 16 > pos) acc[rb][kb][i] = -INFINITY;
-                }
-        }
-        // online (max, sum) update; in masked tiles a row with no usable key so
-        // far keeps m = -inf and s = 0 (its reference is taken as 0 so that no
-        // inf - inf appears)
-        if (full) {
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float mx = fmaxf(fmaxf(acc[rb][0][i], acc[rb][1][i]), fmaxf(acc[rb][2][i], acc[rb][3][i]));
-                    const float mn = fmaxf(m[rb][i], mx * c2);
-                    float add = 0.f;
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb) add += __builtin_amdgcn_exp2f(fmaf(acc[rb][kb][i], c2, -mn));
-                    s[rb][i] = fmaf(s[rb][i], __builtin_amdgcn_exp2f(m[rb][i] - mn), add);
-                    m[rb][i] = mn;
-                }
-        } else {
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float mx = fmaxf(fmaxf(acc[rb][0][i], acc[rb][1][i]), fmaxf(acc[rb][2][i], acc[rb][3][i]));
-                    const float mn = fmaxf(m[rb][i], mx * c2);
-                    const float ref = mn == -INFINITY ? 0.f : mn;
-                    float add = 0.f;
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb) add += __builtin_amdgcn_exp2f(fmaf(acc[rb][kb][i], c2, -ref));
-                    s[rb][i] = fmaf(s[rb][i], __builtin_amdgcn_exp2f(m[rb][i] - ref), add);
-                    m[rb][i] = mn;
-                }
-        }
-    }, [](int, int) {});
-    // combine the 16 lanes that share rows (lane % 16 varies the key column)
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            float mm = m[rb][i], ss = s[rb][i];
-#pragma unroll
-            for (int off = 1; off < 16; off <<= 1) {
-                const float mo = __shfl_xor(mm, off, 64), so = __shfl_xor(ss, off, 64);
-                const float mn = fmaxf(mm, mo);
-                if (mn > -INFINITY) {
-                    ss = ss * __builtin_amdgcn_exp2f(mm - mn) + so * __builtin_amdgcn_exp2f(mo - mn);
-                    mm = mn;
-                }
-            }
-            const int r = wave * 64 + rb * 16 + 4 * (lane / 16) + i;
-            if (lane % 16 == 0 && r < R) part[(u * nchunk + chunk) * (int64_t)R + r] = make_float2(mm, ss);
-        }
-}
-
-// ---------------------------------------------------------------- pass B: merge chunks into the LSE
-__global__ __launch_bounds__(512) void score_lse_kernel(int B, int L, int Hq, int Hkv, int W,
-                                                         const int32_t *__restrict__ cu_seqlens, int64_t T_,
-                                                         int nchunk, const float2 *__restrict__ part,
-                                                         float *__restrict__ lse) {
-    const int64_t u = blockIdx.x;
-    const UnitGeom g = unit_geom(u, B, Hkv, cu_seqlens, T_);
-    const int G = Hq / Hkv, R = G * W;
-    const int r = threadIdx.x;
-    if (r >= R) return;
-    const int64_t out = (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * W + r;
-    if (g.N < W) { lse[out] = INFINITY; return; }
-    const int nc = (int)min<int64_t>(ceil_div(g.N, SC_CHUNK), nchunk);  // a prompt above max_seqlen is cut
-    float M = -INFINITY;
-    for (int c = 0; c < nc; ++c) M = fmaxf(M, part[(u * nchunk + c) * (int64_t)R + r].x);
-    float S = 0.f;
-    for (int c = 0; c < nc; ++c) {
-        const float2 p = part[(u * nchunk + c) * (int64_t)R + r];
-        if (p.x > -INFINITY) S += p.y * __builtin_amdgcn_exp2f(p.x - M);
+    for (int rb = 0; rb < NRB; ++rb) { m[rb] = 0.f; s[rb] = 0.f; }
+    // one tile (in kbA when t is even, kbB when odd): wait for it, release the
+    // other buffer, load the next tile, then `work`
+    auto step = [&](int t, char *cur, char *nxt, auto &&work) {
+        barrier_after_loads();      // tile t landed; every wavefront is done with tile t - 1
+        const int key0 = key_begin + t * KT::TK;
+        if (t + 1 < ntile) KT::template load<NW>(nxt, kunit, key0 + KT::TK, N, wave, lane);
+        work(cur, key0);
+    };
+    auto full = [&](const char *buf, int key0) {       // every row sees every key of the tile
+        unsigned need = 0u;
+        tile_sweep<T, D, true>(buf, q, zero, lane, StatsFast<T, D>{m, s, need, c2});
+        if (__any(need != 0u))             // rare: those blocks again, exactly
+            tile_sweep<T, D, true>(buf, q, zero, lane, StatsExact<T, D, false>{m, s, need, lane, wave, key0, N, W, R, c2});
+    };
+    auto masked = [&](const char *buf, int key0) {     // causal limit and prompt end (or a leftover full tile)
+        tile_sweep_plain<T, D, true>(buf, q, zero, lane, StatsExact<T, D, true>{m, s, ~0u, lane, wave, key0, N, W, R, c2});
+    };
+    const int nfull = full_tiles(key_begin, ntile, KT::TK, N, W);
+    int t = 0;
+    for (; t + 1 < nfull; t += 2) {
+        step(t, kbA, kbB, full);
+        step(t + 1, kbB, kbA, full);
     }
-    lse[out] = (M + __log2f(S)) * SC_LN2;  // natural log, like a flash-attention LSE
+    for (; t < ntile; ++t) {
+        if (t & 1) step(t, kbB, kbA, masked);
+        else step(t, kbA, kbB, masked);
+    }
+    barrier_after_loads();      // no load in flight when the workgroup ends
+    // combine the lane groups that hold the same row (different keys); the
+    // wavefront owns its rows, so the result is the chunk's
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+#pragma unroll
+        for (int off = M::BM; off < 64; off <<= 1) {
+            const float mo = __shfl_xor(m[rb], off, 64), so = __shfl_xor(s[rb], off, 64);
+            const float mn = fmaxf(m[rb], mo);
+            s[rb] = s[rb] * __builtin_amdgcn_exp2f(m[rb] - mn) + so * __builtin_amdgcn_exp2f(mo - mn);
+            m[rb] = mn;
+        }
+        const int row = wave * 64 + rb * M::BM + lane;
+        if (lane < M::BM && row < R) part[(u * nchunk + chunk) * (int64_t)R + row] = make_float2(m[rb], s[rb]);
+    }
 }
 
-// ---------------------------------------------------------------- pass C: normalised column sums
+// ---------------------------------------------------------------- colsum pass
+
+// Column sums of one block: cs[kb] += sum over the lane's rows of exp(z - LSE).
+// Column sums of one block: cs[kb] += sum over the lane's rows of
+// exp2(c2 * acc), where the products were accumulated onto minus each row's
+// normaliser (divided by c2), so acc * c2 = z * c2 - LSE_row in log2 units.
+template <typename T, int D, bool MASK>
+struct ColsumStep {
+    float (&cs)[KTile<T, D>::NKB];
+    const int *poss;    // window position of every row of the unit (-1 for padded rows), LDS
+    int lane, wave, key0;
+    float c2;
+    __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
+        using M = MT<T, D>;
+        const int key = key0 + kb * M::BM + lane % M::BM;
+#pragma unroll
+        for (int g4 = 0; g4 < M::NV / 4; ++g4) {
+            int4 pos = make_int4(0, 0, 0, 0);
+            if (MASK) pos = *reinterpret_cast<const int4 *>(poss + wave * 64 + rb * M::BM + M::crow(4 * g4, lane));
+            const int ps[4] = {pos.x, pos.y, pos.z, pos.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float p = __builtin_amdgcn_exp2f(acc[4 * g4 + i] * c2);
+                cs[kb] += (!MASK || key <= ps[i]) ? p : 0.f;
+            }
+        }
+    }
+};
+
 template <typename T, int D, int NW>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void score_colsum_kernel(int B, int L, int Hq, int Hkv, int W,
-                                                                const int32_t *__restrict__ cu_seqlens, int64_t T_,
-                                                                const T *__restrict__ q_win, const T *__restrict__ k,
-                                                                int64_t k_layer_rows, float c2, int nchunk,
-                                                                const float *__restrict__ lse,
-                                                                float *__restrict__ scores) {
-    __shared__ __attribute__((aligned(16))) char tiles[2 * SC_TK * Frag<T, D>::ROWB];
-    __shared__ float csum[2][NW][SC_TK];
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void score_colsum_kernel(
+    int B, int L, int Hq, int Hkv, int W, const int32_t *__restrict__ cu_seqlens, int64_t T_,
+    const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, float c2, int nchunk, int chunk_keys,
+    const float2 *__restrict__ part, const float *__restrict__ lse_in, float *__restrict__ scores) {
+    using M = MT<T, D>;
+    using KT = KTile<T, D>;
+    constexpr int NRB = QFrags<T, D>::NRB, NKB = KT::NKB;
+    __shared__ __attribute__((aligned(16))) char kbA[KT::BYTES];   // separate objects, see the stats kernel
+    __shared__ __attribute__((aligned(16))) char kbB[KT::BYTES];
+    __shared__ float csum[2][NW][KT::TK];
+    __shared__ __attribute__((aligned(16))) float nl2s[NW * 64];
+    __shared__ __attribute__((aligned(16))) int poss[NW * 64];
     int64_t u;
     int chunk;
     unit_chunk((int64_t)L * Hkv * B, nchunk, u, chunk);
     const UnitGeom g = unit_geom(u, B, Hkv, cu_seqlens, T_);
     const int G = Hq / Hkv, R = G * W;
     const int N = (int)g.N;
-    const int key_begin = chunk * SC_CHUNK;
+    const int key_begin = chunk * chunk_keys;
+    const int key_end = min(N, key_begin + chunk_keys);
     float *srow = scores + ((int64_t)g.l * Hkv + g.h) * T_ + g.s0;
     if (N < W) {  // documented fallback: zero scores
-        for (int j = key_begin + (int)threadIdx.x; j < min(N, key_begin + SC_CHUNK); j += blockDim.x) srow[j] = 0.f;
+        for (int j = key_begin + (int)threadIdx.x; j < key_end; j += blockDim.x) srow[j] = 0.f;
         return;
     }
     if (key_begin >= N) return;
     const int lane = threadIdx.x % 64;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
-    const T *qunit = q_win + (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * W * D;
+    const int64_t rbase = (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * W;   // first window row of the unit
     const T *kunit = k + ((int64_t)g.l * k_layer_rows + (int64_t)g.h * T_ + g.s0) * D;
-    const float *lunit = lse + (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * W;
-    typename Frag<T, D>::A qa[4][Frag<T, D>::KSTEPS];
-    load_q<T, D>(qunit, R, wave, lane, qa);
-    float l2[4][4];
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = wave * 64 + rb * 16 + 4 * (lane / 16) + i;
-            l2[rb][i] = r < R ? lunit[r] * SC_LOG2E : INFINITY;   // padded rows contribute exp2(-inf) = 0
-        }
-    const int key_end = min(N, key_begin + SC_CHUNK);
-    const int nwave = NW;
-    for_each_tile<T, D, NW>(kunit, N, W, key_begin, key_end, tiles, qa, lane,
-                            [&](f32x4 (&acc)[4][4], int key0, bool full, int t) {
-        float cs[4] = {0.f, 0.f, 0.f, 0.f};
-        if (full) {
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb)
-                        cs[kb] += __builtin_amdgcn_exp2f(fmaf(acc[rb][kb][i], c2, -l2[rb][i]));
-        } else {
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int r = wave * 64 + rb * 16 + 4 * (lane / 16) + i;
-                    const int pos = r < R ? N - W + (r % W) : -1;
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb) {
-                        const float p = __builtin_amdgcn_exp2f(fmaf(acc[rb][kb][i], c2, -l2[rb][i]));
-                        cs[kb] += (key0 + kb * 16 + lane % 16 <= pos) ? p : 0.f;
-                    }
+    const int ntile = (int)ceil_div(key_end - key_begin, KT::TK);
+    KT::template load<NW>(kbA, kunit, key_begin, N, wave, lane);
+    QFrags<T, D> q;
+    q.load(q_win + rbase * D, R, wave, lane);
+    // row normalisers in log2 units: the caller's LSE, or the merge of the chunk statistics
+    for (int r = threadIdx.x; r < NW * 64; r += 64 * NW) {
+        float l2 = INFINITY;                     // padded rows contribute exp2(-inf) = 0
+        if (r < R) {
+            if (lse_in) {
+                l2 = lse_in[rbase + r] * SC_LOG2E;
+            } else {
+                const int nc = (int)min<int64_t>(ceil_div(N, chunk_keys), nchunk);  // a prompt above max_seqlen is cut
+                const float2 *pr = part + u * nchunk * (int64_t)R + r;
+                float Mx = -INFINITY;
+                for (int c = 0; c < nc; ++c) Mx = fmaxf(Mx, pr[(int64_t)c * R].x);
+                const float ref = Mx == -INFINITY ? 0.f : Mx;
+                float S = 0.f;
+                for (int c = 0; c < nc; ++c) {
+                    const float2 p = pr[(int64_t)c * R];
+                    S += p.y * __builtin_amdgcn_exp2f(p.x - ref);
                 }
+                l2 = S > 0.f ? ref + __log2f(S) : INFINITY;
+            }
         }
-        // sum over the four lane groups holding different rows of the same keys
+        nl2s[r] = -l2 / c2;
+        poss[r] = r < R ? N - W + r % W : -1;
+    }
+    __syncthreads();
+    // accumulator start of every row block: minus the lane's rows' normalisers
+    TC<T, D> c0[NRB];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            cs[kb] += __shfl_xor(cs[kb], 16, 64);
-            cs[kb] += __shfl_xor(cs[kb], 32, 64);
-        }
-        if (lane < 16) {
+    for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb) csum[t & 1][wave][kb * 16 + lane] = cs[kb];
-        }
-    }, [&](int key0, int t) {
-        // sum over the wavefronts (double-buffered: the next tile writes the other half)
-        if (threadIdx.x < SC_TK) {
+        for (int v = 0; v < M::NV; ++v) c0[rb][v] = nl2s[wave * 64 + rb * M::BM + M::crow(v, lane)];
+
+    // per tile: the wavefronts' partial column sums go to csum[t & 1]; they are
+    // added and stored after the next barrier
+    auto flush = [&](int t) {
+        const int key0 = key_begin + t * KT::TK;
+        for (int j = threadIdx.x; j < KT::TK; j += 64 * NW) {
             float v = 0.f;
-            for (int w = 0; w < nwave; ++w) v += csum[t & 1][w][threadIdx.x];
-            const int key = key0 + (int)threadIdx.x;
-            if (key < N) srow[key] = v;
+            for (int w = 0; w < NW; ++w) v += csum[t & 1][w][j];
+            if (key0 + j < N) srow[key0 + j] = v;
         }
-    });
+    };
+    // one tile (in kbA when t is even, kbB when odd): wait for it, release the
+    // other buffer, load the next tile, multiply
+    auto step = [&](int t, char *cur, char *nxt, auto mask) {
+        constexpr bool MASK = decltype(mask)::value;
+        barrier_after_loads();      // tile t landed; tile t - 1 finished everywhere
+        if (t > 0) flush(t - 1);
+        const int key0 = key_begin + t * KT::TK;
+        if (t + 1 < ntile) KT::template load<NW>(nxt, kunit, key0 + KT::TK, N, wave, lane);
+        float cs[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) cs[kb] = 0.f;
+        if (MASK)
+            tile_sweep_plain<T, D, false>(cur, q, c0, lane, ColsumStep<T, D, true>{cs, poss, lane, wave, key0, c2});
+        else
+            tile_sweep<T, D, false>(cur, q, c0, lane, ColsumStep<T, D, false>{cs, poss, lane, wave, key0, c2});
+        // lanes holding the same key (different rows) add up; every such lane
+        // then holds the total and stores it (same value, same address: no
+        // branch, so the exponentials are not moved behind one)
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+#pragma unroll
+            for (int off = M::BM; off < 64; off <<= 1) cs[kb] += __shfl_xor(cs[kb], off, 64);
+            csum[t & 1][wave][kb * M::BM + lane % M::BM] = cs[kb];
+        }
+    };
+    const int nfull = full_tiles(key_begin, ntile, KT::TK, N, W);
+    int t = 0;
+    for (; t + 1 < nfull; t += 2) {
+        step(t, kbA, kbB, std::false_type{});
+        step(t + 1, kbB, kbA, std::false_type{});
+    }
+    for (; t < ntile; ++t) {                   // the prompt's last keys (and a leftover full tile)
+        if (t & 1) step(t, kbB, kbA, std::true_type{});
+        else step(t, kbA, kbB, std::true_type{});
+    }
+    __syncthreads();
+    flush(ntile - 1);
+}
+
+// Launch plan: each unit's keys split into chunks of chunk_keys (a multiple
+// of the LDS tile), one workgroup per (unit, chunk).  Long chunks keep the
+// per-workgroup set-up (query fragments, row normalisers) small against the
+// streaming work; short prompts or few units take shorter chunks so that the
+// launch still has enough workgroups to fill the chip.
+struct ScorePlan {
+    int chunk_keys, nchunk;
+};
+
+static ScorePlan score_plan(int B, int L, int Hkv, int max_seqlen) {
+    constexpr int64_t MIN_WG = 1024;                      // two rounds of two workgroups per CU
+    constexpr int TILE = 128;                             // chunk granularity (keys)
+    const int64_t units = (int64_t)B * L * Hkv;
+    const int64_t want = std::max<int64_t>(1, ceil_div(MIN_WG, units));       // chunks per unit
+    ScorePlan p;
+    p.chunk_keys = (int)std::min<int64_t>(SC_CHUNK, std::max<int64_t>(TILE, ceil_div(ceil_div(max_seqlen, want), TILE) * TILE));
+    p.nchunk = (int)ceil_div(max_seqlen, p.chunk_keys);
+    return p;
 }
 
 template <typename T, int D, int NW>
-static void launch_two_pass(hipStream_t s, dim3 grid, int units, int B, int L, int Hq, int Hkv, int W,
-                            const int32_t *cu_seqlens, int64_t ntok, const void *q_win, const void *k,
-                            int64_t k_layer_rows, float c2, int nchunk, const float *lse_in, float *scores, void *ws) {
-    const int R = (Hq / Hkv) * W;
-    const float *lse = lse_in;
-    if (!lse) {
-        float2 *part = reinterpret_cast<float2 *>(ws);
-        float *lse_ws = reinterpret_cast<float *>(part + (int64_t)units * nchunk * R);
-        score_stats_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok,
-                                                             reinterpret_cast<const T *>(q_win),
-                                                             reinterpret_cast<const T *>(k), k_layer_rows, c2,
-                                                             nchunk, part);
-        score_lse_kernel<<<(unsigned)units, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, nchunk, part, lse_ws);
-        lse = lse_ws;
-    }
-    score_colsum_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok,
-                                                          reinterpret_cast<const T *>(q_win),
-                                                          reinterpret_cast<const T *>(k), k_layer_rows, c2, nchunk,
-                                                          lse, scores);
+static void launch_passes(hipStream_t s, const ScorePlan &p, int B, int L, int Hq, int Hkv, int W,
+                          const int32_t *cu_seqlens, int64_t ntok, const void *q_win, const void *k,
+                          int64_t k_layer_rows, float c2, const float *lse_in, float *scores, void *ws) {
+    float2 *part = reinterpret_cast<float2 *>(ws);
+    const T *q = reinterpret_cast<const T *>(q_win);
+    const T *kk = reinterpret_cast<const T *>(k);
+    const dim3 grid((unsigned)((int64_t)L * Hkv * B * p.nchunk));
+    if (!lse_in)
+        score_stats_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                             k_layer_rows, c2, p.nchunk, p.chunk_keys, part);
+    score_colsum_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                          k_layer_rows, c2, p.nchunk, p.chunk_keys, part, lse_in,
+                                                          scores);
 }
 
 template <typename T, int D>
@@ -314,14 +497,12 @@ static int launch_score(hipStream_t s, int B, int L, int Hq, int Hkv, int W, con
                         const float *lse_in, float *scores, void *ws) {
     const int R = (Hq / Hkv) * W;
     const int nw = (int)ceil_div(R, 64);
-    const int nchunk = (int)ceil_div(max_seqlen, SC_CHUNK);
-    const int64_t units = (int64_t)L * Hkv * B;
+    const ScorePlan p = score_plan(B, L, Hkv, max_seqlen);
     const float c2 = SC_LOG2E / sqrtf((float)D);
-    dim3 grid((unsigned)(units * nchunk));
-    if (nw <= 1) launch_two_pass<T, D, 1>(s, grid, (int)units, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, nchunk, lse_in, scores, ws);
-    else if (nw <= 2) launch_two_pass<T, D, 2>(s, grid, (int)units, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, nchunk, lse_in, scores, ws);
-    else if (nw <= 4) launch_two_pass<T, D, 4>(s, grid, (int)units, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, nchunk, lse_in, scores, ws);
-    else launch_two_pass<T, D, 8>(s, grid, (int)units, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, nchunk, lse_in, scores, ws);
+    if (nw <= 1) launch_passes<T, D, 1>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, scores, ws);
+    else if (nw <= 2) launch_passes<T, D, 2>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, scores, ws);
+    else if (nw <= 4) launch_passes<T, D, 4>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, scores, ws);
+    else launch_passes<T, D, 8>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, scores, ws);
     return launch_status("sg_score");
 }
 
@@ -329,16 +510,11 @@ static int launch_score(hipStream_t s, int B, int L, int Hq, int Hkv, int W, con
 
 using namespace sg;
 
-static size_t two_pass_workspace(int B, int L, int Hq, int Hkv, int W, int max_seqlen) {
-    const int64_t R = (int64_t)(Hq / Hkv) * W;
-    const int64_t units = (int64_t)L * Hkv * B;
-    const int64_t nchunk = ceil_div(max_seqlen, SC_CHUNK);
-    return (size_t)(units * nchunk * R) * sizeof(float2) + (size_t)B * L * Hq * W * sizeof(float);
-}
-
 extern "C" size_t sg_score_workspace_size(int B, int L, int Hq, int Hkv, int d, int W, int max_seqlen) {
     if (B <= 0 || L <= 0 || Hkv <= 0 || Hq <= 0 || W <= 0 || max_seqlen <= 0 || d <= 0) return 0;
-    return two_pass_workspace(B, L, Hq, Hkv, W, max_seqlen);
+    const int64_t R = (int64_t)(Hq / Hkv) * W;
+    const ScorePlan p = score_plan(B, L, Hkv, max_seqlen);
+    return (size_t)((int64_t)L * Hkv * B * p.nchunk * R) * sizeof(float2);
 }
 
 extern "C" int sg_score(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
@@ -357,7 +533,7 @@ extern "C" int sg_score(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv
     SG_REQUIRE(cu_seqlens && q_win && k && scores, SG_EINVAL, "sg_score: null pointer");
     SG_REQUIRE(aligned16(q_win) && aligned16(k), SG_EINVAL, "sg_score: q_win and k must be 16-byte aligned");
     const int64_t units = (int64_t)L * Hkv * B;
-    SG_REQUIRE(units * ceil_div(max_seqlen, SC_CHUNK) <= 0x7fffffff, SG_EINVAL, "sg_score: grid too large");
+    SG_REQUIRE(units * ceil_div(max_seqlen, 128) <= 0x7fffffff, SG_EINVAL, "sg_score: grid too large");
     if (!lse_in) {
         const size_t need = sg_score_workspace_size(B, L, Hq, Hkv, d, W, max_seqlen);
         SG_REQUIRE(ws && ws_bytes >= need, SG_EWORKSPACE, "sg_score: workspace %zu < %zu", ws_bytes, need);

@@ -1,5 +1,5 @@
-// Shared pieces of the score kernels: MFMA operand fragments, the K-tile
-// stager and the query-fragment loader (gfx950).
+// Shared pieces of the score kernels: MFMA tile traits, work mapping and the
+// LDS K tiles (gfx950).
 #pragma once
 
 #include "sg_internal.h"
@@ -9,46 +9,63 @@ namespace sg {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int SC_TK = 64;          // keys per tile
-constexpr int SC_TPC = 16;         // tiles per chunk
-constexpr int SC_CHUNK = SC_TK * SC_TPC;
+constexpr int SC_CHUNK = 2048;     // keys per workgroup
 constexpr int SC_MAXR = 512;       // rows per unit (G * W): at most 8 wavefronts
 constexpr float SC_LOG2E = 1.4426950408889634f;
 constexpr float SC_LN2 = 0.6931471805599453f;
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// MFMA tile traits.  bf16 runs v_mfma_f32_32x32x16_bf16 (32 x 32 outputs, 16
+// products per instruction and output; on gfx950 its issue overlaps the
+// exponential / add work of the score passes far better than the 16x16x32
+// form); fp32 runs v_mfma_f32_16x16x4_f32.
+//
+// For both operand slots a lane holds row (or column) lane % BM and the
+// contraction slice ks of its lane group, so the same registers serve as A
+// or B: mma(Q, K) gives C[row][key], mma(K, Q) gives C[key][row].  Output
+// register v of a lane holds C[crow(v, lane)][lane % BM].
 template <typename T, int D>
-struct Frag;
+struct MT;
 
 template <int D>
-struct Frag<uint16_t, D> {  // bfloat16 operands, K = 32 per instruction
-    static constexpr int KSTEPS = D / 32;
-    static constexpr int ROWB = D * 2 + 16;  // padded LDS row bytes
+struct MT<uint16_t, D> {
+    static constexpr int BM = 32;                 // rows (and columns) of one output tile
+    static constexpr int KS = D / 16;             // instructions per contraction
+    static constexpr int NV = 16;                 // outputs per lane
+    static constexpr int ROWB = D * 2 + 16;       // padded LDS row bytes (conflict-free column reads)
     using A = bf16x8;
-    __device__ static A zero() { return A{}; }
+    using C = f32x16;
+    __device__ static int crow(int v, int lane) { return 8 * (v / 4) + 4 * (lane / 32) + v % 4; }
     __device__ static A load_global(const uint16_t *row, int ks, int lane) {
-        return *reinterpret_cast<const A *>(row + ks * 32 + 8 * (lane / 16));
+        return *reinterpret_cast<const A *>(row + ks * 16 + 8 * (lane / 32));
     }
-    __device__ static A load_lds(const char *tile, int key, int ks, int lane) {
-        return *reinterpret_cast<const A *>(tile + key * ROWB + (ks * 32 + 8 * (lane / 16)) * 2);
+    __device__ static A load_lds(const char *img, int row, int ks, int lane) {
+        return *reinterpret_cast<const A *>(img + row * ROWB + (ks * 16 + 8 * (lane / 32)) * 2);
     }
-    __device__ static f32x4 mma(const A &a, const A &b, const f32x4 &c) {
-        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    __device__ static C mma(const A &a, const A &b, const C &c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
     }
+    __device__ static C zero() { return C{}; }
 };
 
 template <int D>
-struct Frag<float, D> {  // fp32 operands, K = 4 per instruction
-    static constexpr int KSTEPS = D / 4;
+struct MT<float, D> {
+    static constexpr int BM = 16;
+    static constexpr int KS = D / 4;
+    static constexpr int NV = 4;
     static constexpr int ROWB = D * 4 + 16;
     using A = float;
-    __device__ static A zero() { return 0.f; }
+    using C = f32x4;
+    __device__ static int crow(int v, int lane) { return 4 * (lane / 16) + v; }
     __device__ static A load_global(const float *row, int ks, int lane) { return row[ks * 4 + lane / 16]; }
-    __device__ static A load_lds(const char *tile, int key, int ks, int lane) {
-        return *reinterpret_cast<const float *>(tile + key * ROWB + (ks * 4 + lane / 16) * 4);
+    __device__ static A load_lds(const char *img, int row, int ks, int lane) {
+        return *reinterpret_cast<const float *>(img + row * ROWB + (ks * 4 + lane / 16) * 4);
     }
-    __device__ static f32x4 mma(const A &a, const A &b, const f32x4 &c) {
+    __device__ static C mma(const A &a, const A &b, const C &c) {
         return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
     }
+    __device__ static C zero() { return C{}; }
 };
 
 // Workgroup -> (unit, chunk).  Workgroups are dealt to the 8 XCDs round-robin
@@ -86,52 +103,79 @@ __device__ __forceinline__ UnitGeom unit_geom(int64_t u, int B, int Hkv, const i
     return g;
 }
 
-// Stage one 64-key tile of K (rows [key0, key0+64) of the unit) into LDS.
-template <typename T, int D>
-__device__ __forceinline__ void stage_tile(char *tile, const T *kunit, int64_t key0, int64_t N) {
-    constexpr int ESZ = sizeof(T);
-    constexpr int VPR = D * ESZ / 16;  // 16-byte vectors per key row
-    for (int i = threadIdx.x; i < SC_TK * VPR; i += blockDim.x) {
-        const int key = i / VPR, v = i % VPR;
-        v4u x = v4u{0u, 0u, 0u, 0u};
-        if (key0 + key < N) x = reinterpret_cast<const v4u *>(kunit + (key0 + key) * D)[v];
-        *reinterpret_cast<v4u *>(tile + key * Frag<T, D>::ROWB + v * 16) = x;
-    }
+// LDS offset of a workgroup-shared address.
+__device__ __forceinline__ unsigned lds_addr(const char *p) {
+    return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
 }
 
-// acc[rb][kb] = Q(rows of row-block rb) . K(tile keys of key-block kb); the
-// first k-step multiplies with a zero accumulator operand (no separate clear)
+// Direct global->LDS load: lane i's 16 bytes land at LDS offset lds + 16 i;
+// lds is wavefront-uniform and travels in M0.  Issued from
+// inline assembly: the compiler then neither reorders LDS accesses across them
+// (memory clobber) nor inserts conservative waits for them before unrelated
+// LDS reads; callers wait for completion themselves (vector memory counter)
+// before reading the destination.  The s_nop is the wait state a direct LDS
+// load needs after M0 is written.
+__device__ __forceinline__ void dma16(const char *src, unsigned lds) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+}
+
+// K tiles in LDS.  A tile is TK keys of D elements, stored without padding;
+// the 16-byte vector v of key j sits at slot j * VPR + (v ^ (j % VPR)), so the
+// 32 (or 16) lanes reading one fragment column hit distinct banks.  Tiles
+// arrive through direct global->LDS loads (lane i of an instruction lands at
+// base + 16 i; the swizzle is applied to the global address each lane reads).
 template <typename T, int D>
-__device__ __forceinline__ void tile_mma(const typename Frag<T, D>::A (&qa)[4][Frag<T, D>::KSTEPS],
-                                         const char *tile, int lane, f32x4 (&acc)[4][4]) {
+struct KTile {
+    static constexpr int VPR = D * (int)sizeof(T) / 16;          // 16-byte vectors per key
+    static constexpr int TK = sizeof(T) == 2 ? 128 : 64;          // keys per tile
+    static constexpr int BYTES = TK * VPR * 16;
+    static constexpr int NKB = TK / MT<T, D>::BM;                 // key blocks per tile
+
+    // Issue the loads of keys [key0, key0 + TK) (clamped to the prompt's last
+    // key) into `buf`; the NW wavefronts share the work.  Completion is tracked
+    // by the vector memory counter of the issuing wavefront.
+    template <int NW>
+    __device__ static void load(char *buf, const T *kunit, int key0, int N, int wave, int lane) {
+        constexpr int KPI = 64 / VPR;                              // keys per instruction
+        constexpr int KPW = TK / NW;                               // keys per wavefront
+        static_assert(KPW % KPI == 0, "tile keys must split evenly over the wavefronts");
+        // recompute the per-lane offsets at every call instead of keeping them
+        // live across the caller's loop (registers are the scarce resource)
+        asm volatile("" : "+v"(lane));
+        const unsigned kl = (unsigned)lane / VPR, vl = (unsigned)lane % VPR;
+        const char *tb = reinterpret_cast<const char *>(kunit) + (int64_t)key0 * (VPR * 16);   // wavefront-uniform
+        // the last key of the prompt relative to key0: keys past it read it instead
+        const unsigned last = (unsigned)max(0, min(TK - 1, N - 1 - key0));
+        const bool whole = key0 + TK <= N;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-        const auto bf = Frag<T, D>::load_lds(tile, kb * 16 + lane % 16, 0, lane);
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb) acc[rb][kb] = Frag<T, D>::mma(qa[rb][0], bf, f32x4{0.f, 0.f, 0.f, 0.f});
-    }
-#pragma unroll
-    for (int ks = 1; ks < Frag<T, D>::KSTEPS; ++ks) {
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            const auto bf = Frag<T, D>::load_lds(tile, kb * 16 + lane % 16, ks, lane);
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb) acc[rb][kb] = Frag<T, D>::mma(qa[rb][ks], bf, acc[rb][kb]);
+        for (int j = 0; j < KPW / KPI; ++j) {
+            const unsigned key = (unsigned)(wave * KPW + j * KPI) + kl;
+            const unsigned v = vl ^ (key % VPR);
+            const unsigned row = whole ? key : min(key, last);
+            dma16(tb + (row * (VPR * 16) + v * 16), lds_addr(buf + (wave * KPW + j * KPI) * VPR * 16));
         }
     }
-}
 
-template <typename T, int D>
-__device__ __forceinline__ void load_q(const T *qunit, int R, int wave, int lane,
-                                       typename Frag<T, D>::A (&qa)[4][Frag<T, D>::KSTEPS]) {
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-        const int r = wave * 64 + rb * 16 + lane % 16;
-#pragma unroll
-        for (int ks = 0; ks < Frag<T, D>::KSTEPS; ++ks)
-            qa[rb][ks] = r < R ? Frag<T, D>::load_global(qunit + (int64_t)r * D, ks, lane) : Frag<T, D>::zero();
+    // Operand fragment (key block kb, contraction slice ks) of a lane.
+    __device__ static typename MT<T, D>::A frag(const char *buf, int kb, int ks, int lane) {
+        using M = MT<T, D>;
+        const int key = kb * M::BM + lane % M::BM;
+        if constexpr (sizeof(T) == 2) {
+            const int v = ks * 2 + lane / 32;                     // elements ks * 16 + 8 * (lane / 32) ..
+            return *reinterpret_cast<const typename M::A *>(buf + (key * VPR + (v ^ (key % VPR))) * 16);
+        } else {
+            const int e = ks * 4 + lane / 16;                     // element of the key row
+            const int v = e / 4;
+            return *reinterpret_cast<const float *>(buf + (key * VPR + (v ^ (key % VPR))) * 16 + (e % 4) * 4);
+        }
     }
-}
+};
 
+// Workgroup barrier after this wavefront's LDS operations and vector memory
+// operations (direct LDS loads included) have completed.  The asm's memory
+// clobber keeps the compiler from moving memory accesses across it.
+__device__ __forceinline__ void barrier_after_loads() {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 }  // namespace sg

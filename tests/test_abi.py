@@ -48,7 +48,11 @@ def test_sizes(lib):
     # [K | V | idx] of 2 layers x 8 heads x 819 rows of 128 bf16
     S = 2 * 8 * 819
     assert smartgen.pack_bytes(__import__("torch").bfloat16, 2, 8, 128, 819) == 2 * S * 256 + 4 * S
-    assert smartgen.score_workspace_size(1, 1, 8, 8, 64, 32, 2048) == 8 * 2 * 32 * 8 + 8 * 32 * 4   # 1024-key chunks
+    # 8 units are few: the keys split into 128-key chunks so that the launch
+    # fills the chip; (reference, sum) per row and chunk
+    assert smartgen.score_workspace_size(1, 1, 8, 8, 64, 32, 2048) == 8 * 16 * 32 * 8
+    # 256 units (32 layers x 8 heads) at 8192 keys: 2048-key chunks
+    assert smartgen.score_workspace_size(1, 32, 32, 8, 128, 64, 8192) == 256 * 4 * 256 * 8
     assert smartgen.decode_workspace_size(1, 32, 8, 128, 1, 16) == 0          # one split: no workspace
     assert smartgen.decode_workspace_size(2, 32, 8, 128, 64, 16) == 2 * 8 * 4 * 4 * 130 * 4   # <= 4 splits of 256 rows
 
