@@ -1,25 +1,35 @@
 // sg_decode_attn: GQA decode attention over a partial, page-addressed KV set.
 //
 // Grid: x = (sequence, KV head) unit, y = split of the unit's rows (one split
-// whenever there are at least as many units as compute units).  A workgroup
-// of WAVES wavefronts serves all G q heads of the group, so each K/V row is
-// read from HBM once per step.  Wavefront w walks 32-row sub-tiles w,
-// w + WAVES, ...; within a sub-tile CPR = 16 / esize * d / 16 lanes cover one
-// row with one 16-byte vector each (fully coalesced K and V loads), and a
-// wavefront step covers 64 / CPR rows.  Per sub-tile:
-//   logits : each lane dots its slice of q (held in registers) with its K
-//            slice (v_dot2_f32_bf16 for bf16, fp32 accumulation); DPP adds sum
-//            the partials over the row's lanes;
-//   softmax: online, with a wavefront-uniform running max m (exp2 with
-//            log2(e) folded into the scale); the sums l and the outputs o stay
-//            per-lane partials rescaled by the same factor, reduced once at
-//            the end, so only the max crosses lanes per sub-tile;
-//   values : each lane accumulates its V slice weighted by the row's
-//            probability for the G heads in fp32.
-// The wavefronts' (m, l, o) are merged through LDS at the end.  With one split
-// the normalised output is written directly; otherwise the split's state goes
-// to the workspace and a merge kernel combines the splits in a fixed order.
-// All reductions have a fixed order, so results are deterministic.
+// whenever the units fill the chip), z = group of up to 8 q heads of the KV
+// head.  A workgroup serves all the q heads of its group, so each K/V row is
+// read from HBM once per step (twice for 16-head groups).
+//
+// Memory side.  The split's page entries are staged in LDS once (one round
+// trip, overlapped with the query loads); every wavefront owns one contiguous
+// range of rows and streams it through a private LDS ring with direct
+// global->LDS loads, NS - 1 steps ahead of its arithmetic, without holding
+// registers for the data in flight and without workgroup barriers.
+//
+// Arithmetic side.  LPR lanes cover one row, each with E = d / LPR elements
+// (LPR = 4 for up to 2 heads at d = 128, 8 for 4 heads, 16 for 8 heads, so
+// the output accumulators fit in registers); a wavefront step covers 64 / LPR
+// rows.
+//   logits : each lane dots its slices of q (held in registers) with its K
+//            slices (v_dot2_f32_bf16 for bf16, fp32 accumulation); DPP adds
+//            sum the partials over the row's LPR lanes;
+//   softmax: online, against a wavefront-uniform reference max per head that
+//            is raised only when a logit passes it by more than 2^16 (exp2,
+//            log2(e) folded into the scale), so the outputs are rescaled
+//            only on those rare steps;
+//   values : each lane accumulates its V slices weighted by the row's
+//            probability for every head in fp32.
+// At the end the row groups are summed with DPP adds, and the partial states
+// of the DPP rows of all wavefronts are merged through LDS with (max, sum,
+// output) rescaling.  With one split the normalised output is written
+// directly; otherwise the split's state goes to the workspace and a merge
+// kernel combines the splits in a fixed order.  All reductions have a fixed
+// order, so results are deterministic.
 #include "sg_internal.h"
 
 namespace sg {
@@ -34,27 +44,26 @@ __device__ __forceinline__ bf16x2 as_bf16x2(uint32_t w) {
     return r;
 }
 
-// partial dot product of one 16-byte slice of q with the same slice of a K row
+// acc + the dot product of one 16-byte slice of q with the same slice of a K
+// row (fp32 accumulation)
 template <typename T>
 struct SliceDot;
 template <>
-struct SliceDot<uint16_t> {   // bf16: four v_dot2_f32_bf16, fp32 accumulation
-    __device__ static float run(const v4u &q, const v4u &k) {
-        float a = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.x), as_bf16x2(k.x), 0.f, false);
-        float b = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.y), as_bf16x2(k.y), 0.f, false);
-        a = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.z), as_bf16x2(k.z), a, false);
-        b = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.w), as_bf16x2(k.w), b, false);
-        return a + b;
+struct SliceDot<uint16_t> {   // bf16: four chained v_dot2_f32_bf16
+    __device__ static float run(const v4u &q, const v4u &k, float acc) {
+        acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.x), as_bf16x2(k.x), acc, false);
+        acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.y), as_bf16x2(k.y), acc, false);
+        acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.z), as_bf16x2(k.z), acc, false);
+        return __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.w), as_bf16x2(k.w), acc, false);
     }
 };
 template <>
 struct SliceDot<float> {
-    __device__ static float run(const v4u &q, const v4u &k) {
-        float a = __uint_as_float(q.x) * __uint_as_float(k.x);
-        float b = __uint_as_float(q.y) * __uint_as_float(k.y);
-        a = fmaf(__uint_as_float(q.z), __uint_as_float(k.z), a);
-        b = fmaf(__uint_as_float(q.w), __uint_as_float(k.w), b);
-        return a + b;
+    __device__ static float run(const v4u &q, const v4u &k, float acc) {
+        acc = fmaf(__uint_as_float(q.x), __uint_as_float(k.x), acc);
+        acc = fmaf(__uint_as_float(q.y), __uint_as_float(k.y), acc);
+        acc = fmaf(__uint_as_float(q.z), __uint_as_float(k.z), acc);
+        return fmaf(__uint_as_float(q.w), __uint_as_float(k.w), acc);
     }
 };
 
@@ -77,16 +86,33 @@ struct Elem<uint16_t> {  // bfloat16 bits
     }
 };
 
-template <int G>
+// Work shape for HG heads per workgroup.
+//   LPR  lanes per row: at least 4, and enough that the HG * E output
+//        accumulators stay within 64 registers and the query slices within
+//        32 (two wavefronts per SIMD, no spills);
+//   VPL  16-byte vectors per lane per row; a step moves VPL KB of K and of V;
+//   ring up to 128 KB of LDS: WAVES wavefronts (8 where two slots fit) of NS
+//        slots (at most 8).
+template <typename T, int D, int HG>
 struct DecodeShape {
-    // wavefronts per workgroup: sixteen (four per SIMD at <= 128 registers)
-    // keep enough loads in flight per CU; more heads need more accumulators
-    // and LDS for the final merge, so fewer wavefronts
-    static constexpr int WAVES = G <= 4 ? 16 : (G == 8 ? 8 : 4);
-    // rows per wavefront sub-tile (register budget: K, V slices and logits)
-    static constexpr int SUB = G <= 2 ? 32 : 16;
-    static constexpr int64_t ROWS_PER_PASS = (int64_t)SUB * WAVES;
+    static constexpr int ESZ = (int)sizeof(T);
+    static constexpr int LPR_A = HG * D / 64, LPR_B = HG * D * ESZ / 128;
+    static constexpr int LPR_C = LPR_A > LPR_B ? LPR_A : LPR_B;
+    static constexpr int LPR = LPR_C < 4 ? 4 : (LPR_C > 16 ? 16 : LPR_C);
+    static constexpr int E = D / LPR;
+    static constexpr int VPL = D * ESZ / 16 / LPR;
+    static constexpr int RPS = 64 / LPR;
+    static constexpr int STEPB = VPL * 1024;
+    static constexpr int SLOTB = 2 * STEPB;
+    static constexpr int RINGB_MAX = 128 * 1024;
+    static constexpr int WAVES = RINGB_MAX / (2 * SLOTB) >= 8 ? 8 : RINGB_MAX / (2 * SLOTB);
+    static constexpr int NS = RINGB_MAX / (WAVES * SLOTB) > 8 ? 8 : RINGB_MAX / (WAVES * SLOTB);
+    static_assert(LPR <= 16 && VPL >= 1 && NS >= 2 && WAVES >= 1, "decode work shape");
 };
+constexpr int DEC_MAX_HG = 8;       // heads served by one workgroup; larger groups use several
+constexpr int DEC_PT_CAP = 2048;    // page entries of one split staged in LDS
+constexpr int DEC_MIN_SPLIT_ROWS = 128;
+constexpr float DEC_LAZY = 16.f;    // log2 headroom before the reference max is raised
 
 // partial state of one split: per head (m, l) then o[d]
 __device__ __forceinline__ float *part_ptr(float *ws, int64_t unit, int nsplit, int split, int G, int d) {
@@ -104,7 +130,7 @@ constexpr int DPP_HALF_MIRROR = 0x141;
 constexpr int DPP_ROR4 = 0x124;
 constexpr int DPP_ROR8 = 0x128;
 
-// sum over each group of N consecutive lanes (N = 8, 16 or 32); every lane of
+// sum over each group of N consecutive lanes (N = 4, 8 or 16); every lane of
 // the group receives the group's sum
 template <int N>
 __device__ __forceinline__ float group_sum(float x) {
@@ -112,149 +138,248 @@ __device__ __forceinline__ float group_sum(float x) {
     x += dpp<DPP_XOR2>(x);
     if constexpr (N == 8) {
         x += dpp<DPP_HALF_MIRROR>(x);
-    } else {
+    } else if constexpr (N == 16) {
         x += dpp<DPP_ROR4>(x);
         x += dpp<DPP_ROR8>(x);
-        if constexpr (N == 32) x += __shfl_xor(x, 16, 64);
     }
     return x;
 }
 
-template <typename T, int D, int G, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void decode_kernel(
+// sum over the 16 / N lanes of a 16-lane DPP row that sit N apart (lanes
+// holding the same slice of different rows); every such lane receives it
+template <int N>
+__device__ __forceinline__ float row_groups_sum(float x) {
+    if constexpr (N <= 4) x += dpp<DPP_ROR4>(x);
+    if constexpr (N <= 8) x += dpp<DPP_ROR8>(x);
+    return x;
+}
+
+// Grid: x = (sequence, KV head) unit, y = split of the unit's rows, z = group
+// of HG q heads within the KV head's G.  See the top of the file.
+template <typename T, int D, int HG>
+__global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_kernel(
     int Hq, int Hkv, float scale_log2, const T *__restrict__ q, const v4u *__restrict__ k_pool,
     const v4u *__restrict__ v_pool, int64_t pool_rows, const int32_t *__restrict__ page_table,
-    const int32_t *__restrict__ n_rows, int page_size, int page_shift, int max_pages, int64_t split_rows,
-    float *__restrict__ out, float *__restrict__ ws) {
+    const int32_t *__restrict__ n_rows, int page_size, uint32_t page_mul, int page_shift, int max_pages,
+    int64_t split_rows, float *__restrict__ out, float *__restrict__ ws) {
+    using S = DecodeShape<T, D, HG>;
     constexpr int PER16 = Elem<T>::PER16;  // elements per 16-byte vector
-    constexpr int CPR = D / PER16;         // lanes per row (one vector each)
-    constexpr int RPS = 64 / CPR;          // rows per wavefront step
-    constexpr int SUB = DecodeShape<G>::SUB;
-    constexpr int STEPS = SUB / RPS;       // steps per sub-tile
-    __shared__ float m_s[WAVES][G], l_s[WAVES][G];
-    __shared__ float o_s[WAVES][G][D];
+    constexpr int LPR = S::LPR, VPL = S::VPL, RPS = S::RPS, WAVES = S::WAVES, NS = S::NS;
+    constexpr int STEPB = S::STEPB, SLOTB = S::SLOTB;
+    constexpr int CPR = D / PER16;         // 16-byte vectors per row
+    constexpr int NPART = WAVES * 4;       // partial states: the 4 DPP rows of every wavefront
+    constexpr int RINGB = WAVES * NS * SLOTB, MERGEB = NPART * HG * D * 4;
+    static_assert((NS - 1) * 2 * VPL <= 63, "loads in flight per wavefront");
+    __shared__ __attribute__((aligned(16))) char ring[RINGB > MERGEB ? RINGB : MERGEB];   // the merge reuses it
+    __shared__ int32_t pte[DEC_PT_CAP];
+    __shared__ float m_s[WAVES][HG], l_s[NPART][HG];
 
     const int64_t unit = blockIdx.x;        // b * Hkv + h
     const int b = (int)(unit / Hkv), h = (int)(unit % Hkv);
     const int split = blockIdx.y, nsplit = gridDim.y;
+    const int G = Hq / Hkv;
+    const int gq0 = h * G + (int)blockIdx.z * HG;      // first q head served
     const int tid = threadIdx.x, lane = tid % 64;
     const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
-    const int cg = lane % CPR, rsub = lane / CPR;
-    int64_t n = n_rows[unit];
-    n = max<int64_t>(0, min<int64_t>(n, (int64_t)max_pages * page_size));
-    const int64_t r0 = (int64_t)split * split_rows;
-    const int64_t r1 = min<int64_t>(n, r0 + split_rows);
-    const int32_t *pt = page_table + unit * max_pages;
+    const int c = lane % LPR, r = lane / LPR;       // slice within the row, row within the step
 
-    // this lane's 16-byte slice (vector cg) of each of the G query vectors
-    v4u qs[G];
+    // this lane's slices of the HG query vectors: vectors j * LPR + c, j < VPL
+    v4u qs[HG][VPL];
     {
-        const v4u *qv = reinterpret_cast<const v4u *>(q + ((int64_t)b * Hq + (int64_t)h * G) * D);
+        const v4u *qv = reinterpret_cast<const v4u *>(q + ((int64_t)b * Hq + gq0) * D);
 #pragma unroll
-        for (int g = 0; g < G; ++g) qs[g] = qv[g * CPR + cg];
+        for (int g = 0; g < HG; ++g)
+#pragma unroll
+            for (int j = 0; j < VPL; ++j) qs[g][j] = qv[g * CPR + j * LPR + c];
     }
-    // running state: m is wavefront-uniform; l and o are per-lane partials
-    // (over the rows this lane visits) and are reduced at the end
-    float m[G], l[G], o[G][PER16];
+    // page entries covering the split's rows [r0, r0 + split_rows)
+    const int64_t max_rows = (int64_t)max_pages * page_size;
+    const int64_t r0 = (int64_t)split * split_rows;
+    const int64_t pg0 = r0 / page_size;
+    const int64_t pg1 = min<int64_t>(max_pages, ceil_div(min<int64_t>(max_rows, r0 + split_rows), page_size));
+    const int npg = (int)min<int64_t>(DEC_PT_CAP, max<int64_t>(0, pg1 - pg0));   // the host keeps it within the cap
+    const int32_t *pt = page_table + unit * max_pages + pg0;
+    for (int i = tid; i < npg; i += 64 * WAVES) pte[i] = pt[i];
+
+    int64_t n = n_rows[unit];
+    n = max<int64_t>(0, min<int64_t>(n, max_rows));
+    // rows whose pages lie past the staged entries are not reached (the host
+    // sizes splits so that this never cuts anything)
+    const int64_t r1 = min<int64_t>(min<int64_t>(n, r0 + split_rows), (pg0 + npg) * (int64_t)page_size);
+    const int64_t len = pool_rows > 0 ? max<int64_t>(0, r1 - r0) : 0;     // an empty pool: every row is skipped
+    const int64_t per = ceil_div(ceil_div(len, WAVES), RPS) * RPS;
+    const int64_t w0 = r0 + (int64_t)wave * per;
+    const int64_t w1 = min<int64_t>(r0 + len, w0 + per);
+    // the query slices are used first inside the loop; waiting for them here
+    // keeps the compiler from placing that wait inside the loop, where it
+    // would also drain the ring's loads (it does not see them)
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
+    for (int g = 0; g < HG; ++g)
+#pragma unroll
+        for (int j = 0; j < VPL; ++j) asm volatile("" ::"v"(qs[g][j]));
+    __syncthreads();    // page entries staged
+
+    // m: reference max per head, wavefront-uniform; l and o: this lane's
+    // partials over the rows of its row group
+    float m[HG], l[HG], o[HG][VPL][PER16];
+#pragma unroll
+    for (int g = 0; g < HG; ++g) {
         m[g] = -INFINITY;
         l[g] = 0.f;
 #pragma unroll
-        for (int e = 0; e < PER16; ++e) o[g][e] = 0.f;
+        for (int j = 0; j < VPL; ++j)
+#pragma unroll
+            for (int e = 0; e < PER16; ++e) o[g][j][e] = 0.f;
     }
 
-    for (int64_t t0 = r0 + (int64_t)wave * SUB; t0 < r1; t0 += (int64_t)SUB * WAVES) {
-        int prow[STEPS];
-        v4u kv[STEPS], vv[STEPS];
+    // pool row of logical row lr, or -1 (past the range or outside the pool).
+    // rel < npg * page_size <= max_rows <= 2^30, and rel / page_size is the
+    // exact multiply-shift (rel * page_mul) >> page_shift set up by the host
+    auto pool_row = [&](int64_t lr) -> int {
+        const uint32_t rel = (uint32_t)(min<int64_t>(lr, w1 - 1) - pg0 * page_size);
+        const uint32_t pi = (uint32_t)(((uint64_t)rel * page_mul) >> page_shift);
+        const int64_t x = (int64_t)pte[pi] + (int)(rel - pi * (uint32_t)page_size);
+        return (lr < w1 && x >= 0 && x < pool_rows) ? (int)x : -1;
+    };
+    char *myring = ring + wave * (NS * SLOTB);
+    // the loads of the step at row t into ring slot `slot`: vector j * LPR + c
+    // of the lane's row lands at slot + j KB + 16 lane.  A row left out reads
+    // pool row 0 (in bounds: the pool is not empty when a wavefront has rows;
+    // the repeated address stays in L2) and its bit in `valid` clears.
+    auto issue = [&](int64_t t, int slot, unsigned &valid) {
+        char *sb = myring + slot * SLOTB;
+        const int pr = pool_row(t + r);
+        const int64_t off = (int64_t)max(pr, 0) * CPR + c;
 #pragma unroll
-        for (int st = 0; st < STEPS; ++st) {
-            // logical rows fit in 31 bits and pool rows too (host checks)
-            const int lr = (int)(t0 + st * RPS + rsub);
-            int pr = -1;
-            if (lr < r1) {
-                const int pg = page_shift >= 0 ? (lr >> page_shift) : lr / page_size;
-                const int64_t x = (int64_t)pt[pg] + (lr - pg * page_size);
-                if (x >= 0 && x < pool_rows) pr = (int)x;
-            }
-            prow[st] = pr;
+        for (int j = 0; j < VPL; ++j) {
+            dma16_nt(k_pool + off + j * LPR, lds_addr(sb + j * 1024));
+            dma16_nt(v_pool + off + j * LPR, lds_addr(sb + STEPB + j * 1024));
+        }
+        valid = (valid & ~(1u << slot)) | ((pr >= 0 ? 1u : 0u) << slot);
+    };
+    // logits of the lane's row for every head (log2 units; -inf for a row
+    // left out), and whether any passes its reference max by more than
+    // DEC_LAZY anywhere in the wavefront
+    auto logits = [&](const char *sb, bool ok, float (&z)[HG]) -> bool {
+        v4u kv[VPL];
+#pragma unroll
+        for (int j = 0; j < VPL; ++j) kv[j] = *reinterpret_cast<const v4u *>(sb + j * 1024 + lane * 16);
+        bool grow = false;
+#pragma unroll
+        for (int g = 0; g < HG; ++g) {
+            float a = 0.f;
+#pragma unroll
+            for (int j = 0; j < VPL; ++j) a = SliceDot<T>::run(qs[g][j], kv[j], a);
+            a = group_sum<LPR>(a);
+            z[g] = ok ? a * scale_log2 : -INFINITY;
+            grow |= z[g] > m[g] + DEC_LAZY;
+        }
+        return __any(grow);
+    };
+    // p = 2^(z - m) into l and, weighted over the lane's V slices, into o
+    auto accumulate = [&](const char *sb, const float (&z)[HG]) {
+        v4u vv[VPL];
+#pragma unroll
+        for (int j = 0; j < VPL; ++j) vv[j] = *reinterpret_cast<const v4u *>(sb + STEPB + j * 1024 + lane * 16);
+        float p[HG];
+#pragma unroll
+        for (int g = 0; g < HG; ++g) {
+            const float ref = m[g] == -INFINITY ? 0.f : m[g];     // nothing seen yet: z is -inf too
+            p[g] = __builtin_amdgcn_exp2f(z[g] - ref);
+            l[g] += p[g];
         }
 #pragma unroll
-        for (int st = 0; st < STEPS; ++st)
-            kv[st] = prow[st] >= 0 ? k_pool[(int64_t)prow[st] * CPR + cg] : v4u{0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int st = 0; st < STEPS; ++st)
-            vv[st] = prow[st] >= 0 ? v_pool[(int64_t)prow[st] * CPR + cg] : v4u{0u, 0u, 0u, 0u};
-
-        // logits: partial dot over this lane's vector, summed over the row's lanes
-        float z[STEPS][G];
-#pragma unroll
-        for (int st = 0; st < STEPS; ++st) {
-#pragma unroll
-            for (int g = 0; g < G; ++g) {
-                const float a = group_sum<CPR>(SliceDot<T>::run(qs[g], kv[st]));
-                z[st][g] = prow[st] >= 0 ? a * scale_log2 : -INFINITY;
-            }
-        }
-        // online softmax with a wavefront-wide running max
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            float mx = z[0][g];
-#pragma unroll
-            for (int st = 1; st < STEPS; ++st) mx = fmaxf(mx, z[st][g]);
-#pragma unroll
-            for (int off = CPR; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-            const float mn = fmaxf(m[g], mx);
-            if (mn == -INFINITY) continue;            // nothing usable yet (uniform)
-            const float alpha = __builtin_amdgcn_exp2f(m[g] - mn);
-            m[g] = mn;
-            float ls = 0.f;
-#pragma unroll
-            for (int st = 0; st < STEPS; ++st) {
-                z[st][g] = __builtin_amdgcn_exp2f(z[st][g] - mn);   // z now holds p
-                ls += z[st][g];
-            }
-            l[g] = l[g] * alpha + ls;
-#pragma unroll
-            for (int e = 0; e < PER16; ++e) o[g][e] *= alpha;
-        }
-        // values
-#pragma unroll
-        for (int st = 0; st < STEPS; ++st) {
+        for (int j = 0; j < VPL; ++j) {
             float x[PER16];
-            Elem<T>::unpack(vv[st], x);
+            Elem<T>::unpack(vv[j], x);
 #pragma unroll
-            for (int g = 0; g < G; ++g) {
-                const float p = m[g] == -INFINITY ? 0.f : z[st][g];
+            for (int g = 0; g < HG; ++g)
 #pragma unroll
-                for (int e = 0; e < PER16; ++e) o[g][e] = fmaf(p, x[e], o[g][e]);
+                for (int e = 0; e < PER16; ++e) o[g][j][e] = fmaf(p[g], x[e], o[g][j][e]);
+        }
+    };
+    // raise every head's reference max to cover z (rare)
+    auto rescale = [&](const float (&z)[HG]) {
+#pragma unroll
+        for (int g = 0; g < HG; ++g) {
+            const float mn = fmaxf(m[g], wave_max(z[g]));
+            const float alpha = mn == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m[g] - mn);   // 0 while nothing was seen
+            l[g] *= alpha;
+#pragma unroll
+            for (int j = 0; j < VPL; ++j)
+#pragma unroll
+                for (int e = 0; e < PER16; ++e) o[g][j][e] *= alpha;
+            m[g] = mn;
+        }
+    };
+
+    if (w0 < w1) {      // wavefront-uniform
+        const int nst = (int)ceil_div(w1 - w0, RPS);
+        unsigned valid = 0u;
+#pragma unroll
+        for (int s = 0; s < NS - 1; ++s) issue(w0 + (int64_t)s * RPS, s, valid);
+        // The hot loop has no rescale in it (a rescale inside makes the
+        // compiler copy every accumulator each step): a step whose logits
+        // would pass the reference leaves the loop, is rescaled and
+        // accumulated outside, and the loop resumes at the next step.
+        int i = 0;
+        float z[HG];
+        for (;;) {
+            bool grew = false;
+            for (; i < nst; ++i) {
+                // past the range these loads read pool row 0 (kept uniform so
+                // the wait below is a constant)
+                issue(w0 + (int64_t)(i + NS - 1) * RPS, (i + NS - 1) % NS, valid);
+                wait_vmem<(NS - 1) * 2 * VPL>();          // step i has landed
+                const char *sb = myring + (i % NS) * SLOTB;
+                if (logits(sb, (valid >> (i % NS)) & 1u, z)) {
+                    grew = true;
+                    break;
+                }
+                accumulate(sb, z);
             }
+            if (!grew) break;
+            rescale(z);
+            accumulate(myring + (i % NS) * SLOTB, z);
+            ++i;
         }
+        wait_vmem<0>();     // the ring is reused below
     }
-    // reduce l and o over the row groups of the wavefront (lanes sharing cg)
+
+    // sum the row groups within each 16-lane DPP row (m is wavefront-uniform)
 #pragma unroll
-    for (int off = CPR; off < 64; off <<= 1)
+    for (int g = 0; g < HG; ++g) {
+        l[g] = row_groups_sum<LPR>(l[g]);
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            l[g] += __shfl_xor(l[g], off, 64);
+        for (int j = 0; j < VPL; ++j)
 #pragma unroll
-            for (int e = 0; e < PER16; ++e) o[g][e] += __shfl_xor(o[g][e], off, 64);
-        }
-    if (rsub == 0) {
+            for (int e = 0; e < PER16; ++e) o[g][j][e] = row_groups_sum<LPR>(o[g][j][e]);
+    }
+    __syncthreads();    // every wavefront is done with its ring
+    float *o_s = reinterpret_cast<float *>(ring);       // [NPART][HG][D]
+    const int part = wave * 4 + lane / 16;
+    if (lane % 16 < LPR) {
 #pragma unroll
-        for (int g = 0; g < G; ++g)
+        for (int g = 0; g < HG; ++g)
 #pragma unroll
-            for (int e = 0; e < PER16; ++e) o_s[wave][g][cg * PER16 + e] = o[g][e];
+            for (int j = 0; j < VPL; ++j)
+#pragma unroll
+                for (int e = 0; e < PER16; ++e)
+                    o_s[(part * HG + g) * D + (j * LPR + c) * PER16 + e] = o[g][j][e];
+    }
+    if (lane % 16 == 0) {
+#pragma unroll
+        for (int g = 0; g < HG; ++g) l_s[part][g] = l[g];
     }
     if (lane == 0) {
 #pragma unroll
-        for (int g = 0; g < G; ++g) { m_s[wave][g] = m[g]; l_s[wave][g] = l[g]; }
+        for (int g = 0; g < HG; ++g) m_s[wave][g] = m[g];
     }
     __syncthreads();
 
-    // combine the wavefronts; thread t handles (g, c) pairs
-    for (int i = tid; i < G * D; i += 64 * WAVES) {
-        const int g = i / D, c = i % D;
+    // combine the partial states; thread t handles (g, c) pairs
+    for (int i = tid; i < HG * D; i += 64 * WAVES) {
+        const int g = i / D, cc = i % D;
         float M = -INFINITY;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) M = fmaxf(M, m_s[w][g]);
@@ -263,16 +388,20 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(
 #pragma unroll
             for (int w = 0; w < WAVES; ++w) {
                 const float a = m_s[w][g] > -INFINITY ? __builtin_amdgcn_exp2f(m_s[w][g] - M) : 0.f;
-                Lsum += a * l_s[w][g];
-                O += a * o_s[w][g][c];
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    Lsum += a * l_s[w * 4 + rr][g];
+                    O += a * o_s[((w * 4 + rr) * HG + g) * D + cc];
+                }
             }
         }
+        const int gl = (int)blockIdx.z * HG + g;       // head within the KV group
         if (nsplit == 1) {
-            out[((int64_t)b * Hq + (int64_t)h * G + g) * D + c] = Lsum > 0.f ? O / Lsum : 0.f;
+            out[((int64_t)b * Hq + gq0 + g) * D + cc] = Lsum > 0.f ? O / Lsum : 0.f;
         } else {
-            float *pp = part_ptr(ws, unit, nsplit, split, G, D) + (int64_t)g * (D + 2);
-            if (c == 0) { pp[0] = M; pp[1] = Lsum; }
-            pp[2 + c] = O;
+            float *pp = part_ptr(ws, unit, nsplit, split, G, D) + (int64_t)gl * (D + 2);
+            if (cc == 0) { pp[0] = M; pp[1] = Lsum; }
+            pp[2 + cc] = O;
         }
     }
 }
@@ -315,36 +444,55 @@ static int device_cus() {
     return cus;
 }
 
-template <int G>
-static int max_splits(int64_t max_rows) {
-    return (int)std::max<int64_t>(1, ceil_div(max_rows, DecodeShape<G>::ROWS_PER_PASS));
+// Most splits a call can use (the workspace is sized for it): splits are at
+// least DEC_MIN_SPLIT_ROWS rows long.
+static int64_t max_splits(int64_t max_rows) { return std::max<int64_t>(1, ceil_div(max_rows, DEC_MIN_SPLIT_ROWS)); }
+
+// Rows per split: one split per unit when the units fill the chip, else
+// enough splits to give every CU a workgroup; a split never spans more page
+// entries than the LDS stage holds and starts on a page boundary.
+static int64_t plan_split_rows(int64_t wgs_per_split, int64_t max_rows, int page_size) {
+    int64_t want = 1;
+    if (wgs_per_split < device_cus()) want = ceil_div(device_cus(), wgs_per_split);
+    int64_t rows = std::max<int64_t>(ceil_div(max_rows, want), DEC_MIN_SPLIT_ROWS);
+    rows = std::min<int64_t>(rows, (int64_t)DEC_PT_CAP * page_size);
+    return ceil_div(rows, page_size) * page_size;
 }
 
 template <typename T, int D, int G>
 static int launch_decode(hipStream_t s, int B, int Hq, int Hkv, float scale_log2, const void *q, const void *k_pool,
                          const void *v_pool, int64_t pool_rows, const int32_t *page_table, const int32_t *n_rows,
                          int page_size, int max_pages, float *out, float *ws, size_t ws_bytes) {
-    constexpr int WAVES = DecodeShape<G>::WAVES;
+    constexpr int HG = G < DEC_MAX_HG ? G : DEC_MAX_HG;
+    constexpr int NHG = G / HG;
+    constexpr int WAVES = DecodeShape<T, D, HG>::WAVES;
     const int64_t units = (int64_t)B * Hkv;
     const int64_t max_rows = (int64_t)max_pages * page_size;
-    const int cap = max_splits<G>(max_rows);
-    int nsplit = 1;
-    if (units < device_cus()) nsplit = (int)std::min<int64_t>(cap, ceil_div(device_cus(), units));
-    const int64_t split_rows = ceil_div(ceil_div(max_rows, nsplit), 32) * 32;
-    nsplit = (int)ceil_div(max_rows, split_rows);
+    const int64_t split_rows = plan_split_rows(units * NHG, max_rows, page_size);
+    const int64_t nsplit = ceil_div(max_rows, split_rows);
+    if (nsplit > 65535 || nsplit > max_splits(max_rows)) {
+        set_error("sg_decode_attn: %lld splits of %lld rows are not supported", (long long)nsplit, (long long)split_rows);
+        return SG_EUNSUPPORTED;
+    }
     const size_t need = nsplit > 1 ? (size_t)units * nsplit * G * (D + 2) * sizeof(float) : 0;
     if (need > ws_bytes || (need && !ws)) {
         set_error("sg_decode_attn: workspace %zu < %zu", ws_bytes, need);
         return SG_EWORKSPACE;
     }
-    // page sizes that are powers of two index with a shift (-1: divide)
-    const int page_shift = (page_size & (page_size - 1)) == 0 ? __builtin_ctz((unsigned)page_size) : -1;
-    dim3 grid((unsigned)units, (unsigned)nsplit);
-    decode_kernel<T, D, G, WAVES><<<grid, 64 * WAVES, 0, s>>>(
+    // division by the page size as a multiply-shift, exact for dividends below
+    // 2^30 (Granlund and Montgomery, 1994): with l = ceil(log2 P) and
+    // k = 30 + l, floor(n / P) = (n * ceil(2^k / P)) >> k, and the multiplier
+    // is at most 2^31
+    int lg = 0;
+    while ((1ll << lg) < page_size) ++lg;
+    const int page_shift = 30 + lg;
+    const uint32_t page_mul = (uint32_t)(((1ull << page_shift) + (uint64_t)page_size - 1) / (uint64_t)page_size);
+    dim3 grid((unsigned)units, (unsigned)nsplit, (unsigned)NHG);
+    decode_kernel<T, D, HG><<<grid, 64 * WAVES, 0, s>>>(
         Hq, Hkv, scale_log2, reinterpret_cast<const T *>(q), reinterpret_cast<const v4u *>(k_pool),
-        reinterpret_cast<const v4u *>(v_pool), pool_rows, page_table, n_rows, page_size, page_shift, max_pages,
-        split_rows, out, ws);
-    if (nsplit > 1) decode_merge_kernel<D, G><<<(unsigned)units, 256, 0, s>>>(Hq, Hkv, nsplit, ws, out);
+        reinterpret_cast<const v4u *>(v_pool), pool_rows, page_table, n_rows, page_size, page_mul, page_shift,
+        max_pages, split_rows, out, ws);
+    if (nsplit > 1) decode_merge_kernel<D, G><<<(unsigned)units, 256, 0, s>>>(Hq, Hkv, (int)nsplit, ws, out);
     return launch_status("sg_decode_attn");
 }
 
@@ -369,15 +517,7 @@ using namespace sg;
 extern "C" size_t sg_decode_attn_workspace_size(int B, int Hq, int Hkv, int d, int max_pages, int page_size) {
     if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv != 0 || d <= 0 || max_pages <= 0 || page_size <= 0) return 0;
     const int G = Hq / Hkv;
-    const int64_t max_rows = (int64_t)max_pages * page_size;
-    int cap = 1;
-    switch (G) {
-        case 1: cap = max_splits<1>(max_rows); break;
-        case 2: cap = max_splits<2>(max_rows); break;
-        case 4: cap = max_splits<4>(max_rows); break;
-        case 8: cap = max_splits<8>(max_rows); break;
-        default: cap = max_splits<16>(max_rows); break;
-    }
+    const int64_t cap = max_splits((int64_t)max_pages * page_size);
     if (cap <= 1) return 0;
     return (size_t)B * Hkv * cap * G * (size_t)(d + 2) * sizeof(float);
 }

@@ -103,22 +103,6 @@ __device__ __forceinline__ UnitGeom unit_geom(int64_t u, int B, int Hkv, const i
     return g;
 }
 
-// LDS offset of a workgroup-shared address.
-__device__ __forceinline__ unsigned lds_addr(const char *p) {
-    return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
-}
-
-// Direct global->LDS load: lane i's 16 bytes land at LDS offset lds + 16 i;
-// lds is wavefront-uniform and travels in M0.  Issued from
-// inline assembly: the compiler then neither reorders LDS accesses across them
-// (memory clobber) nor inserts conservative waits for them before unrelated
-// LDS reads; callers wait for completion themselves (vector memory counter)
-// before reading the destination.  The s_nop is the wait state a direct LDS
-// load needs after M0 is written.
-__device__ __forceinline__ void dma16(const char *src, unsigned lds) {
-    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
-}
-
 // K tiles in LDS.  A tile is TK keys of D elements, stored without padding;
 // the 16-byte vector v of key j sits at slot j * VPR + (v ^ (j % VPR)), so the
 // 32 (or 16) lanes reading one fragment column hit distinct banks.  Tiles

@@ -63,4 +63,32 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
+// LDS offset of a workgroup-shared address.
+__device__ __forceinline__ unsigned lds_addr(const void *p) {
+    return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
+}
+
+// Direct global->LDS load: lane i's 16 bytes land at LDS offset lds + 16 i;
+// lds is wavefront-uniform and travels in M0.  Issued from inline assembly:
+// the compiler then neither reorders LDS accesses across them (memory
+// clobber) nor inserts conservative waits for them before unrelated LDS
+// reads; callers wait for completion themselves (vector memory counter)
+// before reading the destination.  The s_nop is the wait state a direct LDS
+// load needs after M0 is written.  The _nt form marks the read non-temporal
+// (streamed data that is not read again soon).
+__device__ __forceinline__ void dma16(const void *src, unsigned lds) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+}
+__device__ __forceinline__ void dma16_nt(const void *src, unsigned lds) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(src), "{m0}"(lds) : "memory");
+}
+
+// Wait until at most N vector memory operations of this wavefront are in
+// flight (direct LDS loads included); a compiler barrier for memory.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 }  // namespace sg

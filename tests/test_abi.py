@@ -54,7 +54,7 @@ def test_sizes(lib):
     # 256 units (32 layers x 8 heads) at 8192 keys: 2048-key chunks
     assert smartgen.score_workspace_size(1, 32, 32, 8, 128, 64, 8192) == 256 * 4 * 256 * 8
     assert smartgen.decode_workspace_size(1, 32, 8, 128, 1, 16) == 0          # one split: no workspace
-    assert smartgen.decode_workspace_size(2, 32, 8, 128, 64, 16) == 2 * 8 * 4 * 4 * 130 * 4   # <= 4 splits of 256 rows
+    assert smartgen.decode_workspace_size(2, 32, 8, 128, 64, 16) == 2 * 8 * 8 * 4 * 130 * 4   # <= 8 splits of 128 rows
 
 
 P = ctypes.c_void_p(16)   # never dereferenced: every call below fails validation first
