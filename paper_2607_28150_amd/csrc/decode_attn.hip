@@ -8,8 +8,9 @@
 // Memory side.  The split's page entries are staged in LDS once (one round
 // trip, overlapped with the query loads); every wavefront owns one contiguous
 // range of rows and streams it through a private LDS ring with direct
-// global->LDS loads, NS - 1 steps ahead of its arithmetic, without holding
-// registers for the data in flight and without workgroup barriers.
+// global->LDS loads (non-temporal), NS - 1 steps ahead of its arithmetic,
+// without holding registers for the data in flight and without workgroup
+// barriers.
 //
 // Arithmetic side.  LPR lanes cover one row, each with E = d / LPR elements
 // (LPR = 4 for up to 2 heads at d = 128, 8 for 4 heads, 16 for 8 heads, so
@@ -89,10 +90,13 @@ struct Elem<uint16_t> {  // bfloat16 bits
 // Work shape for HG heads per workgroup.
 //   LPR  lanes per row: at least 4, and enough that the HG * E output
 //        accumulators stay within 64 registers and the query slices within
-//        32 (two wavefronts per SIMD, no spills);
+//        32;
 //   VPL  16-byte vectors per lane per row; a step moves VPL KB of K and of V;
-//   ring up to 128 KB of LDS: WAVES wavefronts (8 where two slots fit) of NS
-//        slots (at most 8).
+//   ring four wavefronts (one per SIMD), each with NS slots, so that about
+//        12 KB per wavefront (48 KB per workgroup) are in flight.  Measured on
+//        MI355X: deeper rings or more wavefronts per CU lower the bandwidth
+//        these gathers reach (more outstanding requests per CU than the
+//        memory system serves well), shallower ones leave it idle.
 template <typename T, int D, int HG>
 struct DecodeShape {
     static constexpr int ESZ = (int)sizeof(T);
@@ -104,10 +108,10 @@ struct DecodeShape {
     static constexpr int RPS = 64 / LPR;
     static constexpr int STEPB = VPL * 1024;
     static constexpr int SLOTB = 2 * STEPB;
-    static constexpr int RINGB_MAX = 128 * 1024;
-    static constexpr int WAVES = RINGB_MAX / (2 * SLOTB) >= 8 ? 8 : RINGB_MAX / (2 * SLOTB);
-    static constexpr int NS = RINGB_MAX / (WAVES * SLOTB) > 8 ? 8 : RINGB_MAX / (WAVES * SLOTB);
-    static_assert(LPR <= 16 && VPL >= 1 && NS >= 2 && WAVES >= 1, "decode work shape");
+    static constexpr int WAVES = 4;
+    static constexpr int NS_A = 1 + (12 * 1024 + SLOTB - 1) / SLOTB;
+    static constexpr int NS = NS_A < 2 ? 2 : (NS_A > 8 ? 8 : NS_A);
+    static_assert(LPR <= 16 && VPL >= 1, "decode work shape");
 };
 constexpr int DEC_MAX_HG = 8;       // heads served by one workgroup; larger groups use several
 constexpr int DEC_PT_CAP = 2048;    // page entries of one split staged in LDS
@@ -364,8 +368,9 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
 #pragma unroll
             for (int j = 0; j < VPL; ++j)
 #pragma unroll
-                for (int e = 0; e < PER16; ++e)
-                    o_s[(part * HG + g) * D + (j * LPR + c) * PER16 + e] = o[g][j][e];
+                for (int e = 0; e < PER16; e += 4)
+                    *reinterpret_cast<float4 *>(o_s + (part * HG + g) * D + (j * LPR + c) * PER16 + e) =
+                        make_float4(o[g][j][e], o[g][j][e + 1], o[g][j][e + 2], o[g][j][e + 3]);
     }
     if (lane % 16 == 0) {
 #pragma unroll
@@ -377,31 +382,41 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     }
     __syncthreads();
 
-    // combine the partial states; thread t handles (g, c) pairs
-    for (int i = tid; i < HG * D; i += 64 * WAVES) {
-        const int g = i / D, cc = i % D;
+    // combine the partial states; thread t handles four consecutive columns
+    // (g, cc .. cc + 3)
+    for (int i = tid; i < HG * D / 4; i += 64 * WAVES) {
+        const int g = 4 * i / D, cc = 4 * i % D;
         float M = -INFINITY;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) M = fmaxf(M, m_s[w][g]);
-        float Lsum = 0.f, O = 0.f;
+        float Lsum = 0.f;
+        float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
         if (M > -INFINITY) {
 #pragma unroll
             for (int w = 0; w < WAVES; ++w) {
                 const float a = m_s[w][g] > -INFINITY ? __builtin_amdgcn_exp2f(m_s[w][g] - M) : 0.f;
 #pragma unroll
                 for (int rr = 0; rr < 4; ++rr) {
-                    Lsum += a * l_s[w * 4 + rr][g];
-                    O += a * o_s[((w * 4 + rr) * HG + g) * D + cc];
+                    const float4 x = *reinterpret_cast<const float4 *>(o_s + ((w * 4 + rr) * HG + g) * D + cc);
+                    Lsum = fmaf(a, l_s[w * 4 + rr][g], Lsum);
+                    O.x = fmaf(a, x.x, O.x);
+                    O.y = fmaf(a, x.y, O.y);
+                    O.z = fmaf(a, x.z, O.z);
+                    O.w = fmaf(a, x.w, O.w);
                 }
             }
         }
+        const float ov[4] = {O.x, O.y, O.z, O.w};
         const int gl = (int)blockIdx.z * HG + g;       // head within the KV group
         if (nsplit == 1) {
-            out[((int64_t)b * Hq + gq0 + g) * D + cc] = Lsum > 0.f ? O / Lsum : 0.f;
+            float *po = out + ((int64_t)b * Hq + gq0 + g) * D + cc;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) po[k] = Lsum > 0.f ? ov[k] / Lsum : 0.f;
         } else {
             float *pp = part_ptr(ws, unit, nsplit, split, G, D) + (int64_t)gl * (D + 2);
             if (cc == 0) { pp[0] = M; pp[1] = Lsum; }
-            pp[2 + cc] = O;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) pp[2 + cc + k] = ov[k];
         }
     }
 }
