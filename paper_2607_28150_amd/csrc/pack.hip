@@ -3,25 +3,30 @@
 // One workgroup covers ROWS rows of one (unit, request) segment; CPR lanes
 // (16 bytes each) cover one row, so a wavefront moves 64/CPR whole rows per
 // instruction and every global access is a fully used 16-byte vector.  The
-// K and V loads of all rows a thread owns are issued before any store to keep
-// several vectors in flight per lane; stores are non-temporal (the transfer
-// buffer is written once and read by a later phase or by the host link).
+// index, K and V loads of all rows a thread owns are issued before any result
+// is used, so several vectors are in flight per lane; loads and stores are
+// non-temporal (the source is read once, the transfer buffer is written once
+// and read by a later phase or by the host link).
 #include "sg_internal.h"
 
 namespace sg {
 
 constexpr int PACK_THREADS = 256;
-constexpr int PACK_UNROLL = 4;
+constexpr int PACK_UNROLL = 2;
 
 template <int CPR>
 __global__ __launch_bounds__(PACK_THREADS) void pack_kernel(
     int B, int Hkv, const int32_t *__restrict__ cu_seqlens, int64_t T,
     const int32_t *__restrict__ cu_k, int64_t K_total, const v4u *__restrict__ k,
     const v4u *__restrict__ v, int64_t kv_layer_rows, const int32_t *__restrict__ idx,
-    v4u *__restrict__ dk, v4u *__restrict__ dv, int32_t *__restrict__ didx) {
+    v4u *__restrict__ dk, v4u *__restrict__ dv, int32_t *__restrict__ didx, int nchunk) {
     constexpr int RPI = PACK_THREADS / CPR;          // rows per iteration of the block
     constexpr int ROWS = RPI * PACK_UNROLL;           // rows per block pass
-    const int y = blockIdx.x;
+    // one-dimensional grid, segment-major: consecutive workgroups take
+    // consecutive chunks of one (unit, request) segment, so the rows in flight
+    // at a time stay close together (measured faster than chunk-major order)
+    const int y = (int)(blockIdx.x / (unsigned)nchunk);
+    const int chunk = (int)(blockIdx.x % (unsigned)nchunk);
     const int b = y % B;
     const int u = y / B;                              // l * Hkv + h
     const int l = u / Hkv, h = u % Hkv;
@@ -35,34 +40,59 @@ __global__ __launch_bounds__(PACK_THREADS) void pack_kernel(
     const int lane = threadIdx.x % CPR;
     const int rsub = threadIdx.x / CPR;
 
-    for (int64_t base = (int64_t)blockIdx.y * ROWS; base < kb; base += (int64_t)gridDim.y * ROWS) {
-        v4u kr[PACK_UNROLL], vr[PACK_UNROLL];
+    if (nb == 0) {      // a request without tokens: every index is invalid, so zero rows
+        for (int64_t base = (int64_t)chunk * ROWS; base < kb; base += (int64_t)nchunk * ROWS) {
 #pragma unroll
-        for (int j = 0; j < PACK_UNROLL; ++j) {
-            const int64_t i = base + rsub + j * RPI;
-            kr[j] = v4u{0u, 0u, 0u, 0u};
-            vr[j] = v4u{0u, 0u, 0u, 0u};
-            if (i < kb) {
-                const int32_t t = idx[slot0 + i];
-                if (t >= 0 && t < nb) {
-                    const int64_t src = (src0 + t) * CPR + lane;
-                    kr[j] = __builtin_nontemporal_load(k + src);
-                    vr[j] = __builtin_nontemporal_load(v + src);
+            for (int j = 0; j < PACK_UNROLL; ++j) {
+                const int64_t i = base + rsub + j * RPI;
+                if (i < kb) {
+                    const int64_t dst = (slot0 + i) * CPR + lane;
+                    __builtin_nontemporal_store(v4u{0u, 0u, 0u, 0u}, dk + dst);
+                    __builtin_nontemporal_store(v4u{0u, 0u, 0u, 0u}, dv + dst);
                 }
             }
+            if (threadIdx.x < ROWS) {
+                const int64_t i = base + threadIdx.x;
+                if (i < kb) didx[slot0 + i] = idx[slot0 + i];
+            }
         }
+        return;
+    }
+    // Every load of a pass is issued before any result is used: the indices
+    // first (rows past the segment read its last index), then the K and V
+    // rows (an invalid index reads row 0 of the request and is zeroed
+    // afterwards).  Loads behind branches would make each wait for all the
+    // loads before it.
+    for (int64_t base = (int64_t)chunk * ROWS; base < kb; base += (int64_t)nchunk * ROWS) {
+        int32_t t[PACK_UNROLL];
+#pragma unroll
+        for (int j = 0; j < PACK_UNROLL; ++j) t[j] = idx[slot0 + min<int64_t>(base + rsub + j * RPI, kb - 1)];
+        __builtin_amdgcn_sched_barrier(0);      // every index load ahead of the row loads
+        v4u kr[PACK_UNROLL], vr[PACK_UNROLL];
+        bool ok[PACK_UNROLL];
+#pragma unroll
+        for (int j = 0; j < PACK_UNROLL; ++j) {
+            ok[j] = t[j] >= 0 && t[j] < nb;
+            const int64_t src = (src0 + (ok[j] ? t[j] : 0)) * CPR + lane;
+            kr[j] = __builtin_nontemporal_load(k + src);
+            vr[j] = __builtin_nontemporal_load(v + src);
+        }
+        __builtin_amdgcn_sched_barrier(0);      // every row load ahead of the stores
 #pragma unroll
         for (int j = 0; j < PACK_UNROLL; ++j) {
             const int64_t i = base + rsub + j * RPI;
             if (i < kb) {
                 const int64_t dst = (slot0 + i) * CPR + lane;
-                __builtin_nontemporal_store(kr[j], dk + dst);
-                __builtin_nontemporal_store(vr[j], dv + dst);
+                __builtin_nontemporal_store(ok[j] ? kr[j] : v4u{0u, 0u, 0u, 0u}, dk + dst);
+                __builtin_nontemporal_store(ok[j] ? vr[j] : v4u{0u, 0u, 0u, 0u}, dv + dst);
             }
         }
-        if (threadIdx.x < ROWS) {
-            const int64_t i = base + threadIdx.x;
-            if (i < kb) didx[slot0 + i] = idx[slot0 + i];
+        // the index table from the values already loaded (one lane per row);
+        // no second load, so nothing waits for the stores above to complete
+#pragma unroll
+        for (int j = 0; j < PACK_UNROLL; ++j) {
+            const int64_t i = base + rsub + j * RPI;
+            if (lane == 0 && i < kb) didx[slot0 + i] = t[j];
         }
     }
 }
@@ -98,17 +128,17 @@ extern "C" int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,
     v4u *dv = dk + S * cpr;
     int32_t *di = reinterpret_cast<int32_t *>(dv + S * cpr);
     const int rows_per_block = (PACK_THREADS / cpr) * PACK_UNROLL;
-    const int64_t gx = std::min<int64_t>(ceil_div(max_k, rows_per_block), 65535);
     const int64_t units = (int64_t)L * Hkv * B;
-    SG_REQUIRE(units <= 0x7fffffff, SG_EINVAL, "sg_pack: too many units");
-    dim3 grid((unsigned)units, (unsigned)gx);
+    const int64_t nchunk = std::min<int64_t>(ceil_div(max_k, rows_per_block), 65535);
+    SG_REQUIRE(units * nchunk <= 0x7fffffff, SG_EINVAL, "sg_pack: too many units");
+    const dim3 grid((unsigned)(units * nchunk));
     hipStream_t s = as_stream(stream);
     const v4u *kk = reinterpret_cast<const v4u *>(k);
     const v4u *vv = reinterpret_cast<const v4u *>(v);
     switch (cpr) {
-        case 8: pack_kernel<8><<<grid, PACK_THREADS, 0, s>>>(B, Hkv, cu_seqlens, T, cu_k, K_total, kk, vv, kv_layer_rows, idx, dk, dv, di); break;
-        case 16: pack_kernel<16><<<grid, PACK_THREADS, 0, s>>>(B, Hkv, cu_seqlens, T, cu_k, K_total, kk, vv, kv_layer_rows, idx, dk, dv, di); break;
-        case 32: pack_kernel<32><<<grid, PACK_THREADS, 0, s>>>(B, Hkv, cu_seqlens, T, cu_k, K_total, kk, vv, kv_layer_rows, idx, dk, dv, di); break;
+        case 8: pack_kernel<8><<<grid, PACK_THREADS, 0, s>>>(B, Hkv, cu_seqlens, T, cu_k, K_total, kk, vv, kv_layer_rows, idx, dk, dv, di, (int)nchunk); break;
+        case 16: pack_kernel<16><<<grid, PACK_THREADS, 0, s>>>(B, Hkv, cu_seqlens, T, cu_k, K_total, kk, vv, kv_layer_rows, idx, dk, dv, di, (int)nchunk); break;
+        case 32: pack_kernel<32><<<grid, PACK_THREADS, 0, s>>>(B, Hkv, cu_seqlens, T, cu_k, K_total, kk, vv, kv_layer_rows, idx, dk, dv, di, (int)nchunk); break;
         default: set_error("sg_pack: internal row size %d", rowb); return SG_EINTERNAL;
     }
     return launch_status("sg_pack");
