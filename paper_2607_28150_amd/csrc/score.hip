@@ -326,6 +326,9 @@ struct ColsumStep {
     __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
         using M = MT<T, D>;
         const int key = key0 + kb * M::BM + lane % M::BM;
+        // four independent partial sums (one long chain of dependent adds
+        // would stall the wavefront), combined in a fixed order
+        float t[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int g4 = 0; g4 < M::NV / 4; ++g4) {
             int4 pos = make_int4(0, 0, 0, 0);
@@ -334,9 +337,10 @@ struct ColsumStep {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const float p = __builtin_amdgcn_exp2f(acc[4 * g4 + i] * c2);
-                cs[kb] += (!MASK || key <= ps[i]) ? p : 0.f;
+                t[i] += (!MASK || key <= ps[i]) ? p : 0.f;
             }
         }
+        cs[kb] += (t[0] + t[1]) + (t[2] + t[3]);
     }
 };
 
