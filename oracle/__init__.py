@@ -43,7 +43,10 @@ def _load():
                               _vp, _vp, _l]
     lib.sgo_decode_attn.argtypes = [_i, _i, _i, _i, ctypes.c_double, _f32p, _f32p, _f32p, _l, _i32p, _i32p,
                                     _i, _i, _f64p]
-    for f in ("sgo_score", "sgo_topk", "sgo_pack", "sgo_split", "sgo_fetch", "sgo_decode_attn", "sgo_threads"):
+    lib.sgo_block_importance.argtypes = [_i, _i, _i, _i32p, _l, _i, _f32p, _f64p]
+    lib.sgo_pack_blocks.argtypes = [_i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _i, _i32p, _vp]
+    for f in ("sgo_score", "sgo_topk", "sgo_pack", "sgo_split", "sgo_fetch", "sgo_decode_attn", "sgo_threads",
+              "sgo_block_importance", "sgo_pack_blocks"):
         getattr(lib, f).restype = ctypes.c_int
     lib.sgo_set_threads.argtypes = [_i]
     lib.sgo_set_threads.restype = None
@@ -187,4 +190,51 @@ def decode_attn(q, k_pool, v_pool, page_table, n_rows, page_size, scale=None):
                                  kp.shape[0], _p(pt, _i32p), _p(nr, _i32p), int(page_size), int(max_pages),
                                  _p(out, _f64p))
     _check(rc, "decode_attn")
+    return out
+
+
+def block_importance(scores, cu_seqlens, M):
+    """Eq. 1 block importance [B][L][M] float64 from float32 scores [L][Hkv][T]."""
+    sc = _c(scores, np.float32)
+    L, Hkv, T = sc.shape
+    cu = _c(cu_seqlens, np.int32)
+    B = len(cu) - 1
+    out = np.zeros((B, L, M), dtype=np.float64)
+    rc = _load().sgo_block_importance(B, L, Hkv, _p(cu, _i32p), T, int(M), _p(sc, _f32p), _p(out, _f64p))
+    _check(rc, "block_importance")
+    return out
+
+
+def block_budget(M, L, Tp, Tt):
+    """Eq. 2: K_r = M (L - 1) Tp / Tt blocks (an upper bound, so floored), clipped to [2M, L M]."""
+    if M < 1 or L < 1 or not (Tp >= 0) or not (Tt >= 0):
+        raise ValueError("block_budget needs M, L >= 1 and non-negative times")
+    k = L * M if Tt == 0 else int(np.floor(M * (L - 1) * (Tp / Tt)))
+    return min(L * M, max(2 * M, k))
+
+
+def pack_blocks(k, v, ids, s0, N, M, L=None, kv_layer_rows=None):
+    """Block transfer buffer [K rows | V rows | int32 ids] (uint8) of one request.
+    k, v: [Lkv][Hkv][T][d]; L layers (default Lkv); kv_layer_rows: layer stride in rows
+    (default Hkv * T; 0 for one source shared by every layer)."""
+    assert k.dtype == v.dtype and k.shape == v.shape
+    kk = np.ascontiguousarray(k)
+    vv = np.ascontiguousarray(v)
+    ix = _c(ids, np.int32)
+    _, Hkv, T, d = kk.shape
+    return _pack_blocks(kk, vv, ix, s0, N, M, kv_layer_rows, Hkv, T, d, L=L)
+
+
+def _pack_blocks(kk, vv, ix, s0, N, M, kv_layer_rows, Hkv, T, d, L=None):
+    esize = kk.dtype.itemsize
+    if L is None:
+        L = kk.shape[0]
+    if kv_layer_rows is None:
+        kv_layer_rows = Hkv * T
+    Nb = (N + M - 1) // M
+    S = len(ix) * Hkv * Nb
+    out = np.zeros(2 * S * d * esize + 4 * len(ix), dtype=np.uint8)
+    rc = _load().sgo_pack_blocks(L, Hkv, d, esize, T, int(s0), int(N), int(M), kk.ctypes.data, vv.ctypes.data,
+                                 int(kv_layer_rows), len(ix), _p(ix, _i32p), out.ctypes.data)
+    _check(rc, "pack_blocks")
     return out

@@ -351,3 +351,85 @@ int sgo_decode_attn(int B, int Hq, int Hkv, int d, double scale, const float *q,
     }
     return SGO_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Block importance (Section 4.1, eq. 1), over measured per-entry scores.
+ *
+ * Request b with N tokens, layer l: the sequence is cut into M blocks of
+ * Nb = ceil(N / M) tokens; block m holds tokens [m*Nb, min((m+1)*Nb, N)).
+ * A block's entries E are its tokens in every KV head, and
+ *     I[b][l][m] = +inf                                  for l = 0, 1
+ *     I[b][l][m] = (1/|E|) * sum_{(h, t) in E} score[l][h][s0 + t]   otherwise.
+ * A block with no tokens (trailing blocks when N is not a multiple of M)
+ * has no mean; it gets -inf in layers >= 2 (never preferred).
+ */
+int sgo_block_importance(int B, int L, int Hkv, const int32_t *cu_seqlens, int64_t T, int M,
+                         const float *scores, double *out)
+{
+    if (B < 1 || L < 1 || Hkv < 1 || M < 1 || T < 0) return SGO_EINVAL;
+    if (cu_seqlens[0] != 0 || cu_seqlens[B] != T) return SGO_EINVAL;
+    for (int b = 0; b < B; ++b) {
+        const int64_t s0 = cu_seqlens[b], N = cu_seqlens[b + 1] - s0;
+        if (N < 0) return SGO_EINVAL;
+        const int64_t Nb = (N + M - 1) / M;
+        for (int l = 0; l < L; ++l)
+            for (int m = 0; m < M; ++m) {
+                double *o = out + ((int64_t)b * L + l) * M + m;
+                if (l < 2) { *o = INFINITY; continue; }
+                const int64_t t0 = (int64_t)m * Nb;
+                const int64_t t1 = t0 + Nb < N ? t0 + Nb : N;
+                if (t1 <= t0) { *o = -INFINITY; continue; }
+                double sum = 0.0;
+                for (int h = 0; h < Hkv; ++h)
+                    for (int64_t t = t0; t < t1; ++t)
+                        sum += (double)scores[((int64_t)l * Hkv + h) * T + s0 + t];
+                *o = sum / (double)((t1 - t0) * Hkv);
+            }
+    }
+    return SGO_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Block pack (proactive transfer of KV blocks, Section 4.1).
+ *
+ * One request (tokens [s0, s0 + N) of the source rows), blocks of
+ * Nb = ceil(N / M) tokens.  Selected block s has flat id c = l*M + m.  Its
+ * head-h rows go to slots (s*Hkv + h)*Nb + r, r < Nb, of the K region, from
+ * K[l][h][s0 + m*Nb + r]; rows past the prompt end (and every row of an id
+ * outside [0, L*M)) are zero.  Layout: [K rows | V rows | int32 ids].
+ */
+int sgo_pack_blocks(int L, int Hkv, int d, int esize, int64_t T, int64_t s0, int64_t N, int M,
+                    const void *k, const void *v, int64_t kv_layer_rows, int nblk, const int32_t *ids,
+                    void *dst)
+{
+    if (esize != 2 && esize != 4) return SGO_EINVAL;
+    if (L < 1 || Hkv < 1 || M < 1 || N < 0 || nblk < 0) return SGO_EINVAL;
+    const int64_t Nb = (N + M - 1) / M;
+    const int64_t rowb = (int64_t)d * esize;
+    const int64_t S = (int64_t)nblk * Hkv * Nb;
+    unsigned char *Kd = (unsigned char *)dst;
+    unsigned char *Vd = Kd + S * rowb;
+    int32_t *Id = (int32_t *)(Vd + S * rowb);
+    const unsigned char *Ks = (const unsigned char *)k;
+    const unsigned char *Vs = (const unsigned char *)v;
+    for (int s = 0; s < nblk; ++s) {
+        const int32_t c = ids[s];
+        Id[s] = c;
+        const int ok = c >= 0 && (int64_t)c < (int64_t)L * M;
+        const int l = ok ? c / M : 0, m = ok ? c % M : 0;
+        for (int h = 0; h < Hkv; ++h)
+            for (int64_t r = 0; r < Nb; ++r) {
+                const int64_t slot = ((int64_t)s * Hkv + h) * Nb + r;
+                const int64_t t = (int64_t)m * Nb + r;
+                if (!ok || t >= N) {
+                    memset(Kd + slot * rowb, 0, (size_t)rowb);
+                    memset(Vd + slot * rowb, 0, (size_t)rowb);
+                    continue;
+                }
+                const int64_t src = (int64_t)l * kv_layer_rows + (int64_t)h * T + s0 + t;
+                memcpy(Kd + slot * rowb, Ks + src * rowb, (size_t)rowb);
+                memcpy(Vd + slot * rowb, Vs + src * rowb, (size_t)rowb);
+            }
+    }
+    return SGO_OK;
+}

@@ -469,3 +469,111 @@ def test_decode_empty_set_is_zero():
     o = oracle.decode_attn(q, np.ones((4, 4), np.float32), np.ones((4, 4), np.float32),
                            np.zeros((1, 1, 1), np.int32), np.zeros((1, 1), np.int32), 4)
     assert (o == 0).all()
+
+
+# ----------------------------------------------------------------------------- block mode (eq. 1, eq. 2)
+
+def _fl(x):
+    return float(x)                      # "inf" and "-inf" parse to the infinities
+
+
+def test_block_importance_worked_examples():
+    for case in _golden("block_worked.json")["importance"]:
+        L, Hkv, N, M = case["L"], case["Hkv"], case["N"], case["M"]
+        sc = np.arange(L * Hkv * N, dtype=np.float32).reshape(L, Hkv, N)
+        got = oracle.block_importance(sc, [0, N], M)[0]
+        want = np.array([[_fl(x) for x in row] for row in case["expect"]])
+        np.testing.assert_array_equal(got, want, err_msg=case["name"])
+
+
+def test_block_importance_is_reshape_mean_when_blocks_divide():
+    L, Hkv, M, Nb = 4, 3, 8, 5
+    N = M * Nb
+    sc = _rand((L, Hkv, N), 11)
+    got = oracle.block_importance(sc, [0, N], M)[0]
+    want = sc.astype(np.float64).reshape(L, Hkv, M, Nb).mean(axis=(1, 3))
+    assert np.isinf(got[:2]).all() and (got[:2] > 0).all()
+    np.testing.assert_allclose(got[2:], want[2:], rtol=1e-12)
+
+
+def test_block_importance_size_weighted_sum_is_total_varlen():
+    L, Hkv, M = 3, 2, 7
+    lens = [23, 5, 7]                                  # blocks of 4, 1 and 1 tokens; 23 leaves a short last block
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    sc = _rand((L, Hkv, int(cu[-1])), 12)
+    imp = oracle.block_importance(sc, cu, M)
+    for b, N in enumerate(lens):
+        Nb = -(-N // M)
+        sizes = np.array([max(0, min(N, (m + 1) * Nb) - m * Nb) for m in range(M)])
+        for l in range(2, L):
+            tot = sc[l, :, cu[b]:cu[b + 1]].astype(np.float64).sum()
+            finite = sizes > 0
+            assert (imp[b, l, ~finite] == -np.inf).all()
+            np.testing.assert_allclose((imp[b, l, finite] * sizes[finite] * Hkv).sum(), tot, rtol=1e-9, atol=1e-9)
+
+
+def test_block_budget_worked_and_first_form_of_eq2():
+    for case in _golden("block_worked.json")["budget"]:
+        assert oracle.block_budget(case["M"], case["L"], case["Tp"], case["Tt"]) == case["expect"], case
+    # eq. 2 written as L*M*((L-1)/L * Tp/Tt) gives the same count before the clip
+    for M, L, r in [(1024, 32, 0.154), (512, 80, 0.07), (1024, 40, 0.9)]:
+        first = L * M * ((L - 1) / L * r)
+        k = oracle.block_budget(M, L, r, 1.0)
+        assert k == min(L * M, max(2 * M, math.floor(first + 1e-9))) or k == min(L * M, max(2 * M, math.floor(first)))
+
+
+def test_block_selection_keeps_first_two_layers_and_ranks_the_rest():
+    L, Hkv, M, N = 6, 2, 16, 100
+    sc = _rand((L, Hkv, N), 13) ** 2
+    imp = oracle.block_importance(sc, [0, N], M)            # [1][L][M]
+    Kr = oracle.block_budget(M, L, 0.3, 1.0)                 # floor(16 * 5 * 0.3) = 24 -> clipped to 32
+    assert Kr == 2 * M
+    row = imp.reshape(1, 1, L * M).astype(np.float32)
+    for kr in (Kr, 2 * M + 5, L * M - 3):
+        sel = oracle.topk(row, [0, L * M], [0, kr])[0, 0]
+        assert set(range(2 * M)) <= set(sel.tolist())      # layers 0 and 1 always go
+        rest = np.array(sorted(range(2 * M, L * M), key=lambda c: (-row[0, 0, c], c)))
+        np.testing.assert_array_equal(np.sort(sel), np.sort(np.concatenate([np.arange(2 * M), rest[:kr - 2 * M]])))
+
+
+def test_pack_blocks_worked_example():
+    c = _golden("block_worked.json")["pack"]
+    k = np.array(c["k"], dtype=np.float32)
+    v = np.array(c["v"], dtype=np.float32)
+    buf = oracle.pack_blocks(k, v, c["ids"], 0, c["N"], c["M"])
+    S = len(c["expect_k"])
+    d = c["d"]
+    kr = buf[:S * d * 4].view(np.float32).reshape(S, d)
+    vr = buf[S * d * 4:2 * S * d * 4].view(np.float32).reshape(S, d)
+    ids = buf[2 * S * d * 4:].view(np.int32)
+    np.testing.assert_array_equal(kr, np.array(c["expect_k"], dtype=np.float32))
+    np.testing.assert_array_equal(vr, np.array(c["expect_v"], dtype=np.float32))
+    np.testing.assert_array_equal(ids, c["ids"])
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.uint16])
+def test_pack_blocks_slots_are_source_rows(dtype):
+    L, Hkv, d, M = 3, 2, 8, 5
+    lens = [13, 9]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    g = np.random.default_rng(14)
+    k = g.integers(0, 60000, (L, Hkv, T, d)).astype(dtype)
+    v = g.integers(0, 60000, (L, Hkv, T, d)).astype(dtype)
+    b, N = 0, lens[0]
+    Nb = -(-N // M)
+    ids = np.array([1, 7, 14, 3], dtype=np.int32)
+    buf = oracle.pack_blocks(k, v, ids, cu[b], N, M)
+    S = len(ids) * Hkv * Nb
+    es = np.dtype(dtype).itemsize
+    kr = buf[:S * d * es].view(dtype).reshape(len(ids), Hkv, Nb, d)
+    vr = buf[S * d * es:2 * S * d * es].view(dtype).reshape(len(ids), Hkv, Nb, d)
+    for s, c in enumerate(ids):
+        l, m = divmod(int(c), M)
+        for h in range(Hkv):
+            for r in range(Nb):
+                t = m * Nb + r
+                want_k = k[l, h, cu[b] + t] if t < N else np.zeros(d, dtype)
+                want_v = v[l, h, cu[b] + t] if t < N else np.zeros(d, dtype)
+                np.testing.assert_array_equal(kr[s, h, r], want_k)
+                np.testing.assert_array_equal(vr[s, h, r], want_v)
