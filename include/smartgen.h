@@ -14,6 +14,11 @@
  *                   Section 4.4)
  *   sg_decode_attn  decode attention over a partial KV set addressed through a
  *                   page table (Section 2.1; order invariance, Section 4.2)
+ *   sg_block_importance, sg_block_budget, sg_pack_blocks
+ *                   block-granular proactive selection: eq. 1 block
+ *                   importance, eq. 2 block budget, and the push of the chosen
+ *                   KV blocks (Section 4.1); the global top-K_r of the blocks
+ *                   is sg_topk over one row of L * M importances per request
  *
  * Conventions for every call:
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
@@ -106,7 +111,8 @@ int sg_score(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, in
  *
  *   scores  device float [L][Hkv][T].
  *   idx     device int32 [L][Hkv][K_total] (output).
- *   max_seqlen  host bound of every N_b; must be <= 65536.
+ *   max_seqlen  host bound of every N_b; must be <= 81920 (80 layers x 1024
+ *               blocks when the rows are block importances).
  * A request with k_b > N_b or k_b < 0 (device metadata) gets idx = -1 in its
  * segment.
  */
@@ -217,6 +223,46 @@ int sg_decode_attn(void *stream, sg_dtype dt, int B, int Hq, int Hkv, int d, flo
                    const void *q, const void *k_pool, const void *v_pool, int64_t pool_rows,
                    const int32_t *page_table, const int32_t *n_rows, int page_size, int max_pages,
                    float *out, void *ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------- block mode
+ * Block-granular proactive selection (Section 4.1).  Per layer the sequence of
+ * a request (N tokens) is cut into M KV blocks of Nb = ceil(N / M) tokens;
+ * block m holds tokens [m*Nb, min((m+1)*Nb, N)) in every KV head.
+ *
+ * sg_block_importance: eq. 1 over measured per-entry scores,
+ *   imp[b][l][m] = +inf                                     for l = 0, 1
+ *                = mean over the block's (head, token) entries of
+ *                  scores[l][h][cu_seqlens[b] + t]         for l >= 2,
+ *   and -inf for a block without tokens (trailing blocks when N is not a
+ *   multiple of M).  fp32 sums in a fixed order (heads, then tokens).
+ *     scores  device float [L][Hkv][T]; imp device float [B][L][M] (output).
+ *
+ * sg_block_budget (host only): eq. 2, the number of blocks whose transfer can
+ *   overlap the prefill of all but the first layer,
+ *     K_r = floor(M (L - 1) Tp / Tt), clipped to [2M, L M]
+ *   (Tt = 0 gives L M).  Returns -1 for M < 1, L < 1 or negative times.
+ *   The blocks are then chosen with sg_topk over one row per request:
+ *   L' = Hkv' = 1, cu_seqlens' = (0, L M, 2 L M, ...), cu_k' = offsets of the
+ *   per-request K_r; ids come out ascending as c = l * M + m.
+ *
+ * sg_pack_blocks: the chosen blocks of one request (tokens [s0, s0 + N) of the
+ *   source rows) into one buffer, S = nblk * Hkv * Nb rows per tensor,
+ *     [ K rows: S x d x esize | V rows: S x d x esize | ids: nblk x int32 ]
+ *   Slot row (s * Hkv + h) * Nb + r holds source row
+ *   l * kv_layer_rows + h * T + s0 + m * Nb + r of block ids[s] = l * M + m;
+ *   rows past the prompt end, and every row of an id outside [0, L M), are
+ *   zero.  k, v: device (or pinned host), rows of d elements, at least
+ *   (L - 1) * kv_layer_rows + Hkv * T rows; ids: device int32 [nblk];
+ *   dst: device or host-mapped pinned, >= sg_pack_blocks_bytes(...) bytes.
+ *   Requires s0 + N <= T and N > 0 when nblk > 0.
+ */
+int sg_block_importance(void *stream, int B, int L, int Hkv, const int32_t *cu_seqlens, int64_t T, int M,
+                        const float *scores, float *imp);
+int64_t sg_block_budget(int M, int L, double Tp, double Tt);
+size_t sg_pack_blocks_bytes(sg_dtype dt, int Hkv, int d, int64_t N, int M, int nblk);
+int sg_pack_blocks(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, int64_t s0, int64_t N, int M,
+                   const void *k, const void *v, int64_t kv_layer_rows, int nblk, const int32_t *ids,
+                   void *dst, size_t dst_bytes);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,166 @@
+// Block-granular proactive selection (Section 4.1): block importance (eq. 1),
+// the block budget (eq. 2) and the block pack.  The global top-K_r of the
+// blocks is sg_topk over one row of L * M block importances per request.
+//
+// sg_block_importance: one workgroup per (request, layer).  Thread m sums
+//   its block's scores over the KV heads (outer) and tokens (inner) in fp32
+//   and divides by the entry count; consecutive threads read consecutive
+//   token ranges of a head, so the reads are coalesced.  Layers 0 and 1 get
+//   +inf, empty blocks -inf.
+// sg_pack_blocks: a selected block moves Hkv * Nb contiguous source rows per
+//   tensor; the grid is flat over 16-byte vectors of the output, each thread
+//   issues the loads of all its vectors before any store (non-temporal), so
+//   the copy runs like a plain strided memcpy.
+#include <math.h>
+
+#include "sg_internal.h"
+
+namespace sg {
+
+constexpr int BLK_THREADS = 256;
+
+__global__ __launch_bounds__(BLK_THREADS) void block_importance_kernel(int B, int L, int Hkv,
+                                                                         const int32_t *__restrict__ cu_seqlens,
+                                                                         int64_t T, int M,
+                                                                         const float *__restrict__ scores,
+                                                                         float *__restrict__ imp) {
+    const int b = blockIdx.x % B, l = blockIdx.x / B;
+    const int64_t s0 = cu_seqlens[b], s1 = cu_seqlens[b + 1];
+    // device metadata is clamped to the host-checked sizes
+    const int64_t N = (s0 >= 0 && s1 >= s0 && s1 <= T) ? s1 - s0 : 0;
+    const int64_t Nb = (N + M - 1) / M;
+    float *out = imp + ((int64_t)b * L + l) * M;
+    for (int m = threadIdx.x; m < M; m += BLK_THREADS) {
+        if (l < 2) {
+            out[m] = INFINITY;
+            continue;
+        }
+        const int64_t t0 = (int64_t)m * Nb, t1 = min(t0 + Nb, N);
+        if (t1 <= t0) {
+            out[m] = -INFINITY;
+            continue;
+        }
+        float sum = 0.f;
+        for (int h = 0; h < Hkv; ++h) {
+            const float *row = scores + ((int64_t)l * Hkv + h) * T + s0;
+            for (int64_t t = t0; t < t1; ++t) sum += row[t];
+        }
+        out[m] = sum / (float)((t1 - t0) * Hkv);
+    }
+}
+
+constexpr int PB_UNROLL = 4;
+
+// Output vector i of the K (or V) region: slot row r_all = i / CPR, vector
+// c = i % CPR; slot row r_all = (s * Hkv + h) * Nb + r.
+template <int CPR>
+__global__ __launch_bounds__(BLK_THREADS) void pack_blocks_kernel(int L, int Hkv, int64_t T, int64_t s0, int64_t N,
+                                                                    int M, int64_t Nb, const v4u *__restrict__ k,
+                                                                    const v4u *__restrict__ v, int64_t kv_layer_rows,
+                                                                    int nblk, const int32_t *__restrict__ ids,
+                                                                    v4u *__restrict__ dk, v4u *__restrict__ dv,
+                                                                    int32_t *__restrict__ did) {
+    const int64_t total = (int64_t)nblk * Hkv * Nb * CPR;
+    const int64_t stride = (int64_t)gridDim.x * BLK_THREADS * PB_UNROLL;
+    for (int64_t base = (int64_t)blockIdx.x * BLK_THREADS * PB_UNROLL + threadIdx.x; base < total; base += stride) {
+        v4u kr[PB_UNROLL], vr[PB_UNROLL];
+        bool ok[PB_UNROLL];
+        // every load of the pass first (a row past the prompt or of an invalid
+        // id reads the request's first row and is zeroed)
+#pragma unroll
+        for (int u = 0; u < PB_UNROLL; ++u) {
+            const int64_t i = min(base + (int64_t)u * BLK_THREADS, total - 1);
+            const int64_t row = i / CPR, c = i % CPR;
+            const int64_t r = row % Nb, sh = row / Nb;
+            const int h = (int)(sh % Hkv), s = (int)(sh / Hkv);
+            const int32_t id = ids[s];
+            const bool valid = id >= 0 && (int64_t)id < (int64_t)L * M;
+            const int l = valid ? id / M : 0, m = valid ? id % M : 0;
+            const int64_t t = (int64_t)m * Nb + r;
+            ok[u] = valid && t < N;
+            const int64_t src = ((int64_t)l * kv_layer_rows + (int64_t)h * T + s0 + (ok[u] ? t : 0)) * CPR + c;
+            kr[u] = __builtin_nontemporal_load(k + src);
+            vr[u] = __builtin_nontemporal_load(v + src);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < PB_UNROLL; ++u) {
+            const int64_t i = base + (int64_t)u * BLK_THREADS;
+            if (i < total) {
+                __builtin_nontemporal_store(ok[u] ? kr[u] : v4u{0u, 0u, 0u, 0u}, dk + i);
+                __builtin_nontemporal_store(ok[u] ? vr[u] : v4u{0u, 0u, 0u, 0u}, dv + i);
+            }
+        }
+    }
+    for (int64_t s = (int64_t)blockIdx.x * BLK_THREADS + threadIdx.x; s < nblk; s += (int64_t)gridDim.x * BLK_THREADS)
+        did[s] = ids[s];
+}
+
+}  // namespace sg
+
+using namespace sg;
+
+extern "C" int sg_block_importance(void *stream, int B, int L, int Hkv, const int32_t *cu_seqlens, int64_t T,
+                                   int M, const float *scores, float *imp) {
+    SG_REQUIRE(B >= 1 && L >= 1 && Hkv >= 1, SG_EINVAL, "sg_block_importance: B, L, Hkv must be >= 1");
+    SG_REQUIRE(M >= 1 && T >= 0, SG_EINVAL, "sg_block_importance: need M >= 1 and T >= 0");
+    SG_REQUIRE((int64_t)B * L <= 0x7fffffff, SG_EINVAL, "sg_block_importance: too many rows");
+    SG_REQUIRE(cu_seqlens && scores && imp, SG_EINVAL, "sg_block_importance: null pointer");
+    block_importance_kernel<<<(unsigned)(B * L), BLK_THREADS, 0, as_stream(stream)>>>(B, L, Hkv, cu_seqlens, T, M,
+                                                                                       scores, imp);
+    return launch_status("sg_block_importance");
+}
+
+extern "C" int64_t sg_block_budget(int M, int L, double Tp, double Tt) {
+    if (M < 1 || L < 1 || !(Tp >= 0.0) || !(Tt >= 0.0)) return -1;
+    const int64_t lm = (int64_t)L * M;
+    int64_t k = lm;
+    if (Tt > 0.0) {
+        const double x = floor((double)M * (double)(L - 1) * (Tp / Tt));
+        k = x >= (double)lm ? lm : (int64_t)x;
+    }
+    return std::min<int64_t>(lm, std::max<int64_t>(2 * (int64_t)M, k));
+}
+
+extern "C" size_t sg_pack_blocks_bytes(sg_dtype dt, int Hkv, int d, int64_t N, int M, int nblk) {
+    if (Hkv <= 0 || d <= 0 || N < 0 || M <= 0 || nblk < 0) return 0;
+    const size_t Nb = (size_t)((N + M - 1) / M);
+    const size_t S = (size_t)nblk * Hkv * Nb;
+    return 2 * S * (size_t)d * esize_of(dt) + 4 * (size_t)nblk;
+}
+
+extern "C" int sg_pack_blocks(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, int64_t s0, int64_t N,
+                              int M, const void *k, const void *v, int64_t kv_layer_rows, int nblk,
+                              const int32_t *ids, void *dst, size_t dst_bytes) {
+    SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "sg_pack_blocks: unknown dtype %d", (int)dt);
+    SG_REQUIRE(L >= 1 && Hkv >= 1 && M >= 1, SG_EINVAL, "sg_pack_blocks: L, Hkv, M must be >= 1");
+    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "sg_pack_blocks: head dimension %d not supported", d);
+    SG_REQUIRE(T >= 0 && s0 >= 0 && N >= 0 && s0 + N <= T && kv_layer_rows >= 0 && nblk >= 0, SG_EINVAL,
+               "sg_pack_blocks: the request's tokens [s0, s0 + N) must lie in [0, T)");
+    const size_t need = sg_pack_blocks_bytes(dt, Hkv, d, N, M, nblk);
+    SG_REQUIRE(dst_bytes >= need, SG_EWORKSPACE, "sg_pack_blocks: destination holds %zu bytes, needs %zu",
+               dst_bytes, need);
+    if (nblk == 0) return SG_OK;
+    SG_REQUIRE(k && v && ids && dst, SG_EINVAL, "sg_pack_blocks: null pointer");
+    SG_REQUIRE(aligned16(k) && aligned16(v) && aligned16(dst), SG_EINVAL,
+               "sg_pack_blocks: k, v and dst must be 16-byte aligned");
+    SG_REQUIRE(N > 0, SG_EINVAL, "sg_pack_blocks: blocks of an empty request");
+    const int cpr = d * esize_of(dt) / 16;
+    const int64_t Nb = (N + M - 1) / M;
+    const int64_t S = (int64_t)nblk * Hkv * Nb;
+    v4u *dk = reinterpret_cast<v4u *>(dst);
+    v4u *dv = dk + S * cpr;
+    int32_t *di = reinterpret_cast<int32_t *>(dv + S * cpr);
+    const int64_t total = S * cpr;
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, BLK_THREADS * PB_UNROLL), 65536));
+    hipStream_t s = as_stream(stream);
+    const v4u *kk = reinterpret_cast<const v4u *>(k);
+    const v4u *vv = reinterpret_cast<const v4u *>(v);
+    switch (cpr) {
+        case 8: pack_blocks_kernel<8><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, kk, vv, kv_layer_rows, nblk, ids, dk, dv, di); break;
+        case 16: pack_blocks_kernel<16><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, kk, vv, kv_layer_rows, nblk, ids, dk, dv, di); break;
+        case 32: pack_blocks_kernel<32><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, kk, vv, kv_layer_rows, nblk, ids, dk, dv, di); break;
+        default: set_error("sg_pack_blocks: internal row size"); return SG_EINTERNAL;
+    }
+    return launch_status("sg_pack_blocks");
+}

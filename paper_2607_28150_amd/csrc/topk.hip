@@ -1,9 +1,10 @@
 // sg_topk: exact budgeted top-k per unit row by wavefront-level radix select.
 //
-// One 1024-thread workgroup owns one (request, layer, KV head) row.  The row is
-// held in registers, ITEMS consecutive keys per thread.  Scores are mapped to
-// order-preserving 32-bit keys (NaN -> 0, the lowest key; -0 -> +0).  Four
-// 8-bit digit passes, most significant first, narrow down the exact k-th
+// One 1024-thread workgroup owns one (request, layer, KV head) row (or, for
+// block selection, one request's row of L * M block importances).  The row is
+// held in registers, ITEMS consecutive keys per thread (up to 80).  Scores
+// are mapped to order-preserving 32-bit keys (NaN -> 0, the lowest key;
+// -0 -> +0).  Four 8-bit digit passes, most significant first, narrow down the exact k-th
 // largest key T and how many entries equal to T must be taken ("need").
 // Histograms are built per wavefront: the lanes holding the same digit are
 // found with eight ballots (one per digit bit), and one lane per distinct
@@ -161,8 +162,8 @@ extern "C" int sg_topk(void *stream, int B, int L, int Hkv, const int32_t *cu_se
                        const int32_t *cu_k, int64_t K_total, const float *scores, int32_t *idx) {
     SG_REQUIRE(B >= 1 && L >= 1 && Hkv >= 1, SG_EINVAL, "sg_topk: B, L, Hkv must be >= 1");
     SG_REQUIRE(T >= 0 && K_total >= 0 && max_seqlen >= 0, SG_EINVAL, "sg_topk: negative size");
-    SG_REQUIRE(max_seqlen <= 64 * TOPK_THREADS, SG_EUNSUPPORTED, "sg_topk: max_seqlen %d above %d", max_seqlen,
-               64 * TOPK_THREADS);
+    SG_REQUIRE(max_seqlen <= 80 * TOPK_THREADS, SG_EUNSUPPORTED, "sg_topk: max_seqlen %d above %d", max_seqlen,
+               80 * TOPK_THREADS);
     if (K_total == 0) return SG_OK;
     SG_REQUIRE(cu_seqlens && cu_k && scores && idx, SG_EINVAL, "sg_topk: null pointer");
     const int64_t blocks = (int64_t)B * L * Hkv;
@@ -174,7 +175,9 @@ extern "C" int sg_topk(void *stream, int B, int L, int Hkv, const int32_t *cu_se
         topk_kernel<8><<<(unsigned)blocks, TOPK_THREADS, 0, s>>>(B, cu_seqlens, T, cu_k, K_total, scores, idx);
     else if (max_seqlen <= 32 * TOPK_THREADS)
         topk_kernel<32><<<(unsigned)blocks, TOPK_THREADS, 0, s>>>(B, cu_seqlens, T, cu_k, K_total, scores, idx);
-    else
+    else if (max_seqlen <= 64 * TOPK_THREADS)
         topk_kernel<64><<<(unsigned)blocks, TOPK_THREADS, 0, s>>>(B, cu_seqlens, T, cu_k, K_total, scores, idx);
+    else    // block rows of up to 80 layers x 1024 blocks
+        topk_kernel<80><<<(unsigned)blocks, TOPK_THREADS, 0, s>>>(B, cu_seqlens, T, cu_k, K_total, scores, idx);
     return launch_status("sg_topk");
 }

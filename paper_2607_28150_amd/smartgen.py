@@ -27,6 +27,7 @@ EXPORTS = [
     "sg_split",
     "sg_fetch",
     "sg_decode_attn_workspace_size", "sg_decode_attn",
+    "sg_block_importance", "sg_block_budget", "sg_pack_blocks_bytes", "sg_pack_blocks",
 ]
 
 
@@ -64,7 +65,14 @@ def load() -> ctypes.CDLL:
     lib.sg_decode_attn_workspace_size.argtypes = [_i] * 6
     lib.sg_decode_attn_workspace_size.restype = _sz
     lib.sg_decode_attn.argtypes = [_vp, _i, _i, _i, _i, _i, _f, _vp, _vp, _vp, _l, _vp, _vp, _i, _i, _vp, _vp, _sz]
-    for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn"):
+    lib.sg_block_importance.argtypes = [_vp, _i, _i, _i, _vp, _l, _i, _vp, _vp]
+    lib.sg_block_budget.argtypes = [_i, _i, ctypes.c_double, ctypes.c_double]
+    lib.sg_block_budget.restype = _l
+    lib.sg_pack_blocks_bytes.argtypes = [_i, _i, _i, _l, _i, _i]
+    lib.sg_pack_blocks_bytes.restype = _sz
+    lib.sg_pack_blocks.argtypes = [_vp, _i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _i, _vp, _vp, _sz]
+    for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn", "sg_block_importance",
+              "sg_pack_blocks"):
         getattr(lib, f).restype = _i
     _lib = lib
     return lib
@@ -289,3 +297,47 @@ class DecodeCall:
                                       self._geom[0], self._geom[1], out.data_ptr(), self._ws, self._wsb)
         _check("sg_decode_attn", rc)
 
+
+
+# ----------------------------------------------------------------------------- block mode (Section 4.1)
+
+def sg_block_importance(scores, cu_seqlens, T, M, imp, stream=None):
+    """imp[B][L][M] (float32, written): eq. 1 block importance from scores [L][Hkv][T]."""
+    L, Hkv = scores.shape[0], scores.shape[1]
+    B = cu_seqlens.numel() - 1
+    _need(scores.dtype == torch.float32 and scores.numel() >= L * Hkv * T, "scores must be float32 [L][Hkv][T]")
+    _need(imp.dtype == torch.float32 and imp.numel() >= B * L * M, "imp must be float32 [B][L][M]")
+    _need(cu_seqlens.dtype == torch.int32, "cu_seqlens must be int32 [B+1]")
+    rc = load().sg_block_importance(_stream(stream), B, L, Hkv, _ptr(cu_seqlens), int(T), int(M), _ptr(scores),
+                                    _ptr(imp))
+    _check("sg_block_importance", rc)
+    return imp
+
+
+def block_budget(M, L, Tp, Tt) -> int:
+    """Eq. 2 block budget K_r (host only)."""
+    k = load().sg_block_budget(int(M), int(L), float(Tp), float(Tt))
+    if k < 0:
+        raise SmartgenError("sg_block_budget", SG_EINVAL, "need M, L >= 1 and non-negative times")
+    return int(k)
+
+
+def pack_blocks_bytes(dtype, Hkv, d, N, M, nblk) -> int:
+    return int(load().sg_pack_blocks_bytes(SG_BF16 if dtype == torch.bfloat16 else SG_F32, Hkv, d, int(N), int(M),
+                                           int(nblk)))
+
+
+def sg_pack_blocks(k, v, ids, s0, N, M, dst, L=None, kv_layer_rows=None, stream=None):
+    """Block transfer buffer of one request (tokens [s0, s0 + N) of k / v [Lkv][Hkv][T][d])."""
+    _need(k.dtype == v.dtype and k.shape == v.shape, "k and v must match")
+    _need(ids.dtype == torch.int32, "ids must be int32")
+    Lkv, Hkv, T, d = k.shape
+    if L is None:
+        L = Lkv
+    if kv_layer_rows is None:
+        kv_layer_rows = 0 if (Lkv == 1 and L > 1) else Hkv * T
+    rc = load().sg_pack_blocks(_stream(stream), _dtype_code(k), int(L), Hkv, d, int(T), int(s0), int(N), int(M),
+                               _ptr(k), _ptr(v), int(kv_layer_rows), ids.numel(), _ptr(ids), _ptr(dst),
+                               dst.numel() * dst.element_size())
+    _check("sg_pack_blocks", rc)
+    return dst

@@ -78,7 +78,7 @@ def test_score_rejections(lib):
 
 
 def test_topk_rejections(lib):
-    rc = lib.sg_topk(None, 1, 1, 1, P, 100000, 70000, P, 100, P, P)
+    rc = lib.sg_topk(None, 1, 1, 1, P, 100000, 90000, P, 100, P, P)      # rows above 80 x 1024
     assert rc == smartgen.SG_EUNSUPPORTED
     rc = lib.sg_topk(None, 0, 1, 1, P, 100, 100, P, 10, P, P)
     assert rc == smartgen.SG_EINVAL
@@ -106,3 +106,24 @@ def test_split_fetch_decode_rejections(lib):
     assert rc == smartgen.SG_EWORKSPACE
     rc = lib.sg_decode_attn(None, 1, 1, 24, 8, 128, 0.1, P, P, P, 10, P, P, 16, 4, P, None, 0)
     assert rc == smartgen.SG_EUNSUPPORTED       # group size 3
+
+
+def test_block_mode_host_checks(lib):
+    # eq. 2 on the host: the worked values of the paper's setting and the clip
+    assert smartgen.block_budget(1024, 32, 1.0, 6.5) == 4883
+    assert smartgen.block_budget(1024, 32, 1.0, 100.0) == 2048
+    assert smartgen.block_budget(1024, 32, 1.0, 0.5) == 32768
+    assert smartgen.block_budget(1024, 32, 1.0, 0.0) == 32768
+    assert lib.sg_block_budget(0, 32, 1.0, 1.0) == -1
+    assert lib.sg_block_budget(1024, 32, -1.0, 1.0) == -1
+    # [K | V | ids] of 5 blocks of ceil(8192 / 1024) = 8 tokens in 8 heads, bf16 d = 128
+    assert smartgen.pack_blocks_bytes(__import__("torch").bfloat16, 8, 128, 8192, 1024, 5) == 2 * 5 * 8 * 8 * 256 + 20
+    assert lib.sg_block_importance(None, 0, 1, 1, P, 10, 4, P, P) == smartgen.SG_EINVAL
+    assert lib.sg_block_importance(None, 1, 1, 1, P, 10, 0, P, P) == smartgen.SG_EINVAL
+    rc = lib.sg_pack_blocks(None, 1, 2, 8, 128, 100, 90, 20, 4, P, P, 800, 3, P, P, 1 << 20)   # s0 + N > T
+    assert rc == smartgen.SG_EINVAL
+    rc = lib.sg_pack_blocks(None, 1, 2, 8, 128, 100, 0, 20, 4, P, P, 800, 3, P, P, 16)          # too small
+    assert rc == smartgen.SG_EWORKSPACE
+    rc = lib.sg_pack_blocks(None, 1, 2, 8, 80, 100, 0, 20, 4, P, P, 800, 3, P, P, 1 << 20)      # d = 80
+    assert rc == smartgen.SG_EUNSUPPORTED
+    assert lib.sg_pack_blocks(None, 1, 2, 8, 128, 100, 0, 20, 4, P, P, 800, 0, P, P, 0) == smartgen.SG_OK
