@@ -198,6 +198,10 @@ def main():
     torch.cuda.synchronize()
     t_score_lse = ev_l[0].elapsed_time(ev_l[1]) / nrep
 
+    # block-granular proactive selection (eq. 1, eq. 2; M = 1024 blocks per
+    # layer, transfer time 6.5x the prefill time), timed on its own
+    blk = block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize)
+
     # ------------------------------------------------------------- per-op times (HIP events on the launch stream)
     def ms(a, b):
         return a.elapsed_time(b)
@@ -226,6 +230,7 @@ def main():
                          "tflops": round(score_flops / (t_score_lse * 1e-3) / 1e12, 2),
                          "frac_mfma_peak": round(score_flops / (t_score_lse * 1e-3) / 1e12 / peak_mfma, 4),
                          "note": "one pass: row normalisers supplied by the prefill attention"},
+        "block_mode": blk,
         "topk": {"ms": round(t_topk, 4),
                  "gbs": round((scores.numel() * 4 + idx.numel() * 4) / (t_topk * 1e-3) / 1e9, 1)},
         "pack": {"ms": round(t_pack, 4), "gbs": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9, 1),
@@ -268,6 +273,51 @@ def main():
         if line["cpu_baseline"].get("value"):
             line["gpu_over_cpu"] = round(value / line["cpu_baseline"]["value"], 1)
     print(json.dumps(line), flush=True)
+
+
+def block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize, M=1024, ratio=1 / 6.5, nrep=10):
+    """Times eq. 1 (block importance), the top-K_r over the L * M blocks and the
+    push of the chosen blocks (device destination, two alternating buffers)."""
+    import torch
+    dev = scores.device
+    Kr = sg.block_budget(M, L, ratio, 1.0)
+    imp = torch.empty((1, L, M), device=dev)
+    ids = torch.empty((1, 1, Kr), dtype=torch.int32, device=dev)
+    cu_row, cu_kr = (torch.tensor([0, L * M], dtype=torch.int32, device=dev),
+                     torch.tensor([0, Kr], dtype=torch.int32, device=dev))
+    nbytes = sg.pack_blocks_bytes(pre["k"].dtype, Hkv, d, N, M, Kr)
+    dsts = [torch.empty(nbytes, dtype=torch.uint8, device=dev) for _ in range(2)]
+
+    def run(i, ev=None):
+        if ev:
+            ev[0].record()
+        sg.sg_block_importance(scores, cus, T, M, imp)
+        if ev:
+            ev[1].record()
+        sg.sg_topk(imp.view(1, 1, L * M), cu_row, L * M, L * M, cu_kr, Kr, ids)
+        if ev:
+            ev[2].record()
+        sg.sg_pack_blocks(pre["k"], pre["v"], ids.view(-1), 0, N, M, dsts[i % 2])
+        if ev:
+            ev[3].record()
+    run(0)
+    run(1)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(nrep)]
+    for i in range(nrep):
+        run(i, evs[i])
+    torch.cuda.synchronize()
+    t = [sum(e[j].elapsed_time(e[j + 1]) for e in evs) / nrep for j in range(3)]
+    Nb = -(-N // M)
+    rows = Kr * Hkv * Nb
+    pack_bytes = 2 * 2 * rows * d * esize + 2 * Kr * 4                # rows read + written, ids read + written
+    imp_bytes = L * Hkv * N * 4 + L * M * 4
+    return {"M": M, "transfer_over_prefill": round(1 / ratio, 2), "K_r": Kr, "blocks": L * M,
+            "importance_ms": round(t[0], 4), "importance_gbs": round(imp_bytes / (t[0] * 1e-3) / 1e9, 1),
+            "topk_ms": round(t[1], 4),
+            "pack_ms": round(t[2], 4), "pack_gbs": round(pack_bytes / (t[2] * 1e-3) / 1e9, 1),
+            "pack_frac_hbm_peak": round(pack_bytes / (t[2] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "pack_mb_algorithmic": round(pack_bytes / 1e6, 2)}
 
 
 def window_lse(q_win, k, N, Hkv, W, d):

@@ -234,7 +234,7 @@ int sg_decode_attn(void *stream, sg_dtype dt, int B, int Hq, int Hkv, int d, flo
  *                = mean over the block's (head, token) entries of
  *                  scores[l][h][cu_seqlens[b] + t]         for l >= 2,
  *   and -inf for a block without tokens (trailing blocks when N is not a
- *   multiple of M).  fp32 sums in a fixed order (heads, then tokens).
+ *   multiple of M).  fp32 sums in a fixed order, so results repeat exactly.
  *     scores  device float [L][Hkv][T]; imp device float [B][L][M] (output).
  *
  * sg_block_budget (host only): eq. 2, the number of blocks whose transfer can

@@ -2,10 +2,9 @@
 // the block budget (eq. 2) and the block pack.  The global top-K_r of the
 // blocks is sg_topk over one row of L * M block importances per request.
 //
-// sg_block_importance: one workgroup per (request, layer).  Thread m sums
-//   its block's scores over the KV heads (outer) and tokens (inner) in fp32
-//   and divides by the entry count; consecutive threads read consecutive
-//   token ranges of a head, so the reads are coalesced.  Layers 0 and 1 get
+// sg_block_importance: 8 lanes per block, one KV head each (more heads
+//   loop), 32 blocks per workgroup; fp32 sums in a fixed order (eight token
+//   partials per head, then the lanes by xor shuffles).  Layers 0 and 1 get
 //   +inf, empty blocks -inf.
 // sg_pack_blocks: a selected block moves Hkv * Nb contiguous source rows per
 //   tensor; the grid is flat over 16-byte vectors of the output, each thread
@@ -19,33 +18,50 @@ namespace sg {
 
 constexpr int BLK_THREADS = 256;
 
+// Importance: a workgroup covers BI_BLOCKS blocks of one (request, layer);
+// the 8 lanes of a block take KV heads j, j + 8, ... and sum their tokens
+// (every load of a head issued before its adds), then add up in a fixed
+// order with xor shuffles.
+constexpr int BI_LANES = 8;
+constexpr int BI_BLOCKS = BLK_THREADS / BI_LANES;
+
 __global__ __launch_bounds__(BLK_THREADS) void block_importance_kernel(int B, int L, int Hkv,
                                                                          const int32_t *__restrict__ cu_seqlens,
-                                                                         int64_t T, int M,
+                                                                         int64_t T, int M, int nchunk,
                                                                          const float *__restrict__ scores,
                                                                          float *__restrict__ imp) {
-    const int b = blockIdx.x % B, l = blockIdx.x / B;
+    const int chunk = blockIdx.x % nchunk;
+    const int bl = blockIdx.x / nchunk;
+    const int b = bl % B, l = bl / B;
     const int64_t s0 = cu_seqlens[b], s1 = cu_seqlens[b + 1];
     // device metadata is clamped to the host-checked sizes
     const int64_t N = (s0 >= 0 && s1 >= s0 && s1 <= T) ? s1 - s0 : 0;
     const int64_t Nb = (N + M - 1) / M;
-    float *out = imp + ((int64_t)b * L + l) * M;
-    for (int m = threadIdx.x; m < M; m += BLK_THREADS) {
-        if (l < 2) {
-            out[m] = INFINITY;
-            continue;
-        }
-        const int64_t t0 = (int64_t)m * Nb, t1 = min(t0 + Nb, N);
-        if (t1 <= t0) {
-            out[m] = -INFINITY;
-            continue;
-        }
-        float sum = 0.f;
-        for (int h = 0; h < Hkv; ++h) {
+    const int j = threadIdx.x % BI_LANES;
+    const int m = chunk * BI_BLOCKS + threadIdx.x / BI_LANES;
+    const int64_t t0 = (int64_t)m * Nb, t1 = min(t0 + Nb, N);
+    float sum = 0.f;
+    if (l >= 2 && m < M) {
+        for (int h = j; h < Hkv; h += BI_LANES) {
             const float *row = scores + ((int64_t)l * Hkv + h) * T + s0;
-            for (int64_t t = t0; t < t1; ++t) sum += row[t];
+            float part[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            int64_t t = t0;
+            for (; t + 8 <= t1; t += 8) {
+                float x[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) x[u] = row[t + u];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) part[u] += x[u];
+            }
+            for (int u = 0; t < t1; ++t, ++u) part[u] += row[t];
+            sum += ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
         }
-        out[m] = sum / (float)((t1 - t0) * Hkv);
+    }
+#pragma unroll
+    for (int off = 1; off < BI_LANES; off <<= 1) sum += __shfl_xor(sum, off, 64);
+    if (j == 0 && m < M) {
+        float *out = imp + ((int64_t)b * L + l) * M;
+        out[m] = l < 2 ? INFINITY : (t1 <= t0 ? -INFINITY : sum / (float)((t1 - t0) * Hkv));
     }
 }
 
@@ -106,8 +122,10 @@ extern "C" int sg_block_importance(void *stream, int B, int L, int Hkv, const in
     SG_REQUIRE(M >= 1 && T >= 0, SG_EINVAL, "sg_block_importance: need M >= 1 and T >= 0");
     SG_REQUIRE((int64_t)B * L <= 0x7fffffff, SG_EINVAL, "sg_block_importance: too many rows");
     SG_REQUIRE(cu_seqlens && scores && imp, SG_EINVAL, "sg_block_importance: null pointer");
-    block_importance_kernel<<<(unsigned)(B * L), BLK_THREADS, 0, as_stream(stream)>>>(B, L, Hkv, cu_seqlens, T, M,
-                                                                                       scores, imp);
+    const int64_t nchunk = ceil_div(M, BI_BLOCKS);
+    SG_REQUIRE((int64_t)B * L * nchunk <= 0x7fffffff, SG_EINVAL, "sg_block_importance: too many blocks");
+    block_importance_kernel<<<(unsigned)(B * L * nchunk), BLK_THREADS, 0, as_stream(stream)>>>(
+        B, L, Hkv, cu_seqlens, T, M, (int)nchunk, scores, imp);
     return launch_status("sg_block_importance");
 }
 
