@@ -277,7 +277,9 @@ def main():
 
 def block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize, M=1024, ratio=1 / 6.5, nrep=10):
     """Times eq. 1 (block importance), the top-K_r over the L * M blocks and the
-    push of the chosen blocks (device destination, two alternating buffers)."""
+    push of the chosen blocks (device destination, two alternating buffers).
+    The default T_p / T_t of 1 / 6.5 is the transfer-to-prefill time ratio
+    that Section 1 reports for a 48K-token prompt."""
     import torch
     dev = scores.device
     Kr = sg.block_budget(M, L, ratio, 1.0)
