@@ -45,8 +45,12 @@ def _load():
                                     _i, _i, _f64p]
     lib.sgo_block_importance.argtypes = [_i, _i, _i, _i32p, _l, _i, _f32p, _f64p]
     lib.sgo_pack_blocks.argtypes = [_i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _i, _i32p, _vp]
+    lib.sgo_spec_push.argtypes = [_i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _vp, _vp, _l, _i, _i32p, _i8p,
+                                  _f32p]
+    lib.sgo_fetch_keep.argtypes = [_i, _i, _i, _i32p, _i32p, _i32p, _i64p, _l, _vp, _vp, _i32p, _i, _i, _i32p,
+                                   _vp, _vp, _l, _i64p, _vp, _vp, _l, _i8p, _l, _i64p, _i32p]
     for f in ("sgo_score", "sgo_topk", "sgo_pack", "sgo_split", "sgo_fetch", "sgo_decode_attn", "sgo_threads",
-              "sgo_block_importance", "sgo_pack_blocks"):
+              "sgo_block_importance", "sgo_pack_blocks", "sgo_spec_push", "sgo_fetch_keep"):
         getattr(lib, f).restype = ctypes.c_int
     lib.sgo_set_threads.argtypes = [_i]
     lib.sgo_set_threads.restype = None
@@ -238,3 +242,70 @@ def _pack_blocks(kk, vv, ix, s0, N, M, kv_layer_rows, Hkv, T, d, L=None):
                                  int(kv_layer_rows), len(ix), _p(ix, _i32p), out.ctypes.data)
     _check(rc, "pack_blocks")
     return out
+
+
+def spec_quota(blocks, ratio_bp):
+    """Section 4.3: a speculative transfer sends a fixed fraction (the
+    speculative ratio, in basis points) of all KV blocks, rounded up so that
+    1 / ratio transfers deliver everything; at least one block."""
+    if blocks < 0 or ratio_bp < 1:
+        raise ValueError("spec_quota needs blocks >= 0 and a positive ratio")
+    return min(blocks, max(1, -(-blocks * ratio_bp // 10000)))
+
+
+def spec_push(k_src, v_src, ids, s0, N, M, k_dst, v_dst, mask, rem=None, L=None, src_layer_rows=None,
+              dst_layer_rows=None):
+    """Section 4.3: copies the blocks `ids` of one request from the prefill
+    side's K/V [Lkv][Hkv][T][d] into the decode side's store [Ld][Hkv][T][d] at
+    the same rows, sets their mask [L][Hkv][T] (int8) entries to 1 and their
+    entries of rem [L*M] (float32) to NaN.  k_dst, v_dst, mask, rem change in place."""
+    assert k_src.dtype == v_src.dtype == k_dst.dtype == v_dst.dtype
+    for a in (k_src, v_src, k_dst, v_dst, mask):
+        assert a.flags.c_contiguous
+    assert mask.dtype == np.int8 and (rem is None or (rem.dtype == np.float32 and rem.flags.c_contiguous))
+    _, Hkv, T, d = k_src.shape
+    if L is None:
+        L = k_src.shape[0]
+    ix = _c(ids, np.int32)
+    rc = _load().sgo_spec_push(int(L), Hkv, d, k_src.dtype.itemsize, T, int(s0), int(N), int(M),
+                               k_src.ctypes.data, v_src.ctypes.data,
+                               Hkv * T if src_layer_rows is None else int(src_layer_rows),
+                               k_dst.ctypes.data, v_dst.ctypes.data,
+                               Hkv * T if dst_layer_rows is None else int(dst_layer_rows),
+                               len(ix), _p(ix, _i32p), _p(mask, _i8p), None if rem is None else _p(rem, _f32p))
+    _check(rc, "spec_push")
+
+
+def fetch_keep(row_off, index, n_valid, src_row_base, k_src, v_src, page_table, page_size, dst_start,
+               k_pool, v_pool, keep_row_base, k_keep, v_keep, mask, mask_off, mask_len):
+    """The fetch of `fetch` (pool written when page_table is not None) that also
+    keeps every copied row at keep row keep_row_base[r] + index and turns its
+    mask entry to 1.  Pools, keep arrays (2-D [rows][d]) and mask change in place."""
+    ro = _c(row_off, np.int32)
+    rows = len(ro) - 1
+    ix = _c(index, np.int32)
+    nv = None if n_valid is None else _c(n_valid, np.int32)
+    sb = _c(src_row_base, np.int64)
+    kb = _c(keep_row_base, np.int64)
+    ks = np.ascontiguousarray(k_src)
+    vs = np.ascontiguousarray(v_src)
+    d = ks.shape[-1]
+    for a in (k_keep, v_keep) + ((k_pool, v_pool) if page_table is not None else ()):
+        assert a.flags.c_contiguous and a.dtype == ks.dtype
+    pt = None if page_table is None else _c(page_table, np.int32)
+    ds = _c(dst_start, np.int32)
+    max_pages = 1 if pt is None else pt.shape[-1]
+    mo = None if mask is None else _c(mask_off, np.int64)
+    ml = None if mask is None else _c(mask_len, np.int32)
+    if mask is not None:
+        assert mask.dtype == np.int8 and mask.flags.c_contiguous
+    rc = _load().sgo_fetch_keep(rows, ks.dtype.itemsize, d, _p(ro, _i32p), _p(ix, _i32p),
+                                None if nv is None else _p(nv, _i32p), _p(sb, _i64p), ks.size // d,
+                                ks.ctypes.data, vs.ctypes.data, None if pt is None else _p(pt, _i32p),
+                                int(page_size), int(max_pages), _p(ds, _i32p),
+                                None if pt is None else k_pool.ctypes.data, None if pt is None else v_pool.ctypes.data,
+                                0 if pt is None else k_pool.size // d,
+                                _p(kb, _i64p), k_keep.ctypes.data, v_keep.ctypes.data, k_keep.size // d,
+                                None if mask is None else _p(mask, _i8p), 0 if mask is None else mask.size,
+                                None if mask is None else _p(mo, _i64p), None if mask is None else _p(ml, _i32p))
+    _check(rc, "fetch_keep")

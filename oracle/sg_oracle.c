@@ -433,3 +433,101 @@ int sgo_pack_blocks(int L, int Hkv, int d, int esize, int64_t T, int64_t s0, int
     }
     return SGO_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Speculative transfer (Section 4.3).  The prefill side pushes KV blocks that
+ * the proactive transfer left behind into the decode side's KV store, in
+ * importance order (eq. 1), and turns their KV mask entries local (Section
+ * 4.2: mask 1 = local, 2 = remote).
+ *
+ * One request (tokens [s0, s0 + N) of T), blocks of Nb = ceil(N / M) tokens,
+ * flat id c = l*M + m.  For each id of `ids` with 0 <= c < L*M, in order:
+ *   for every KV head h and block token t = m*Nb + r < N:
+ *     K_dst, V_dst row l*dst_layer_rows + h*T + s0 + t
+ *         = K_src, V_src row l*src_layer_rows + h*T + s0 + t
+ *     mask[(l*Hkv + h)*T + s0 + t] = 1
+ *   rem[c] = NaN when rem is given: the block leaves the row of remaining
+ *   importances, so a later top-k over that row ranks it last.
+ * Other ids are skipped.
+ */
+int sgo_spec_push(int L, int Hkv, int d, int esize, int64_t T, int64_t s0, int64_t N, int M,
+                  const void *k_src, const void *v_src, int64_t src_layer_rows,
+                  void *k_dst, void *v_dst, int64_t dst_layer_rows,
+                  int nblk, const int32_t *ids, int8_t *mask, float *rem)
+{
+    if (esize != 2 && esize != 4) return SGO_EINVAL;
+    if (L < 1 || Hkv < 1 || M < 1 || N < 0 || nblk < 0 || s0 < 0 || s0 + N > T) return SGO_EINVAL;
+    const int64_t Nb = (N + M - 1) / M;
+    const int64_t rowb = (int64_t)d * esize;
+    for (int s = 0; s < nblk; ++s) {
+        const int32_t c = ids[s];
+        if (c < 0 || (int64_t)c >= (int64_t)L * M) continue;
+        const int l = c / M, m = c % M;
+        for (int h = 0; h < Hkv; ++h)
+            for (int64_t r = 0; r < Nb; ++r) {
+                const int64_t t = (int64_t)m * Nb + r;
+                if (t >= N) break;
+                const int64_t src = (int64_t)l * src_layer_rows + (int64_t)h * T + s0 + t;
+                const int64_t dst = (int64_t)l * dst_layer_rows + (int64_t)h * T + s0 + t;
+                memcpy((unsigned char *)k_dst + dst * rowb, (const unsigned char *)k_src + src * rowb, (size_t)rowb);
+                memcpy((unsigned char *)v_dst + dst * rowb, (const unsigned char *)v_src + src * rowb, (size_t)rowb);
+                mask[((int64_t)l * Hkv + h) * T + s0 + t] = 1;
+            }
+        if (rem) rem[c] = NAN;
+    }
+    return SGO_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* On-demand fetch with reuse (Section 4.2; Section 5.3 compares against
+ * reusing fetched entries).  The fetch of sgo_fetch, where each copied entry
+ * is also kept in the decode side's KV store and its mask entry turns local,
+ * so later steps load it on the local lane.
+ *
+ * Row r, entry i < n_r (as in sgo_fetch), t = index[row_off[r] + i]:
+ *   src = src_row_base[r] + t; an entry with src outside [0, src_rows) is
+ *   skipped entirely;
+ *   pool: as sgo_fetch (logical row dst_start[r] + i through the page table),
+ *   when page_table is given;
+ *   keep: row keep_row_base[r] + t of k_keep / v_keep, when inside
+ *   [0, keep_rows); only then, and when mask is given, 0 <= t < mask_len[r]
+ *   and 0 <= mask_off[r] + t < mask_bytes: mask[mask_off[r] + t] = 1.
+ */
+int sgo_fetch_keep(int rows, int esize, int d, const int32_t *row_off, const int32_t *index,
+                   const int32_t *n_valid, const int64_t *src_row_base, int64_t src_rows,
+                   const void *k_src, const void *v_src,
+                   const int32_t *page_table, int page_size, int max_pages, const int32_t *dst_start,
+                   void *k_pool, void *v_pool, int64_t pool_rows,
+                   const int64_t *keep_row_base, void *k_keep, void *v_keep, int64_t keep_rows,
+                   int8_t *mask, int64_t mask_bytes, const int64_t *mask_off, const int32_t *mask_len)
+{
+    if ((esize != 2 && esize != 4) || !index) return SGO_EINVAL;
+    if (page_table && page_size <= 0) return SGO_EINVAL;
+    const int64_t rowb = (int64_t)d * esize;
+    for (int r = 0; r < rows; ++r) {
+        const int64_t seg = row_off[r + 1] - row_off[r];
+        const int64_t n = n_valid ? n_valid[r] : seg;
+        for (int64_t i = 0; i < n && i < seg; ++i) {
+            const int64_t t = index[row_off[r] + i];
+            const int64_t src = src_row_base[r] + t;
+            if (src < 0 || src >= src_rows) continue;
+            const unsigned char *ks = (const unsigned char *)k_src + src * rowb;
+            const unsigned char *vs = (const unsigned char *)v_src + src * rowb;
+            const int64_t lrow = (int64_t)dst_start[r] + i;
+            if (page_table && lrow >= 0 && lrow / page_size < max_pages) {
+                const int64_t dst = (int64_t)page_table[(int64_t)r * max_pages + lrow / page_size] + lrow % page_size;
+                if (dst >= 0 && dst < pool_rows) {
+                    memcpy((unsigned char *)k_pool + dst * rowb, ks, (size_t)rowb);
+                    memcpy((unsigned char *)v_pool + dst * rowb, vs, (size_t)rowb);
+                }
+            }
+            const int64_t kr = keep_row_base[r] + t;
+            if (kr < 0 || kr >= keep_rows) continue;
+            memcpy((unsigned char *)k_keep + kr * rowb, ks, (size_t)rowb);
+            memcpy((unsigned char *)v_keep + kr * rowb, vs, (size_t)rowb);
+            if (mask && t >= 0 && t < mask_len[r] && mask_off[r] + t >= 0 && mask_off[r] + t < mask_bytes)
+                mask[mask_off[r] + t] = 1;
+        }
+    }
+    return SGO_OK;
+}

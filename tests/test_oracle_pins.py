@@ -577,3 +577,158 @@ def test_pack_blocks_slots_are_source_rows(dtype):
                 want_v = v[l, h, cu[b] + t] if t < N else np.zeros(d, dtype)
                 np.testing.assert_array_equal(kr[s, h, r], want_k)
                 np.testing.assert_array_equal(vr[s, h, r], want_v)
+
+
+# ----------------------------------------------------------------------------- speculative transfer, reuse
+
+def test_spec_push_worked_example():
+    c = _golden("spec_keep_worked.json")["spec_push"]
+    k = np.array(c["k_src"], dtype=np.float32)
+    v = -k
+    kd, vd = np.zeros_like(k), np.zeros_like(v)
+    mask = np.array(c["mask_in"], dtype=np.int8)
+    rem = np.array(c["rem_in"], dtype=np.float32)
+    oracle.spec_push(k, v, c["ids"], c["s0"], c["N"], c["M"], kd, vd, mask, rem)
+    np.testing.assert_array_equal(kd, np.array(c["expect_k"], dtype=np.float32))
+    np.testing.assert_array_equal(vd, -np.array(c["expect_k"], dtype=np.float32))
+    np.testing.assert_array_equal(mask, np.array(c["expect_mask"], dtype=np.int8))
+    np.testing.assert_array_equal(rem, np.array([float(x) for x in c["expect_rem"]], dtype=np.float32))
+
+
+@pytest.mark.parametrize("shared", [False, True])
+def test_spec_push_of_every_block_delivers_the_request(shared):
+    L, Hkv, d, M = 3, 2, 4, 5
+    lens = [11, 7]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    g = np.random.default_rng(31)
+    k = g.standard_normal((1 if shared else L, Hkv, T, d)).astype(np.float32)
+    v = g.standard_normal(k.shape).astype(np.float32)
+    kd = np.full((L, Hkv, T, d), 7.0, np.float32)
+    vd = kd.copy()
+    mask = np.full((L, Hkv, T), 2, np.int8)
+    b, s0, N = 1, int(cu[1]), lens[1]
+    oracle.spec_push(k, v, g.permutation(L * M), s0, N, M, kd, vd, mask, L=L, src_layer_rows=0 if shared else None)
+    for l in range(L):
+        src = 0 if shared else l
+        np.testing.assert_array_equal(kd[l, :, s0:s0 + N], k[src, :, s0:s0 + N])
+        np.testing.assert_array_equal(vd[l, :, s0:s0 + N], v[src, :, s0:s0 + N])
+    assert (kd[:, :, :s0] == 7).all() and (mask[:, :, :s0] == 2).all()     # the other request is untouched
+    assert (mask[:, :, s0:s0 + N] == 1).all()
+
+
+def test_spec_quota_matches_the_papers_step_counts():
+    # 10% delivers every block within 10 transfers, 20% within 5, 5% within 20
+    for L in (32, 40, 80):
+        LM = L * 1024
+        for bp, steps in ((1000, 10), (2000, 5), (500, 20)):
+            assert -(-LM // oracle.spec_quota(LM, bp)) == steps
+    for LM in range(1, 3001):
+        for bp, steps in ((1000, 10), (2000, 5), (500, 20)):
+            r = oracle.spec_quota(LM, bp)
+            assert 1 <= r <= LM and -(-LM // r) <= steps
+
+
+def test_spec_steps_follow_the_importance_order():
+    """Proactive top-K_r, then speculative transfers of the quota each: step s
+    delivers exactly the blocks ranked [K_r + (s-1) r, K_r + s r) by (importance
+    descending, id ascending), and the last step completes the request."""
+    L, Hkv, d, M, N = 5, 2, 4, 8, 37                   # Nb = 5; block 7 of each layer holds 2 tokens
+    g = np.random.default_rng(32)
+    sc = (g.standard_normal((L, Hkv, N)) ** 2).astype(np.float32)
+    sc[3, :, 10:15] = sc[4, :, 0:5]                    # equal blocks (ties go to the lower id)
+    imp = oracle.block_importance(sc, [0, N], M)[0].reshape(-1)
+    LM = L * M
+    order = np.array(sorted(range(LM), key=lambda c: (-imp[c], c)))
+    k = g.standard_normal((L, Hkv, N, d)).astype(np.float32)
+    v = g.standard_normal(k.shape).astype(np.float32)
+    kd, vd = np.zeros_like(k), np.zeros_like(v)
+    mask = np.full((L, Hkv, N), 2, np.int8)
+    rem = imp.astype(np.float32)
+    Kr = oracle.block_budget(M, L, 0.3, 1.0)
+    r = oracle.spec_quota(LM, 1000)
+    done, step, quota = 0, 0, Kr
+    while done < LM:
+        q = min(quota, LM - done)
+        sel = oracle.topk(rem.reshape(1, 1, LM), [0, LM], [0, q])[0, 0]
+        np.testing.assert_array_equal(np.sort(sel), np.sort(order[done:done + q]))
+        oracle.spec_push(k, v, sel, 0, N, M, kd, vd, mask, rem)
+        done += q
+        step += 1
+        quota = r
+        pushed = np.zeros(LM, bool)
+        pushed[order[:done]] = True
+        assert np.isnan(rem[pushed]).all() and not np.isnan(rem[~pushed]).any()
+        Nb = -(-N // M)
+        for c in range(LM):
+            l, m = divmod(c, M)
+            toks = slice(m * Nb, min(N, (m + 1) * Nb))
+            assert (mask[l, :, toks] == (1 if pushed[c] else 2)).all()
+    assert step == 1 + -(-(LM - Kr) // r)
+    np.testing.assert_array_equal(kd, k)
+    np.testing.assert_array_equal(vd, v)
+
+
+def test_fetch_keep_worked_example():
+    c = _golden("spec_keep_worked.json")["fetch_keep"]
+    ks = np.array(c["k_src"], dtype=np.float32)
+    vs = -ks
+    kp, vp = np.zeros((c["pool_rows"], 2), np.float32), np.zeros((c["pool_rows"], 2), np.float32)
+    kk, vk = np.zeros((c["keep_rows"], 2), np.float32), np.zeros((c["keep_rows"], 2), np.float32)
+    mask = np.array(c["mask_in"], dtype=np.int8)
+    n = len(c["index"])
+    oracle.fetch_keep([0, n], c["index"], None, [c["src_row_base"]], ks, vs, np.array([c["page_table"]]),
+                      c["page_size"], [c["dst_start"]], kp, vp, [c["keep_row_base"]], kk, vk, mask,
+                      [c["mask_off"]], [c["mask_len"]])
+    np.testing.assert_array_equal(kp, np.array(c["expect_pool_k"], np.float32))
+    np.testing.assert_array_equal(vp, -np.array(c["expect_pool_k"], np.float32))
+    np.testing.assert_array_equal(kk, np.array(c["expect_keep_k"], np.float32))
+    np.testing.assert_array_equal(vk, -np.array(c["expect_keep_k"], np.float32))
+    np.testing.assert_array_equal(mask, np.array(c["expect_mask"], np.int8))
+
+
+def test_fetch_keep_brute_force_and_reuse():
+    """Every fetched entry lands in the pool like a plain fetch and in the store
+    at its own token row, its mask entry turns local; a split of the same
+    index afterwards finds no remote entry (Algorithm 1), so a later step loads
+    them on the local lane."""
+    g = np.random.default_rng(33)
+    rows, N, d, P = 6, 50, 4, 4
+    src = g.standard_normal((rows * N, d)).astype(np.float32)
+    vsrc = g.standard_normal((rows * N, d)).astype(np.float32)
+    mask = np.where(g.random(rows * N) < 0.6, 2, 1).astype(np.int8)
+    lens = g.integers(0, 12, rows)
+    row_off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    index = np.concatenate([np.sort(g.choice(N, size=n, replace=False)) for n in lens]).astype(np.int32)
+    base = np.arange(rows, dtype=np.int64) * N
+    mo, ml = base.copy(), np.full(rows, N, np.int32)
+    _, loc, rem_idx, nl, nr = oracle.split(row_off, index, mask, mo, ml, 0)
+    # fetch the remote partition only: pool pages in reverse order, store = [rows][N]
+    max_pages = 4
+    pt = (np.arange(rows * max_pages)[::-1].reshape(rows, max_pages) * P).astype(np.int32)
+    kp = np.zeros((rows * max_pages * P, d), np.float32)
+    vp = np.zeros_like(kp)
+    kk = np.zeros((rows * N, d), np.float32)
+    vk = np.zeros_like(kk)
+    mask0 = mask.copy()
+    oracle.fetch_keep(row_off, rem_idx, nr, base, src, vsrc, pt, P, np.zeros(rows, np.int32), kp, vp,
+                      base, kk, vk, mask, mo, ml)
+    want_mask = mask0.copy()
+    for r in range(rows):
+        for i in range(nr[r]):
+            t = rem_idx[row_off[r] + i]
+            prow = pt[r, i // P] + i % P
+            np.testing.assert_array_equal(kp[prow], src[base[r] + t])
+            np.testing.assert_array_equal(vp[prow], vsrc[base[r] + t])
+            np.testing.assert_array_equal(kk[base[r] + t], src[base[r] + t])
+            np.testing.assert_array_equal(vk[base[r] + t], vsrc[base[r] + t])
+            want_mask[base[r] + t] = 1
+    np.testing.assert_array_equal(mask, want_mask)
+    kept = np.zeros(rows * N, bool)
+    for r in range(rows):
+        kept[base[r] + rem_idx[row_off[r]:row_off[r] + nr[r]]] = True
+    assert (kk[~kept] == 0).all()
+    _, loc2, _, nl2, nr2 = oracle.split(row_off, index, mask, mo, ml, 0)
+    assert (nr2 == 0).all()
+    np.testing.assert_array_equal(nl2, lens)
+    np.testing.assert_array_equal(loc2, index)
