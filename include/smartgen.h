@@ -19,6 +19,11 @@
  *                   importance, eq. 2 block budget, and the push of the chosen
  *                   KV blocks (Section 4.1); the global top-K_r of the blocks
  *                   is sg_topk over one row of L * M importances per request
+ *   sg_fetch_keep   on-demand fetch that keeps fetched rows in the decode
+ *                   side's store and marks them local (reuse, Section 4.2)
+ *   sg_spec_quota, sg_spec_push
+ *                   speculative transfer of the remaining KV blocks in
+ *                   importance order (Section 4.3)
  *
  * Conventions for every call:
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
@@ -157,18 +162,21 @@ int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,
  *       descending (remote entries first, then local, then pads);
  *   (2) local = entries with m == 1, (3) remote = entries with m == 2, both in
  *       row order, written from the start of the row's segment;
- *       n_local[r], n_remote[r] count them; the rest of each segment is -1.
+ *       n_local[r], n_remote[r] count them; the rest of each segment is -1;
+ *       n_kept[r] = n_local[r] + n_remote[r] (the row count of a decode set
+ *       assembled from both lanes) when n_kept is not NULL.
  *
  *   row_off device int32 [rows+1]; total = row_off[rows] (host copy).
  *   kv_index, out_index, local, remote: device int32 [total]; out_index may be
  *   NULL when reorder == 0.  mask: device int8 of mask_bytes entries; mask_off:
  *   device int64 [rows]; mask_len: device int32 [rows]; n_local, n_remote:
- *   device int32 [rows].  A mask entry outside [0, mask_bytes) counts as 0.
+ *   device int32 [rows]; n_kept: device int32 [rows] or NULL.  A mask entry
+ *   outside [0, mask_bytes) counts as 0.
  */
 int sg_split(void *stream, int rows, const int32_t *row_off, int64_t total,
              const int32_t *kv_index, const int8_t *mask, int64_t mask_bytes,
              const int64_t *mask_off, const int32_t *mask_len, int reorder, int32_t *out_index,
-             int32_t *local, int32_t *remote, int32_t *n_local, int32_t *n_remote);
+             int32_t *local, int32_t *remote, int32_t *n_local, int32_t *n_remote, int32_t *n_kept);
 
 /* ---------------------------------------------------------------- sg_fetch
  * Copies indexed K/V rows into paged destination slots: the remote lane of
@@ -197,6 +205,39 @@ int sg_fetch(void *stream, sg_dtype dt, int d, int rows, const int32_t *row_off,
              const void *k_src, const void *v_src,
              const int32_t *page_table, int page_size, int max_pages, const int32_t *dst_start,
              void *k_pool, void *v_pool, int64_t pool_rows);
+
+/* ---------------------------------------------------------------- sg_fetch_keep
+ * On-demand fetch with reuse of fetched entries (Section 4.2; the evaluation
+ * of Section 5.3 compares against keeping fetched entries).  The copy of
+ * sg_fetch, where every fetched entry is also kept in the decode side's KV
+ * store at its own token row and its KV mask entry turns local (1), so that a
+ * later sg_split finds it local.
+ *
+ * Row r, entry i < n_r (n_r as in sg_fetch), token t = index[row_off[r] + i]
+ * (index is required):
+ *   - an entry whose source row src_row_base[r] + t is outside [0, src_rows)
+ *     is skipped entirely;
+ *   - pool: as sg_fetch (logical row dst_start[r] + i through the page table)
+ *     when page_table is not NULL; with page_table NULL, dst_start, k_pool,
+ *     v_pool, page_size, max_pages and pool_rows are ignored;
+ *   - keep: row keep_row_base[r] + t of k_keep / v_keep when it lies in
+ *     [0, keep_rows); only then, when mask is not NULL, 0 <= t < mask_len[r]
+ *     and 0 <= mask_off[r] + t < mask_bytes: mask[mask_off[r] + t] = 1.
+ *
+ *   keep_row_base device int64 [rows]; k_keep, v_keep device, dtype rows of d;
+ *   mask device int8 [mask_bytes] or NULL; mask_off device int64 [rows];
+ *   mask_len device int32 [rows].  Store rows, pool rows and the mask become
+ *   visible to work ordered after the call (stream order or an event); two
+ *   entries that write one pool row leave either row.
+ */
+int sg_fetch_keep(void *stream, sg_dtype dt, int d, int rows, const int32_t *row_off, int64_t total,
+                  const int32_t *index, const int32_t *n_valid,
+                  const int64_t *src_row_base, int64_t src_rows,
+                  const void *k_src, const void *v_src,
+                  const int32_t *page_table, int page_size, int max_pages, const int32_t *dst_start,
+                  void *k_pool, void *v_pool, int64_t pool_rows,
+                  const int64_t *keep_row_base, void *k_keep, void *v_keep, int64_t keep_rows,
+                  int8_t *mask, int64_t mask_bytes, const int64_t *mask_off, const int32_t *mask_len);
 
 /* ---------------------------------------------------------------- sg_decode_attn
  * Decode attention over a partial KV set (Section 2.1; Section 4.2 notes that
@@ -263,6 +304,41 @@ size_t sg_pack_blocks_bytes(sg_dtype dt, int Hkv, int d, int64_t N, int M, int n
 int sg_pack_blocks(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, int64_t s0, int64_t N, int M,
                    const void *k, const void *v, int64_t kv_layer_rows, int nblk, const int32_t *ids,
                    void *dst, size_t dst_bytes);
+
+/* ---------------------------------------------------------------- speculative transfer
+ * Speculative transfer (Section 4.3): while the decode side computes
+ * attention, the prefill side pushes the KV blocks that the proactive transfer
+ * left behind, in importance order (eq. 1), a fixed fraction of all blocks
+ * (the speculative ratio) per transfer, and updates the KV mask.
+ *
+ * sg_spec_quota (host only): blocks per transfer, ceil(blocks * ratio_bp /
+ *   10000) clipped to [1, blocks] (0 for blocks = 0), so 1 / ratio transfers
+ *   deliver every block.  Returns -1 for blocks < 0, ratio_bp < 1 or overflow.
+ *
+ * The blocks of one transfer are the quota's top entries of `rem`, a float row
+ * of the L * M importances of a request in which every delivered block is NaN
+ * (sg_topk ranks NaN last): sg_topk(rem, k = min(quota, blocks left)).
+ *
+ * sg_spec_push: delivers blocks ids[0 .. nblk) of one request (tokens
+ *   [s0, s0 + N) of T, blocks of Nb = ceil(N / M) tokens).  For an id
+ *   c = l * M + m in [0, L M), every KV head h and block token
+ *   t = m * Nb + r < N:
+ *     k_dst, v_dst row l * dst_layer_rows + h * T + s0 + t
+ *         = k_src, v_src row l * src_layer_rows + h * T + s0 + t
+ *     mask[(l * Hkv + h) * T + s0 + t] = 1                 (local)
+ *   and rem[c] = NaN when rem is not NULL.  Other ids are skipped.
+ *   k_src, v_src: device or pinned host (the prefill side), at least
+ *   (L - 1) * src_layer_rows + Hkv * T rows (a stride of 0 shares one source
+ *   across layers); k_dst, v_dst: device (the decode side's store), at least
+ *   (L - 1) * dst_layer_rows + Hkv * T rows; ids device int32 [nblk]; mask
+ *   device int8 [L][Hkv][T]; rem device float [L M] or NULL.  Requires
+ *   s0 + N <= T and N > 0 when nblk > 0.  Store rows, mask and rem become
+ *   visible to work ordered after the call (stream order or an event).
+ */
+int64_t sg_spec_quota(int64_t blocks, int ratio_bp);
+int sg_spec_push(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, int64_t s0, int64_t N, int M,
+                 const void *k_src, const void *v_src, int64_t src_layer_rows, void *k_dst, void *v_dst,
+                 int64_t dst_layer_rows, int nblk, const int32_t *ids, int8_t *mask, float *rem);
 
 #ifdef __cplusplus
 }

@@ -1,5 +1,6 @@
 // Block-granular proactive selection (Section 4.1): block importance (eq. 1),
-// the block budget (eq. 2) and the block pack.  The global top-K_r of the
+// the block budget (eq. 2) and the block pack; speculative transfer of the
+// remaining blocks (Section 4.3).  The global top-K_r of the
 // blocks is sg_topk over one row of L * M block importances per request.
 //
 // sg_block_importance: 8 lanes per block, one KV head each (more heads
@@ -10,6 +11,9 @@
 //   tensor; the grid is flat over 16-byte vectors of the output, each thread
 //   issues the loads of all its vectors before any store (non-temporal), so
 //   the copy runs like a plain strided memcpy.
+// sg_spec_push (speculative transfer, Section 4.3): the same flat copy, with
+//   each row stored at its own position in the decode side's store, its mask
+//   entry turned local and the block marked in the remaining importances.
 #include <math.h>
 
 #include "sg_internal.h"
@@ -112,6 +116,59 @@ __global__ __launch_bounds__(BLK_THREADS) void pack_blocks_kernel(int L, int Hkv
         did[s] = ids[s];
 }
 
+// Speculative push: the grid is flat over 16-byte vectors of the pushed rows
+// like the block pack, but every row goes back to its own position in the
+// decode side's store; the lane holding vector 0 of a row turns its mask entry
+// local, and the first lane of a block takes the block out of the remaining
+// importances.
+template <int CPR>
+__global__ __launch_bounds__(BLK_THREADS) void spec_push_kernel(int L, int Hkv, int64_t T, int64_t s0, int64_t N,
+                                                                  int M, int64_t Nb, const v4u *__restrict__ k,
+                                                                  const v4u *__restrict__ v, int64_t src_layer_rows,
+                                                                  v4u *__restrict__ kd, v4u *__restrict__ vd,
+                                                                  int64_t dst_layer_rows, int nblk,
+                                                                  const int32_t *__restrict__ ids,
+                                                                  int8_t *__restrict__ mask, float *__restrict__ rem) {
+    const int64_t total = (int64_t)nblk * Hkv * Nb * CPR;
+    const int64_t stride = (int64_t)gridDim.x * BLK_THREADS * PB_UNROLL;
+    for (int64_t base = (int64_t)blockIdx.x * BLK_THREADS * PB_UNROLL + threadIdx.x; base < total; base += stride) {
+        v4u kr[PB_UNROLL], vr[PB_UNROLL];
+        int64_t row_dst[PB_UNROLL], mpos[PB_UNROLL];
+        int32_t lead[PB_UNROLL];
+        // every load of the pass first (a row that is not pushed reads the
+        // request's first row of layer 0 and is not stored)
+#pragma unroll
+        for (int u = 0; u < PB_UNROLL; ++u) {
+            const int64_t iu = base + (int64_t)u * BLK_THREADS;
+            const int64_t i = min(iu, total - 1);
+            const int64_t row = i / CPR, c = i % CPR;
+            const int64_t r = row % Nb, sh = row / Nb;
+            const int h = (int)(sh % Hkv), s = (int)(sh / Hkv);
+            const int32_t id = ids[s];
+            const bool valid = iu < total && id >= 0 && (int64_t)id < (int64_t)L * M;
+            const int l = valid ? id / M : 0, m = valid ? id % M : 0;
+            const int64_t t = (int64_t)m * Nb + r;
+            const bool ok = valid && t < N;
+            const int64_t off = (int64_t)h * T + s0 + (ok ? t : 0);
+            kr[u] = __builtin_nontemporal_load(k + ((int64_t)l * src_layer_rows + off) * CPR + c);
+            vr[u] = __builtin_nontemporal_load(v + ((int64_t)l * src_layer_rows + off) * CPR + c);
+            row_dst[u] = ok ? ((int64_t)l * dst_layer_rows + off) * CPR + c : -1;
+            mpos[u] = ok && c == 0 ? ((int64_t)l * Hkv + h) * T + s0 + t : -1;
+            lead[u] = valid && c == 0 && h == 0 && r == 0 ? id : -1;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < PB_UNROLL; ++u) {
+            if (row_dst[u] >= 0) {
+                __builtin_nontemporal_store(kr[u], kd + row_dst[u]);
+                __builtin_nontemporal_store(vr[u], vd + row_dst[u]);
+            }
+            if (mpos[u] >= 0) mask[mpos[u]] = 1;
+            if (rem && lead[u] >= 0) rem[lead[u]] = __builtin_nanf("");
+        }
+    }
+}
+
 }  // namespace sg
 
 using namespace sg;
@@ -181,4 +238,44 @@ extern "C" int sg_pack_blocks(void *stream, sg_dtype dt, int L, int Hkv, int d, 
         default: set_error("sg_pack_blocks: internal row size"); return SG_EINTERNAL;
     }
     return launch_status("sg_pack_blocks");
+}
+
+extern "C" int64_t sg_spec_quota(int64_t blocks, int ratio_bp) {
+    if (blocks < 0 || ratio_bp < 1) return -1;
+    if (blocks == 0) return 0;
+    if (blocks > (INT64_MAX - 9999) / ratio_bp) return -1;
+    return std::min<int64_t>(blocks, std::max<int64_t>(1, (blocks * ratio_bp + 9999) / 10000));
+}
+
+extern "C" int sg_spec_push(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, int64_t s0, int64_t N,
+                            int M, const void *k_src, const void *v_src, int64_t src_layer_rows, void *k_dst,
+                            void *v_dst, int64_t dst_layer_rows, int nblk, const int32_t *ids, int8_t *mask,
+                            float *rem) {
+    SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "sg_spec_push: unknown dtype %d", (int)dt);
+    SG_REQUIRE(L >= 1 && Hkv >= 1 && M >= 1, SG_EINVAL, "sg_spec_push: L, Hkv, M must be >= 1");
+    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "sg_spec_push: head dimension %d not supported", d);
+    SG_REQUIRE(T >= 0 && s0 >= 0 && N >= 0 && s0 + N <= T && nblk >= 0, SG_EINVAL,
+               "sg_spec_push: the request's tokens [s0, s0 + N) must lie in [0, T)");
+    SG_REQUIRE(src_layer_rows >= 0 && dst_layer_rows >= 0, SG_EINVAL, "sg_spec_push: negative layer stride");
+    if (nblk == 0) return SG_OK;
+    SG_REQUIRE(k_src && v_src && k_dst && v_dst && ids && mask, SG_EINVAL, "sg_spec_push: null pointer");
+    SG_REQUIRE(aligned16(k_src) && aligned16(v_src) && aligned16(k_dst) && aligned16(v_dst), SG_EINVAL,
+               "sg_spec_push: row arrays must be 16-byte aligned");
+    SG_REQUIRE(N > 0, SG_EINVAL, "sg_spec_push: blocks of an empty request");
+    const int cpr = d * esize_of(dt) / 16;
+    const int64_t Nb = (N + M - 1) / M;
+    const int64_t total = (int64_t)nblk * Hkv * Nb * cpr;
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, BLK_THREADS * PB_UNROLL), 65536));
+    hipStream_t s = as_stream(stream);
+    auto ks = reinterpret_cast<const v4u *>(k_src);
+    auto vs = reinterpret_cast<const v4u *>(v_src);
+    auto kd = reinterpret_cast<v4u *>(k_dst);
+    auto vd = reinterpret_cast<v4u *>(v_dst);
+    switch (cpr) {
+        case 8: spec_push_kernel<8><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem); break;
+        case 16: spec_push_kernel<16><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem); break;
+        case 32: spec_push_kernel<32><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem); break;
+        default: set_error("sg_spec_push: internal row size"); return SG_EINTERNAL;
+    }
+    return launch_status("sg_spec_push");
 }

@@ -25,13 +25,17 @@ __global__ __launch_bounds__(64 * SPLIT_WAVES) void split_kernel(
     const int8_t *__restrict__ mask, int64_t mask_bytes, const int64_t *__restrict__ mask_off,
     const int32_t *__restrict__ mask_len, int reorder, int32_t *__restrict__ out_index,
     int32_t *__restrict__ local, int32_t *__restrict__ remote, int32_t *__restrict__ n_local,
-    int32_t *__restrict__ n_remote) {
+    int32_t *__restrict__ n_remote, int32_t *__restrict__ n_kept) {
     const int r = blockIdx.x * SPLIT_WAVES + threadIdx.x / 64;
     if (r >= rows) return;
     const int lane = threadIdx.x % 64;
     int64_t o = row_off[r], e = row_off[r + 1];
     if (o < 0 || e < o || e > total) {  // bad device metadata: empty row
-        if (lane == 0) { n_local[r] = 0; n_remote[r] = 0; }
+        if (lane == 0) {
+            n_local[r] = 0;
+            n_remote[r] = 0;
+            if (n_kept) n_kept[r] = 0;
+        }
         return;
     }
     const int64_t n = e - o;
@@ -83,6 +87,7 @@ __global__ __launch_bounds__(64 * SPLIT_WAVES) void split_kernel(
     if (lane == 0) {
         n_local[r] = (int32_t)n1;
         n_remote[r] = (int32_t)n2;
+        if (n_kept) n_kept[r] = (int32_t)(n1 + n2);
     }
 }
 
@@ -93,7 +98,7 @@ using namespace sg;
 extern "C" int sg_split(void *stream, int rows, const int32_t *row_off, int64_t total,
                         const int32_t *kv_index, const int8_t *mask, int64_t mask_bytes,
                         const int64_t *mask_off, const int32_t *mask_len, int reorder, int32_t *out_index, int32_t *local,
-                        int32_t *remote, int32_t *n_local, int32_t *n_remote) {
+                        int32_t *remote, int32_t *n_local, int32_t *n_remote, int32_t *n_kept) {
     SG_REQUIRE(rows >= 0 && total >= 0 && mask_bytes >= 0, SG_EINVAL, "sg_split: negative size");
     if (rows == 0) return SG_OK;
     SG_REQUIRE(row_off && n_local && n_remote && mask_off && mask_len, SG_EINVAL, "sg_split: null pointer");
@@ -102,6 +107,6 @@ extern "C" int sg_split(void *stream, int rows, const int32_t *row_off, int64_t 
     const int blocks = (int)ceil_div(rows, SPLIT_WAVES);
     split_kernel<<<blocks, 64 * SPLIT_WAVES, 0, as_stream(stream)>>>(
         rows, row_off, total, kv_index, mask, mask_bytes, mask_off, mask_len, reorder ? 1 : 0, out_index, local, remote,
-        n_local, n_remote);
+        n_local, n_remote, n_kept);
     return launch_status("sg_split");
 }

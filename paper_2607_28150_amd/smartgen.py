@@ -28,6 +28,7 @@ EXPORTS = [
     "sg_fetch",
     "sg_decode_attn_workspace_size", "sg_decode_attn",
     "sg_block_importance", "sg_block_budget", "sg_pack_blocks_bytes", "sg_pack_blocks",
+    "sg_fetch_keep", "sg_spec_quota", "sg_spec_push",
 ]
 
 
@@ -60,7 +61,7 @@ def load() -> ctypes.CDLL:
     lib.sg_pack_bytes.argtypes = [_i, _i, _i, _i, _l]
     lib.sg_pack_bytes.restype = _sz
     lib.sg_pack.argtypes = [_vp, _i, _i, _i, _i, _i, _vp, _l, _vp, _l, _i, _vp, _vp, _l, _vp, _vp, _sz]
-    lib.sg_split.argtypes = [_vp, _i, _vp, _l, _vp, _vp, _l, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp]
+    lib.sg_split.argtypes = [_vp, _i, _vp, _l, _vp, _vp, _l, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _vp]
     lib.sg_fetch.argtypes = [_vp, _i, _i, _i, _vp, _l, _vp, _vp, _vp, _l, _vp, _vp, _vp, _i, _i, _vp, _vp, _vp, _l]
     lib.sg_decode_attn_workspace_size.argtypes = [_i] * 6
     lib.sg_decode_attn_workspace_size.restype = _sz
@@ -71,8 +72,13 @@ def load() -> ctypes.CDLL:
     lib.sg_pack_blocks_bytes.argtypes = [_i, _i, _i, _l, _i, _i]
     lib.sg_pack_blocks_bytes.restype = _sz
     lib.sg_pack_blocks.argtypes = [_vp, _i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _i, _vp, _vp, _sz]
+    lib.sg_fetch_keep.argtypes = [_vp, _i, _i, _i, _vp, _l, _vp, _vp, _vp, _l, _vp, _vp, _vp, _i, _i, _vp, _vp, _vp,
+                                  _l, _vp, _vp, _vp, _l, _vp, _l, _vp, _vp]
+    lib.sg_spec_quota.argtypes = [_l, _i]
+    lib.sg_spec_quota.restype = _l
+    lib.sg_spec_push.argtypes = [_vp, _i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _vp, _vp, _l, _i, _vp, _vp, _vp]
     for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn", "sg_block_importance",
-              "sg_pack_blocks"):
+              "sg_pack_blocks", "sg_fetch_keep", "sg_spec_push"):
         getattr(lib, f).restype = _i
     _lib = lib
     return lib
@@ -206,17 +212,17 @@ def sg_pack(k, v, idx, cu_seqlens, T, cu_k, K_total, max_k, dst, L=None, Hkv=Non
 # ------------------------------------------------------------------------ split
 
 def sg_split(row_off, kv_index, mask, mask_off, mask_len, reorder, local, remote, n_local, n_remote,
-             out_index=None, stream=None):
+             out_index=None, n_kept=None, stream=None):
     rows = row_off.numel() - 1
     total = kv_index.numel()
     _need(mask.dtype == torch.int8, "mask must be int8")
-    for t in (mask_off, mask_len, n_local, n_remote):
+    for t in (mask_off, mask_len, n_local, n_remote) + ((n_kept,) if n_kept is not None else ()):
         _need(t.numel() >= rows, "per-row arrays need one entry per row")
     for t in (local, remote) + ((out_index,) if out_index is not None else ()):
         _need(t.numel() >= total, "outputs need one entry per index")
     rc = load().sg_split(_stream(stream), rows, _ptr(row_off), int(total), _ptr(kv_index), _ptr(mask),
                          mask.numel(), _ptr(mask_off), _ptr(mask_len), int(bool(reorder)), _ptr(out_index),
-                         _ptr(local), _ptr(remote), _ptr(n_local), _ptr(n_remote))
+                         _ptr(local), _ptr(remote), _ptr(n_local), _ptr(n_remote), _ptr(n_kept))
     _check("sg_split", rc)
 
 
@@ -239,6 +245,46 @@ def sg_fetch(row_off, total, index, n_valid, src_row_base, k_src, v_src, page_ta
                          _ptr(n_valid), _ptr(src_row_base), src_rows, _ptr(k_src), _ptr(v_src), _ptr(page_table),
                          int(page_size), int(max_pages), _ptr(dst_start), _ptr(k_pool), _ptr(v_pool), pool_rows)
     _check("sg_fetch", rc)
+
+
+def sg_fetch_keep(row_off, total, index, n_valid, src_row_base, k_src, v_src, page_table, page_size, dst_start,
+                  k_pool, v_pool, keep_row_base, k_keep, v_keep, mask=None, mask_off=None, mask_len=None,
+                  stream=None):
+    """sg_fetch that also keeps each fetched row at keep row keep_row_base[r] + index
+    of k_keep / v_keep and turns its mask entry local; page_table=None skips the pool."""
+    rows = row_off.numel() - 1
+    d = k_src.shape[-1]
+    _need(k_keep.dtype == k_src.dtype and v_keep.dtype == v_src.dtype, "store and source dtypes differ")
+    src_rows = k_src.numel() // d
+    keep_rows = k_keep.numel() // d
+    _need(v_src.numel() >= src_rows * d and v_keep.numel() >= keep_rows * d, "v arrays smaller than k arrays")
+    _need(keep_row_base.dtype == torch.int64 and keep_row_base.numel() >= rows, "keep_row_base must be int64 [rows]")
+    _need(src_row_base.dtype == torch.int64 and src_row_base.numel() >= rows, "src_row_base must be int64 [rows]")
+    _need(index is not None and index.numel() >= total, "index shorter than total")
+    _need(n_valid is None or n_valid.numel() >= rows, "n_valid too short")
+    max_pages, pool_rows = 1, 0
+    if page_table is not None:
+        _need(k_pool.dtype == k_src.dtype and v_pool.dtype == v_src.dtype, "pool and source dtypes differ")
+        max_pages = page_table.shape[-1]
+        pool_rows = k_pool.numel() // d
+        _need(v_pool.numel() >= pool_rows * d, "v_pool smaller than k_pool")
+        _need(page_table.numel() >= rows * max_pages, "page_table must be [rows][max_pages]")
+        _need(dst_start.numel() >= rows, "dst_start too short")
+    if mask is not None:
+        _need(mask.dtype == torch.int8, "mask must be int8")
+        _need(mask_off.dtype == torch.int64 and mask_off.numel() >= rows and mask_len.numel() >= rows,
+              "mask_off (int64) and mask_len need one entry per row")
+    rc = load().sg_fetch_keep(_stream(stream), _dtype_code(k_src), d, rows, _ptr(row_off), int(total), _ptr(index),
+                              _ptr(n_valid), _ptr(src_row_base), src_rows, _ptr(k_src), _ptr(v_src),
+                              _ptr(page_table), int(page_size), int(max_pages),
+                              _ptr(dst_start) if page_table is not None else None,
+                              _ptr(k_pool) if page_table is not None else None,
+                              _ptr(v_pool) if page_table is not None else None, pool_rows,
+                              _ptr(keep_row_base), _ptr(k_keep), _ptr(v_keep), keep_rows,
+                              _ptr(mask), 0 if mask is None else mask.numel(),
+                              _ptr(mask_off) if mask is not None else None,
+                              _ptr(mask_len) if mask is not None else None)
+    _check("sg_fetch_keep", rc)
 
 
 # ------------------------------------------------------------------------ decode attention
@@ -341,3 +387,37 @@ def sg_pack_blocks(k, v, ids, s0, N, M, dst, L=None, kv_layer_rows=None, stream=
                                dst.numel() * dst.element_size())
     _check("sg_pack_blocks", rc)
     return dst
+
+
+# ----------------------------------------------------------------------------- speculative transfer (Section 4.3)
+
+def spec_quota(blocks, ratio_bp) -> int:
+    """Blocks per speculative transfer (host only): ceil(blocks * ratio_bp / 10000)."""
+    r = load().sg_spec_quota(int(blocks), int(ratio_bp))
+    if r < 0:
+        raise SmartgenError("sg_spec_quota", SG_EINVAL, "need blocks >= 0 and ratio_bp >= 1")
+    return int(r)
+
+
+def sg_spec_push(k_src, v_src, ids, s0, N, M, k_dst, v_dst, mask, rem=None, L=None, src_layer_rows=None,
+                 dst_layer_rows=None, stream=None):
+    """Delivers the blocks `ids` of one request from k_src / v_src [Lkv][Hkv][T][d]
+    (device or pinned host) into the store k_dst / v_dst [L][Hkv][T][d] at the same
+    rows, turns their mask [L][Hkv][T] entries local and their rem [L*M] entries NaN."""
+    _need(k_src.dtype == v_src.dtype == k_dst.dtype == v_dst.dtype, "k/v source and store dtypes differ")
+    _need(ids.dtype == torch.int32 and mask.dtype == torch.int8, "ids must be int32 and mask int8")
+    Lkv, Hkv, T, d = k_src.shape
+    Ld = k_dst.shape[0]
+    if L is None:
+        L = Ld
+    _need(tuple(k_dst.shape[1:]) == (Hkv, T, d) and v_dst.shape == k_dst.shape, "store must be [L][Hkv][T][d]")
+    _need(mask.numel() >= L * Hkv * T, "mask must be int8 [L][Hkv][T]")
+    _need(rem is None or (rem.dtype == torch.float32), "rem must be float32 [L*M]")
+    if src_layer_rows is None:
+        src_layer_rows = 0 if (Lkv == 1 and L > 1) else Hkv * T
+    if dst_layer_rows is None:
+        dst_layer_rows = 0 if (Ld == 1 and L > 1) else Hkv * T
+    rc = load().sg_spec_push(_stream(stream), _dtype_code(k_src), int(L), Hkv, d, int(T), int(s0), int(N), int(M),
+                             _ptr(k_src), _ptr(v_src), int(src_layer_rows), _ptr(k_dst), _ptr(v_dst),
+                             int(dst_layer_rows), ids.numel(), _ptr(ids), _ptr(mask), _ptr(rem))
+    _check("sg_spec_push", rc)

@@ -95,8 +95,8 @@ def test_pack_rejections(lib):
 
 
 def test_split_fetch_decode_rejections(lib):
-    assert lib.sg_split(None, -1, P, 0, P, P, 0, P, P, 0, None, P, P, P, P) == smartgen.SG_EINVAL
-    assert lib.sg_split(None, 2, P, 5, P, P, 10, P, P, 1, None, P, P, P, P) == smartgen.SG_EINVAL
+    assert lib.sg_split(None, -1, P, 0, P, P, 0, P, P, 0, None, P, P, P, P, None) == smartgen.SG_EINVAL
+    assert lib.sg_split(None, 2, P, 5, P, P, 10, P, P, 1, None, P, P, P, P, None) == smartgen.SG_EINVAL
     assert lib.sg_fetch(None, 1, 128, 1, P, 5, P, None, P, 10, P, P, P, 0, 1, P, P, P, 10) == smartgen.SG_EINVAL
     rc = lib.sg_decode_attn(None, 1, 1, 6, 4, 128, 0.1, P, P, P, 10, P, P, 16, 4, P, None, 0)
     assert rc == smartgen.SG_EINVAL
@@ -127,3 +127,30 @@ def test_block_mode_host_checks(lib):
     rc = lib.sg_pack_blocks(None, 1, 2, 8, 80, 100, 0, 20, 4, P, P, 800, 3, P, P, 1 << 20)      # d = 80
     assert rc == smartgen.SG_EUNSUPPORTED
     assert lib.sg_pack_blocks(None, 1, 2, 8, 128, 100, 0, 20, 4, P, P, 800, 0, P, P, 0) == smartgen.SG_OK
+
+
+def test_spec_and_keep_host_checks(lib):
+    # the paper's speculative ratios: 10% delivers 32 x 1024 blocks in 10 transfers, 20% in 5, 5% in 20
+    assert smartgen.spec_quota(32768, 1000) == 3277
+    assert smartgen.spec_quota(32768, 2000) == 6554
+    assert smartgen.spec_quota(32768, 500) == 1639
+    assert smartgen.spec_quota(5, 1) == 1 and smartgen.spec_quota(0, 1000) == 0
+    assert smartgen.spec_quota(10, 20000) == 10
+    assert lib.sg_spec_quota(-1, 1000) == -1 and lib.sg_spec_quota(10, 0) == -1
+    rc = lib.sg_spec_push(None, 1, 2, 8, 128, 100, 90, 20, 4, P, P, 800, P, P, 800, 3, P, P, None)   # s0 + N > T
+    assert rc == smartgen.SG_EINVAL
+    rc = lib.sg_spec_push(None, 1, 2, 8, 96, 100, 0, 20, 4, P, P, 800, P, P, 800, 3, P, P, None)     # d = 96
+    assert rc == smartgen.SG_EUNSUPPORTED
+    rc = lib.sg_spec_push(None, 1, 2, 8, 128, 100, 0, 20, 4, P, P, -1, P, P, 800, 3, P, P, None)     # stride
+    assert rc == smartgen.SG_EINVAL
+    assert lib.sg_spec_push(None, 1, 2, 8, 128, 100, 0, 20, 4, P, P, 800, P, P, 800, 0, P, P, None) == smartgen.SG_OK
+    # fetch with reuse: the index is required, and a mask needs its offsets
+    rc = lib.sg_fetch_keep(None, 1, 128, 1, P, 5, None, None, P, 10, P, P, None, 1, 1, None, None, None, 0,
+                           P, P, P, 10, None, 0, None, None)
+    assert rc == smartgen.SG_EINVAL and "null" in _err(lib)
+    rc = lib.sg_fetch_keep(None, 1, 128, 1, P, 5, P, None, P, 10, P, P, None, 1, 1, None, None, None, 0,
+                           P, P, P, 10, P, 10, None, None)
+    assert rc == smartgen.SG_EINVAL and "mask" in _err(lib)
+    rc = lib.sg_fetch_keep(None, 1, 128, 1, P, 5, P, None, P, 10, P, P, P, 1, 1, None, P, P, 10,
+                           P, P, P, 10, None, 0, None, None)
+    assert rc == smartgen.SG_EINVAL and "dst_start" in _err(lib)

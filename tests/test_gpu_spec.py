@@ -1,0 +1,182 @@
+"""GPU parity of speculative transfer (Section 4.3) and of on-demand fetch with
+reuse of fetched entries (Section 4.2) against the CPU oracle, through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.gpu_util import cu, raw, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _rows(shape, dtype, g):
+    x = g.standard_normal(shape, dtype=np.float32)
+    return torch.from_numpy(x).to(torch.bfloat16 if dtype == "bf16" else torch.float32)
+
+
+@pytest.mark.parametrize("dtype,d,lens,M,b,shared,pinned", [
+    ("bf16", 128, (8192,), 1024, 0, False, False),       # the paper's M: blocks of 8 tokens
+    ("bf16", 64, (1000, 37), 7, 1, False, False),        # second request, 6-token blocks, an empty block
+    ("f32", 64, (300,), 1024, 0, False, True),           # one-token blocks, empty ones; pinned-host source
+    ("f32", 128, (513, 90), 64, 0, True, False),         # one source shared by every layer
+])
+def test_spec_push_parity(gpu_lib, dtype, d, lens, M, b, shared, pinned):
+    L, Hkv = 3, 2
+    say("spec push", dtype, d, lens, M, b, shared, pinned)
+    g = np.random.default_rng(d + M + len(lens))
+    cus = np.concatenate([[0], np.cumsum(lens)])
+    T, s0, N = int(cus[-1]), int(cus[b]), lens[b]
+    Lkv = 1 if shared else L
+    k = _rows((Lkv, Hkv, T, d), dtype, g)
+    v = _rows((Lkv, Hkv, T, d), dtype, g)
+    kd0 = _rows((L, Hkv, T, d), dtype, g)
+    vd0 = _rows((L, Hkv, T, d), dtype, g)
+    mask0 = g.integers(0, 3, (L, Hkv, T)).astype(np.int8)
+    rem0 = g.standard_normal(L * M).astype(np.float32)
+    ids = g.choice(L * M, size=min(L * M, 41), replace=False).astype(np.int32)
+    ids[5] = L * M + 3                                           # invalid: skipped
+    ids[7] = -2
+    src_k = k.pin_memory() if pinned else k.cuda()
+    src_v = v.pin_memory() if pinned else v.cuda()
+    kd, vd = kd0.cuda(), vd0.cuda()
+    mask = torch.from_numpy(mask0).cuda()
+    rem = torch.from_numpy(rem0).cuda()
+    gpu_lib.sg_spec_push(src_k, src_v, cu(ids), s0, N, M, kd, vd, mask, rem, L=L,
+                         src_layer_rows=0 if shared else None)
+    torch.cuda.synchronize()
+    okd, ovd, omask, orem = raw(kd0), raw(vd0), mask0.copy(), rem0.copy()
+    oracle.spec_push(raw(k), raw(v), ids, s0, N, M, okd, ovd, omask, orem, L=L,
+                     src_layer_rows=0 if shared else None)
+    np.testing.assert_array_equal(raw(kd), okd)
+    np.testing.assert_array_equal(raw(vd), ovd)
+    np.testing.assert_array_equal(mask.cpu().numpy(), omask)
+    got = rem.cpu().numpy()
+    np.testing.assert_array_equal(np.isnan(got), np.isnan(orem))
+    np.testing.assert_array_equal(got[~np.isnan(orem)], orem[~np.isnan(orem)])
+
+
+def test_spec_schedule_llama8b_8k_shape(gpu_lib):
+    """Proactive top-K_r, then transfers of the 10% quota until every block is
+    delivered, at the 8B shape (32 x 1024 blocks of 8 tokens, 8 KV heads, bf16
+    d = 128): each transfer's ids and the remaining importances are bit-exact
+    against the oracle, and the store ends equal to the source."""
+    L, Hkv, d, N, M = 32, 8, 128, 8192, 1024
+    LM = L * M
+    say("spec schedule", L, Hkv, d, N, M)
+    g = np.random.default_rng(77)
+    imp = (g.standard_normal(LM) ** 2).astype(np.float32)
+    imp[:2 * M] = np.inf                                          # eq. 1: layers 0 and 1
+    imp[5000:5400] = np.float32(0.5)                              # ties
+    k = _rows((L, Hkv, N, d), "bf16", g)
+    v = _rows((L, Hkv, N, d), "bf16", g)
+    kdev, vdev = k.cuda(), v.cuda()
+    kd = torch.zeros_like(kdev)
+    vd = torch.zeros_like(vdev)
+    mask = torch.full((L, Hkv, N), 2, dtype=torch.int8, device="cuda")
+    rem = torch.from_numpy(imp).cuda()
+    Kr = gpu_lib.block_budget(M, L, 1.0, 6.5)
+    r = gpu_lib.spec_quota(LM, 1000)
+    assert (Kr, r) == (oracle.block_budget(M, L, 1.0, 6.5), oracle.spec_quota(LM, 1000)) == (4883, 3277)
+    o_rem = imp.copy()
+    ok_, ov_ = np.zeros((L, Hkv, N, d), np.uint16), np.zeros((L, Hkv, N, d), np.uint16)
+    om = np.full((L, Hkv, N), 2, np.int8)
+    kh, vh = raw(k), raw(v)
+    done, steps, quota = 0, 0, Kr
+    cu_row = cu([0, LM])
+    while done < LM:
+        q = min(quota, LM - done)
+        ids = torch.empty(q, dtype=torch.int32, device="cuda")
+        gpu_lib.sg_topk(rem.view(1, 1, LM), cu_row, LM, LM, cu([0, q]), q, ids.view(1, 1, q))
+        gpu_lib.sg_spec_push(kdev, vdev, ids, 0, N, M, kd, vd, mask, rem)
+        o_ids = oracle.topk(o_rem.reshape(1, 1, LM), [0, LM], [0, q])[0, 0]
+        oracle.spec_push(kh, vh, o_ids, 0, N, M, ok_, ov_, om, o_rem)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+        np.testing.assert_array_equal(np.isnan(rem.cpu().numpy()), np.isnan(o_rem))
+        done += q
+        steps += 1
+        quota = r
+        if steps == 2:                                          # a partial state, checked whole
+            np.testing.assert_array_equal(mask.cpu().numpy(), om)
+            np.testing.assert_array_equal(raw(kd), ok_)
+    assert steps == 1 + -(-(LM - Kr) // r) == 10
+    assert (mask == 1).all().item() and torch.isnan(rem).all().item()
+    assert torch.equal(kd, kdev) and torch.equal(vd, vdev)
+
+
+@pytest.mark.parametrize("dtype,d,pinned,pool,with_mask,n_valid", [
+    ("bf16", 128, True, True, True, False),    # remote lane: pinned-host source into the pool, kept, marked
+    ("bf16", 64, False, False, True, True),    # keep only (no pool), n_valid limits each row
+    ("f32", 128, False, True, False, False),   # no mask
+    ("f32", 64, True, True, True, True),
+])
+def test_fetch_keep_parity(gpu_lib, dtype, d, pinned, pool, with_mask, n_valid):
+    say("fetch keep", dtype, d, pinned, pool, with_mask, n_valid)
+    g = np.random.default_rng(d + 3 * pinned + 5 * pool + 7 * with_mask + 11 * n_valid)
+    rows, N, P, max_pages = 40, 700, 16, 8
+    lens = g.integers(0, 120, rows)
+    lens[3] = 0
+    row_off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    index = np.concatenate([np.sort(g.choice(N, size=n, replace=False)) for n in lens]).astype(np.int32)
+    index[5] = N + 1000                                          # source row out of range: skipped
+    index[9] = -1
+    src = _rows((rows * N, d), dtype, g)
+    vsrc = _rows((rows * N, d), dtype, g)
+    src_base = (np.arange(rows) * N).astype(np.int64)
+    keep_base = src_base.copy()
+    keep_rows = rows * N + 50
+    keep_base[7] = rows * N + 20                                 # into a spare zone; t >= 30 falls off the store
+    perm = g.permutation(rows * max_pages).reshape(rows, max_pages)
+    pt = (perm * P).astype(np.int32)
+    pt[2, 1] = -P                                                # an invalid page
+    pool_rows = rows * max_pages * P
+    nv = np.minimum(lens, g.integers(0, 120, rows)).astype(np.int32)
+    mask0 = g.integers(0, 3, rows * N).astype(np.int8)
+    mo = src_base.copy()
+    ml = np.full(rows, N, np.int32)
+    ml[4] = 100
+    dst_start = g.integers(0, 3, rows).astype(np.int32)
+    kp0 = _rows((pool_rows, d), dtype, g)
+    vp0 = _rows((pool_rows, d), dtype, g)
+    kk0 = _rows((keep_rows, d), dtype, g)
+    vk0 = _rows((keep_rows, d), dtype, g)
+    s_k = src.pin_memory() if pinned else src.cuda()
+    s_v = vsrc.pin_memory() if pinned else vsrc.cuda()
+    kp, vp, kk, vk = kp0.cuda(), vp0.cuda(), kk0.cuda(), vk0.cuda()
+    mask = torch.from_numpy(mask0).cuda()
+    gpu_lib.sg_fetch_keep(cu(row_off), int(row_off[-1]), cu(index), cu(nv) if n_valid else None,
+                          cu(src_base, dtype=torch.int64), s_k, s_v, cu(pt) if pool else None, P, cu(dst_start),
+                          kp, vp, cu(keep_base, dtype=torch.int64), kk, vk,
+                          mask if with_mask else None, cu(mo, dtype=torch.int64), cu(ml))
+    torch.cuda.synchronize()
+    okp, ovp, okk, ovk, om = raw(kp0), raw(vp0), raw(kk0), raw(vk0), mask0.copy()
+    oracle.fetch_keep(row_off, index, nv if n_valid else None, src_base, raw(src), raw(vsrc), pt if pool else None,
+                      P, dst_start, okp, ovp, keep_base, okk, ovk, om if with_mask else None, mo, ml)
+    np.testing.assert_array_equal(raw(kp), okp)
+    np.testing.assert_array_equal(raw(vp), ovp)
+    np.testing.assert_array_equal(raw(kk), okk)
+    np.testing.assert_array_equal(raw(vk), ovk)
+    np.testing.assert_array_equal(mask.cpu().numpy(), om)
+
+
+def test_split_reports_kept_rows(gpu_lib):
+    say("split n_kept")
+    g = np.random.default_rng(5)
+    rows, N = 50, 300
+    lens = g.integers(0, 200, rows)
+    row_off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    ix = np.concatenate([g.choice(N + 20, size=n, replace=False) for n in lens]).astype(np.int32)
+    mask = g.integers(0, 4, rows * N).astype(np.int8)
+    mo = (np.arange(rows) * N).astype(np.int64)
+    ml = np.full(rows, N, np.int32)
+    tot = int(row_off[-1])
+    outs = [torch.empty(tot, dtype=torch.int32, device="cuda") for _ in range(2)]
+    cnt = [torch.full((rows,), -7, dtype=torch.int32, device="cuda") for _ in range(3)]
+    gpu_lib.sg_split(cu(row_off), cu(ix), cu(mask, dtype=torch.int8), cu(mo, dtype=torch.int64), cu(ml), 0,
+                     outs[0], outs[1], cnt[0], cnt[1], n_kept=cnt[2])
+    torch.cuda.synchronize()
+    _, _, _, nl, nr = oracle.split(row_off, ix, mask, mo, ml, 0)
+    np.testing.assert_array_equal(cnt[0].cpu().numpy(), nl)
+    np.testing.assert_array_equal(cnt[1].cpu().numpy(), nr)
+    np.testing.assert_array_equal(cnt[2].cpu().numpy(), nl + nr)
