@@ -1,0 +1,117 @@
+"""Parallel on-demand transfer with reuse (Section 4.2): the two lanes on two
+streams against the oracle replaying the same steps, at the 8B / 32K-token
+shape (5% selected, 2% fetched on demand per step), two layers."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from datagen import configs, inputs
+from paper_2607_28150_amd.lanes import StepBuffers, TwoLane
+from tests.gpu_util import cu, raw, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _f32_rows(a, dt):
+    if dt == torch.bfloat16:
+        return (a.astype(np.uint32) << 16).view(np.float32)
+    return a
+
+
+@pytest.mark.parametrize("reuse", [True, False])
+def test_two_lane_steps_llama8b_32k(gpu_lib, reuse):
+    cfg = configs.get("llama8b_32k")
+    layers = (0, 31)
+    Ls, Hkv, d, P, steps = len(layers), cfg.Hkv, cfg.d, 16, 3
+    say("two-lane steps llama8b_32k", layers, "reuse", reuse)
+    pre = inputs.make_prefill(cfg, device="cuda")
+    lens, T = pre["seqlens"], pre["T"]
+    N = lens[0]
+    bud = inputs.make_budget(cfg, lens)
+    cu_k, kb = bud["cu_k"], bud["k"][0]
+    sel = inputs.random_selection(cfg, lens, bud["k"], device="cuda")          # [L][Hkv][K]
+    dt = pre["k"].dtype
+    src_k = pre["k"][list(layers)].contiguous().cpu().pin_memory()             # the prefill side's copy
+    src_v = pre["v"][list(layers)].contiguous().cpu().pin_memory()
+    units = [(li, h) for li in range(Ls) for h in range(Hkv)]
+    rows = len(units)
+    base = np.array([(li * Hkv + h) * T for (li, h) in units], np.int64)
+    base_d = cu(base, dtype=torch.int64)
+    mlen = cu(np.full(rows, N, np.int32))
+    # decode side: the store and its mask, filled with the proactively sent rows
+    store_k = torch.zeros((Ls, Hkv, T, d), dtype=dt, device="cuda")
+    store_v = torch.zeros_like(store_k)
+    mask = torch.full((Ls, Hkv, T), 2, dtype=torch.int8, device="cuda")
+    sel_rows = [sel[layers[li], h, cu_k[0]:cu_k[1]].cpu().numpy() for (li, h) in units]
+    sel_off = cu(np.arange(rows + 1) * kb)
+    sel_flat = cu(np.concatenate(sel_rows))
+    gpu_lib.sg_fetch_keep(sel_off, rows * kb, sel_flat, None, base_d, src_k, src_v, None, 1, None, None, None,
+                          base_d, store_k, store_v, mask.view(-1), base_d, mlen)
+    o_store_k = np.zeros((Ls * Hkv * T, d), raw(store_k[:0]).dtype)
+    o_store_v = np.zeros_like(o_store_k)
+    o_mask = np.full(Ls * Hkv * T, 2, np.int8)
+    hk, hv = raw(src_k).reshape(-1, d), raw(src_v).reshape(-1, d)
+    oracle.fetch_keep(np.arange(rows + 1) * kb, np.concatenate(sel_rows), None, base, hk, hv, None, 1,
+                      np.zeros(rows, np.int32), None, None, base, o_store_k, o_store_v, o_mask, base,
+                      np.full(rows, N, np.int32))
+    # pool pages: every unit owns ceil(max rows / P) pages, scattered
+    e = inputs.extras_count(N, cfg.extra_bp)
+    max_pages = -(-(kb + e) // P)
+    perm = np.random.default_rng(9).permutation(rows * max_pages + 5)[:rows * max_pages]
+    pt = (perm.reshape(rows, max_pages) * P).astype(np.int32)
+    pool_rows = (rows * max_pages + 5) * P
+    pt_d = cu(pt)
+    lanes = TwoLane()
+    ratios, o_ratios = [], []
+    for step in range(steps):
+        say("two-lane step", step)
+        ex = [inputs.extras_for_step(cfg, step, lens, sel[l], cu_k, l) for l in layers]
+        idx_rows = [np.concatenate([ex[li][h].cpu().numpy(), sel_rows[i]]).astype(np.int32)
+                    for i, (li, h) in enumerate(units)]
+        row_off = np.cumsum([0] + [len(r) for r in idx_rows]).astype(np.int32)
+        kv_index = np.concatenate(idx_rows)
+        total = int(row_off[-1])
+        kp = torch.zeros((pool_rows, d), dtype=dt, device="cuda")
+        vp = torch.zeros_like(kp)
+        buf = StepBuffers.alloc(rows, total)
+        n_kept = lanes.gather(row_off=cu(row_off), kv_index=cu(kv_index), mask=mask.view(-1), mask_off=base_d,
+                              mask_len=mlen, store_k=store_k, store_v=store_v, store_base=base_d, src_k=src_k,
+                              src_v=src_v, src_base=base_d, page_table=pt_d, page_size=P, k_pool=kp, v_pool=vp,
+                              buf=buf, reuse=reuse)
+        q = inputs.decode_queries(cfg, step, device="cuda", mu=pre["mu"])[0, list(layers)].contiguous()
+        out = torch.empty((Ls, cfg.Hq, d), dtype=torch.float32, device="cuda")
+        ws = torch.empty(max(1, gpu_lib.decode_workspace_size(Ls, cfg.Hq, Hkv, d, max_pages, P)), dtype=torch.uint8,
+                         device="cuda")
+        gpu_lib.sg_decode_attn(q, kp, vp, pt_d.view(Ls, Hkv, max_pages), n_kept, P, out, ws=ws)
+        torch.cuda.synchronize()
+        # the oracle replays the step on its own state
+        r_out, r_loc, r_rem, r_nl, r_nr = oracle.split(row_off, kv_index, o_mask, base, np.full(rows, N), 1)
+        np.testing.assert_array_equal(buf.order[:total].cpu().numpy(), r_out)
+        np.testing.assert_array_equal(buf.n_local.cpu().numpy(), r_nl)
+        np.testing.assert_array_equal(buf.n_remote.cpu().numpy(), r_nr)
+        np.testing.assert_array_equal(n_kept.cpu().numpy(), r_nl + r_nr)
+        okp = np.zeros((pool_rows, d), o_store_k.dtype)
+        ovp = np.zeros_like(okp)
+        oracle.fetch(row_off, r_loc, r_nl, base, o_store_k, o_store_v, pt, P, r_nr, okp, ovp)
+        if reuse:
+            oracle.fetch_keep(row_off, r_rem, r_nr, base, hk, hv, pt, P, np.zeros(rows, np.int32), okp, ovp,
+                              base, o_store_k, o_store_v, o_mask, base, np.full(rows, N, np.int32))
+        else:
+            oracle.fetch(row_off, r_rem, r_nr, base, hk, hv, pt, P, np.zeros(rows, np.int32), okp, ovp)
+        np.testing.assert_array_equal(raw(kp), okp)
+        np.testing.assert_array_equal(raw(vp), ovp)
+        np.testing.assert_array_equal(mask.view(-1).cpu().numpy(), o_mask)
+        ref = oracle.decode_attn(q.float().cpu().numpy(), _f32_rows(okp, dt), _f32_rows(ovp, dt),
+                                 pt.reshape(Ls, Hkv, max_pages), (r_nl + r_nr).reshape(Ls, Hkv), P)
+        np.testing.assert_allclose(out.cpu().numpy(), ref, atol=2e-2, rtol=0)
+        ratios.append(buf.n_remote.sum().item() / n_kept.sum().item())
+        o_ratios.append(r_nr.sum() / (r_nl + r_nr).sum())
+    np.testing.assert_array_equal(raw(store_k).reshape(-1, d), o_store_k)
+    np.testing.assert_array_equal(raw(store_v).reshape(-1, d), o_store_v)
+    assert ratios == pytest.approx(o_ratios, abs=0)
+    assert ratios[0] == pytest.approx(e / (kb + e))                         # step 0: every extra is remote
+    if reuse:
+        assert ratios[-1] <= ratios[0]
+    else:
+        assert ratios == pytest.approx([ratios[0]] * steps)
