@@ -50,6 +50,7 @@ def parse():
     p.add_argument("--workload", default="llama8b_8k")
     p.add_argument("--decode-steps", type=int, default=None, help="decode steps per step (default: workload's)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-decode-side", action="store_true", help="skip the 32K-token decode-side section")
     p.add_argument("--cpu-layers", type=int, default=0, help="layers the oracle is timed on (0 = all)")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="repeat the oracle sample to at least this long")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -202,6 +203,9 @@ def main():
     # layer, transfer time 6.5x the prefill time), timed on its own
     blk = block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize)
 
+    # the decode side of the 32K-token workload: two lanes, reuse, speculative transfer
+    dside = None if args.no_decode_side else decode_side(sg)
+
     # ------------------------------------------------------------- per-op times (HIP events on the launch stream)
     def ms(a, b):
         return a.elapsed_time(b)
@@ -231,6 +235,7 @@ def main():
                          "frac_mfma_peak": round(score_flops / (t_score_lse * 1e-3) / 1e12 / peak_mfma, 4),
                          "note": "one pass: row normalisers supplied by the prefill attention"},
         "block_mode": blk,
+        "decode_side": dside,
         "topk": {"ms": round(t_topk, 4),
                  "gbs": round((scores.numel() * 4 + idx.numel() * 4) / (t_topk * 1e-3) / 1e9, 1)},
         "pack": {"ms": round(t_pack, 4), "gbs": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9, 1),
@@ -320,6 +325,199 @@ def block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize, M=1024, ratio=1 / 6
             "pack_ms": round(t[2], 4), "pack_gbs": round(pack_bytes / (t[2] * 1e-3) / 1e9, 1),
             "pack_frac_hbm_peak": round(pack_bytes / (t[2] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "pack_mb_algorithmic": round(pack_bytes / 1e6, 2)}
+
+
+def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
+    """Decode side of the 8B-shaped 32K-token workload (5% of the rows sent at
+    prefill, 2% more fetched on demand per step, all 32 layers per step):
+    Algorithm 1 and the two lanes of Section 4.2 (serial on one stream, or on
+    two streams; with and without reuse of fetched rows), and speculative
+    transfer (Section 4.3: the quota of remaining blocks pushed while the
+    attention runs; the next step's split waits for it).  The prefill side's
+    copy of K / V is pinned host memory, so the remote lane and the speculative
+    push cross the host link; the decode side's store is in HBM."""
+    import numpy as np
+    import torch
+    from datagen import inputs
+    from datagen.configs import get
+    from paper_2607_28150_amd.lanes import StepBuffers, TwoLane
+
+    cfg = get("llama8b_32k")
+    dev = "cuda"
+    L, Hq, Hkv, d, W, P = cfg.L, cfg.Hq, cfg.Hkv, cfg.d, cfg.W, cfg.page_size
+    pre = inputs.make_prefill(cfg, device=dev)
+    lens, T = pre["seqlens"], pre["T"]
+    N = lens[0]
+    bud = inputs.make_budget(cfg, lens)
+    kb = bud["k"][0]
+    e = inputs.extras_count(N, cfg.extra_bp)
+    sel = inputs.random_selection(cfg, lens, bud["k"], device=dev)               # [L][Hkv][kb]
+    src_k = pre["k"].cpu().pin_memory()
+    src_v = pre["v"].cpu().pin_memory()
+    store_k = torch.zeros_like(pre["k"])
+    store_v = torch.zeros_like(pre["v"])
+    mask = torch.empty((L, Hkv, T), dtype=torch.int8, device=dev)
+    rows = L * Hkv
+    base = torch.arange(rows, device=dev, dtype=torch.int64) * T
+    mlen = torch.full((rows,), N, dtype=torch.int32, device=dev)
+    sel_off = (torch.arange(rows + 1, device=dev) * kb).to(torch.int32)
+
+    def reset():
+        mask.fill_(2)
+        sg.sg_fetch_keep(sel_off, rows * kb, sel.view(-1), None, base, src_k, src_v, None, 1, None, None, None,
+                         base, store_k, store_v, mask.view(-1), base, mlen)
+
+    # each step's KV index per (layer, head): that step's extras, then the selected rows
+    per = kb + e
+    idx = torch.empty((nsteps, rows, per), dtype=torch.int32, device=dev)
+    for s in range(nsteps):
+        for l in range(L):
+            ex = inputs.extras_for_step(cfg, s, lens, sel[l], bud["cu_k"], l)
+            for h in range(Hkv):
+                idx[s, l * Hkv + h, :e] = ex[h].to(torch.int32)
+        idx[s, :, e:] = sel.view(rows, kb)
+    row_off = (torch.arange(rows + 1, device=dev) * per).to(torch.int32)
+    max_pages = -(-per // P)
+    page_table = ((torch.arange(rows, device=dev)[:, None] * max_pages + torch.arange(max_pages, device=dev))
+                  * P).to(torch.int32).contiguous()
+    pool_rows = rows * max_pages * P
+    kp = torch.empty((pool_rows, d), dtype=pre["k"].dtype, device=dev)
+    vp = torch.empty_like(kp)
+    qdec = torch.stack([inputs.decode_queries(cfg, s, device=dev, mu=pre["mu"])[0] for s in range(nsteps)])
+    out = torch.empty((L, Hq, d), device=dev)
+    ws = torch.empty(max(16, sg.decode_workspace_size(L, Hq, Hkv, d, max_pages, P)), dtype=torch.uint8, device=dev)
+    buf = StepBuffers.alloc(rows, rows * per)
+    lanes = TwoLane()
+    zeros = buf.zeros
+    # speculative transfer: block importances from the window score (eq. 1)
+    scores = torch.empty((L, Hkv, T), device=dev)
+    cus = torch.tensor(pre["cu_seqlens"], dtype=torch.int32, device=dev)
+    ws_score = torch.empty(sg.score_workspace_size(1, L, Hq, Hkv, d, W, N), dtype=torch.uint8, device=dev)
+    sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score)
+    imp = torch.empty((1, L, M), device=dev)
+    sg.sg_block_importance(scores, cus, T, M, imp)
+    LM = L * M
+    quota = sg.spec_quota(LM, ratio_bp)
+    rem = torch.empty(LM, device=dev)
+    ids = torch.empty(quota, dtype=torch.int32, device=dev)
+    cu_row = torch.tensor([0, LM], dtype=torch.int32, device=dev)
+    spec_stream = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    counts = torch.empty((nsteps, 2, rows), dtype=torch.int32, device=dev)
+    # top-k offsets of every push size, made before any stream uses them
+    cu_q = {q: torch.tensor([0, q], dtype=torch.int32, device=dev) for q in {quota, LM % quota or quota}}
+
+    def run(mode):
+        reset()
+        rem.copy_(imp.view(-1))
+        left = LM
+        torch.cuda.synchronize()
+        t = []
+        for s in range(nsteps):
+            a, b = ev(), ev()
+            a.record(main)
+            if mode == "serial":
+                sg.sg_split(row_off, idx[s].view(-1), mask.view(-1), base, mlen, 1, buf.local, buf.remote,
+                            buf.n_local, buf.n_remote, out_index=buf.order, n_kept=buf.n_kept)
+                sg.sg_fetch(row_off, rows * per, buf.local, buf.n_local, base, store_k, store_v, page_table, P,
+                            buf.n_remote, kp, vp)
+                sg.sg_fetch_keep(row_off, rows * per, buf.remote, buf.n_remote, base, src_k, src_v, page_table, P,
+                                 zeros, kp, vp, base, store_k, store_v, mask.view(-1), base, mlen)
+            else:
+                lanes.gather(row_off=row_off, kv_index=idx[s].view(-1), mask=mask.view(-1), mask_off=base,
+                             mask_len=mlen, store_k=store_k, store_v=store_v, store_base=base, src_k=src_k,
+                             src_v=src_v, src_base=base, page_table=page_table, page_size=P, k_pool=kp, v_pool=vp,
+                             buf=buf, reuse=mode != "two_lane_no_reuse")
+            if mode == "speculative" and left > 0:
+                # the prefill side pushes the next blocks while the attention runs
+                q = min(quota, left)
+                go = torch.cuda.Event()
+                go.record(main)
+                spec_stream.wait_event(go)
+                sg.sg_topk(rem.view(1, 1, LM), cu_row, LM, LM, cu_q[q], q, ids[:q].view(1, 1, q), stream=spec_stream)
+                sg.sg_spec_push(src_k, src_v, ids[:q], 0, N, M, store_k, store_v, mask, rem, stream=spec_stream)
+                left -= q
+            sg.sg_decode_attn(qdec[s], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P, out, ws=ws)
+            if mode == "speculative":
+                done = torch.cuda.Event()
+                done.record(spec_stream)
+                main.wait_event(done)
+            b.record(main)
+            counts[s, 0].copy_(buf.n_remote)
+            counts[s, 1].copy_(buf.n_kept)
+            t.append((a, b))
+        torch.cuda.synchronize()
+        c = counts.double().sum(dim=2).cpu().numpy()
+        ratio = [round(float(x), 4) for x in c[:, 0] / c[:, 1]]
+        ms_steps = [a.elapsed_time(b) for a, b in t]
+        return {"ms_per_step": round(float(np.mean(ms_steps[1:])), 3), "ms_first": round(ms_steps[0], 3),
+                "ms_steps": [round(x, 3) for x in ms_steps],
+                "on_demand_ratio": ratio, "remote_rows_per_step": [int(x) for x in c[:, 0]]}
+
+    res = {"workload": cfg.name, "steps": nsteps, "rows_per_unit": per, "selected": kb, "extras": e}
+    for mode in ("serial", "two_lane", "two_lane_no_reuse", "speculative"):
+        res[mode] = run(mode)
+    res["speculative"]["ratio_bp"] = ratio_bp
+    res["speculative"]["blocks_per_push"] = quota
+    res["speculative"]["pushes_to_complete"] = -(-LM // quota)
+    # lane rates and interference, each on its own
+    reset()
+    torch.cuda.synchronize()
+    sg.sg_split(row_off, idx[1].view(-1), mask.view(-1), base, mlen, 1, buf.local, buf.remote, buf.n_local,
+                buf.n_remote, out_index=buf.order, n_kept=buf.n_kept)
+    torch.cuda.synchronize()
+    n_loc = int(buf.n_local.sum().item())
+    n_rem = int(buf.n_remote.sum().item())
+    rowb = 2 * d * pre["k"].element_size()
+    e0, e1, e2, e3 = ev(), ev(), ev(), ev()
+    e0.record()
+    sg.sg_fetch(row_off, rows * per, buf.local, buf.n_local, base, store_k, store_v, page_table, P, buf.n_remote,
+                kp, vp)
+    e1.record()
+    sg.sg_fetch(row_off, rows * per, buf.remote, buf.n_remote, base, src_k, src_v, page_table, P, zeros, kp, vp)
+    e2.record()
+    sg.sg_decode_attn(qdec[1], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P, out, ws=ws)
+    e3.record()
+    torch.cuda.synchronize()
+    t_loc, t_rem, t_dec = e0.elapsed_time(e1), e1.elapsed_time(e2), e2.elapsed_time(e3)
+    # decode attention alone and beside a speculative push on another stream
+    rem.copy_(imp.view(-1))
+    sg.sg_topk(rem.view(1, 1, LM), cu_row, LM, LM, cu_q[quota], quota, ids.view(1, 1, quota))
+    torch.cuda.synchronize()
+    f0, f1 = ev(), ev()
+    s0, s1 = ev(), ev()
+    s0.record(spec_stream)
+    sg.sg_spec_push(src_k, src_v, ids, 0, N, M, store_k, store_v, mask, None, stream=spec_stream)
+    s1.record(spec_stream)
+    f0.record(main)
+    for r in range(10):
+        sg.sg_decode_attn(qdec[r % nsteps], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P, out, ws=ws)
+    f1.record(main)
+    torch.cuda.synchronize()
+    t_dec_busy = f0.elapsed_time(f1) / 10
+    t_push = s0.elapsed_time(s1)
+    g0, g1 = ev(), ev()
+    g0.record()
+    for r in range(10):
+        sg.sg_decode_attn(qdec[r % nsteps], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P, out, ws=ws)
+    g1.record()
+    torch.cuda.synchronize()
+    t_dec_alone = g0.elapsed_time(g1) / 10
+    Nb = -(-N // M)
+    push_bytes = quota * Hkv * Nb * rowb
+    res["lanes"] = {"local_rows": n_loc, "local_ms": round(t_loc, 4),
+                    "local_gbs": round(n_loc * rowb * 2 / (t_loc * 1e-3) / 1e9, 1),
+                    "remote_rows": n_rem, "remote_ms": round(t_rem, 4),
+                    "remote_host_link_gbs": round(n_rem * rowb / (t_rem * 1e-3) / 1e9, 1),
+                    "decode_ms": round(t_dec, 4)}
+    res["spec_push"] = {"blocks": quota, "mb": round(push_bytes / 1e6, 1), "ms": round(t_push, 3),
+                        "host_link_gbs": round(push_bytes / (t_push * 1e-3) / 1e9, 1),
+                        "decode_ms_alone": round(t_dec_alone, 4), "decode_ms_beside_push": round(t_dec_busy, 4),
+                        "decode_slowdown": round(t_dec_busy / t_dec_alone, 3)}
+    del pre, src_k, src_v, store_k, store_v
+    torch.cuda.synchronize()
+    return res
 
 
 def window_lse(q_win, k, N, Hkv, W, d):

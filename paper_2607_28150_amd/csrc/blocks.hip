@@ -265,7 +265,8 @@ extern "C" int sg_spec_push(void *stream, sg_dtype dt, int L, int Hkv, int d, in
     const int cpr = d * esize_of(dt) / 16;
     const int64_t Nb = (N + M - 1) / M;
     const int64_t total = (int64_t)nblk * Hkv * Nb * cpr;
-    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, BLK_THREADS * PB_UNROLL), 65536));
+    const int64_t cap = host_memory(k_src) || host_memory(v_src) ? HOST_LINK_WORKGROUPS : 65536;
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, BLK_THREADS * PB_UNROLL), cap));
     hipStream_t s = as_stream(stream);
     auto ks = reinterpret_cast<const v4u *>(k_src);
     auto vs = reinterpret_cast<const v4u *>(v_src);

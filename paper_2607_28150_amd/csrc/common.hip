@@ -25,6 +25,15 @@ int launch_status(const char *what) {
     return SG_OK;
 }
 
+bool host_memory(const void *p) {
+    hipPointerAttribute_t a;
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();   // an unknown pointer is not an error of the next launch
+        return false;
+    }
+    return a.type == hipMemoryTypeHost;
+}
+
 }  // namespace sg
 
 extern "C" int sg_version(void) { return 100; }

@@ -27,15 +27,14 @@ struct KeepArgs {
 };
 
 template <int CPR, bool KEEP>
-__global__ __launch_bounds__(FETCH_THREADS) void fetch_kernel(
-    int rows, const int32_t *__restrict__ row_off, int64_t total, const int32_t *__restrict__ index,
+__device__ __forceinline__ void fetch_row(
+    int r, const int32_t *__restrict__ row_off, int64_t total, const int32_t *__restrict__ index,
     const int32_t *__restrict__ n_valid, const int64_t *__restrict__ src_row_base, int64_t src_rows,
     const v4u *__restrict__ k_src, const v4u *__restrict__ v_src, const int32_t *__restrict__ page_table,
     int page_size, int max_pages, const int32_t *__restrict__ dst_start, v4u *__restrict__ k_pool,
-    v4u *__restrict__ v_pool, int64_t pool_rows, KeepArgs keep) {
+    v4u *__restrict__ v_pool, int64_t pool_rows, const KeepArgs &keep) {
     constexpr int EPI = FETCH_THREADS / CPR;   // entries per step
     constexpr int EPB = EPI * FETCH_UNROLL;    // entries per block pass
-    const int r = blockIdx.x;
     const int64_t o = row_off[r], e = row_off[r + 1];
     if (o < 0 || e < o || e > total) return;
     int64_t n = e - o;
@@ -56,42 +55,49 @@ __global__ __launch_bounds__(FETCH_THREADS) void fetch_kernel(
     const int lane = threadIdx.x % CPR;
     const int esub = threadIdx.x / CPR;
 
+    if (src_rows <= 0) return;
     for (int64_t base = (int64_t)blockIdx.y * EPB; base < n; base += (int64_t)gridDim.y * EPB) {
+        // all index loads of the pass, then all row loads (an entry that is not
+        // copied reads source row 0), then the stores: every load is in flight
+        // before the first use
+        int64_t tok[FETCH_UNROLL];
+#pragma unroll
+        for (int j = 0; j < FETCH_UNROLL; ++j) {
+            const int64_t i = min(base + esub + j * EPI, n - 1);
+            tok[j] = index ? (int64_t)index[o + i] : i;
+        }
+        __builtin_amdgcn_sched_barrier(0);
         v4u kr[FETCH_UNROLL], vr[FETCH_UNROLL];
         int64_t dst[FETCH_UNROLL], kdst[FETCH_UNROLL], mpos[FETCH_UNROLL];
 #pragma unroll
         for (int j = 0; j < FETCH_UNROLL; ++j) {
             const int64_t i = base + esub + j * EPI;
+            const int64_t t = tok[j];
+            const int64_t src = sbase + t;
+            const bool live = i < n && src >= 0 && src < src_rows;
             dst[j] = -1;
             kdst[j] = -1;
             mpos[j] = -1;
-            if (i < n) {
-                const int64_t t = index ? (int64_t)index[o + i] : i;
-                const int64_t src = sbase + t;
-                if (src >= 0 && src < src_rows) {
-                    if (to_pool) {
-                        const int64_t lr = lbase + i;
-                        if (lr >= 0 && lr / page_size < max_pages) {
-                            const int64_t pr = (int64_t)pt[lr / page_size] + lr % page_size;
-                            if (pr >= 0 && pr < pool_rows) dst[j] = pr;
-                        }
-                    }
-                    if (KEEP) {
-                        const int64_t kr_row = kbase + t;
-                        if (kr_row >= 0 && kr_row < keep.rows) {
-                            kdst[j] = kr_row;
-                            if (keep.mask && lane == 0 && t >= 0 && t < mlen && moff + t >= 0 &&
-                                moff + t < keep.mask_bytes)
-                                mpos[j] = moff + t;
-                        }
-                    }
-                    if (dst[j] >= 0 || kdst[j] >= 0) {
-                        kr[j] = __builtin_nontemporal_load(k_src + src * CPR + lane);
-                        vr[j] = __builtin_nontemporal_load(v_src + src * CPR + lane);
-                    }
+            if (to_pool) {
+                const int64_t lr = lbase + i;
+                if (live && lr >= 0 && lr / page_size < max_pages) {
+                    const int64_t pr = (int64_t)pt[lr / page_size] + lr % page_size;
+                    if (pr >= 0 && pr < pool_rows) dst[j] = pr;
                 }
             }
+            if (KEEP) {
+                const int64_t kr_row = kbase + t;
+                if (live && kr_row >= 0 && kr_row < keep.rows) {
+                    kdst[j] = kr_row;
+                    if (keep.mask && lane == 0 && t >= 0 && t < mlen && moff + t >= 0 && moff + t < keep.mask_bytes)
+                        mpos[j] = moff + t;
+                }
+            }
+            const int64_t s_row = live ? src : 0;    // independent of the page-table loads
+            kr[j] = __builtin_nontemporal_load(k_src + s_row * CPR + lane);
+            vr[j] = __builtin_nontemporal_load(v_src + s_row * CPR + lane);
         }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < FETCH_UNROLL; ++j) {
             if (dst[j] >= 0) {
@@ -109,15 +115,31 @@ __global__ __launch_bounds__(FETCH_THREADS) void fetch_kernel(
     }
 }
 
+template <int CPR, bool KEEP>
+__global__ __launch_bounds__(FETCH_THREADS) void fetch_kernel(
+    int rows, const int32_t *__restrict__ row_off, int64_t total, const int32_t *__restrict__ index,
+    const int32_t *__restrict__ n_valid, const int64_t *__restrict__ src_row_base, int64_t src_rows,
+    const v4u *__restrict__ k_src, const v4u *__restrict__ v_src, const int32_t *__restrict__ page_table,
+    int page_size, int max_pages, const int32_t *__restrict__ dst_start, v4u *__restrict__ k_pool,
+    v4u *__restrict__ v_pool, int64_t pool_rows, KeepArgs keep) {
+    for (int r = blockIdx.x; r < rows; r += gridDim.x)
+        fetch_row<CPR, KEEP>(r, row_off, total, index, n_valid, src_row_base, src_rows, k_src, v_src, page_table,
+                             page_size, max_pages, dst_start, k_pool, v_pool, pool_rows, keep);
+}
+
 template <bool KEEP>
 int launch_fetch(const char *name, hipStream_t s, int cpr, int rows, const int32_t *row_off, int64_t total,
                  const int32_t *index, const int32_t *n_valid, const int64_t *src_row_base, int64_t src_rows,
                  const void *k_src, const void *v_src, const int32_t *page_table, int page_size, int max_pages,
                  const int32_t *dst_start, void *k_pool, void *v_pool, int64_t pool_rows, const KeepArgs &keep) {
-    // enough blocks per row to keep the host link or HBM busy; rows longer than
-    // one pass are covered by the grid-stride loop
-    const int ysplit = 4;
-    dim3 grid((unsigned)rows, ysplit);
+    // four workgroups per row keep HBM busy; from a host source the rows are
+    // shared out over HOST_LINK_WORKGROUPS workgroups.  Rows longer than one
+    // pass are covered by the grid-stride loops.
+    dim3 grid((unsigned)rows, 4);
+    if (host_memory(k_src) || host_memory(v_src)) {
+        grid.x = (unsigned)std::min(rows, HOST_LINK_WORKGROUPS);
+        grid.y = (unsigned)std::max(1, HOST_LINK_WORKGROUPS / (int)grid.x);
+    }
     auto ks = reinterpret_cast<const v4u *>(k_src);
     auto vs = reinterpret_cast<const v4u *>(v_src);
     auto kp = reinterpret_cast<v4u *>(k_pool);
