@@ -49,8 +49,13 @@ def _load():
                                   _f32p]
     lib.sgo_fetch_keep.argtypes = [_i, _i, _i, _i32p, _i32p, _i32p, _i64p, _l, _vp, _vp, _i32p, _i, _i, _i32p,
                                    _vp, _vp, _l, _i64p, _vp, _vp, _l, _i8p, _l, _i64p, _i32p]
+    lib.sgo_score_count.argtypes = [_i, _i, _i, _i, _i, _i, _i32p, _l, _f32p, _f32p, _l, ctypes.c_double,
+                                    ctypes.c_double, _i32p, _i32p]
+    lib.sgo_decode_select.argtypes = [_i, _i, _i, _i, _i, _f32p, _i32p, _l, _f32p, _l, _i32p, _l, ctypes.c_double,
+                                      _i32p, _i32p, _f64p]
     for f in ("sgo_score", "sgo_topk", "sgo_pack", "sgo_split", "sgo_fetch", "sgo_decode_attn", "sgo_threads",
-              "sgo_block_importance", "sgo_pack_blocks", "sgo_spec_push", "sgo_fetch_keep"):
+              "sgo_block_importance", "sgo_pack_blocks", "sgo_spec_push", "sgo_fetch_keep", "sgo_score_count",
+              "sgo_decode_select"):
         getattr(lib, f).restype = ctypes.c_int
     lib.sgo_set_threads.argtypes = [_i]
     lib.sgo_set_threads.restype = None
@@ -309,3 +314,44 @@ def fetch_keep(row_off, index, n_valid, src_row_base, k_src, v_src, page_table, 
                                 None if mask is None else _p(mask, _i8p), 0 if mask is None else mask.size,
                                 None if mask is None else _p(mo, _i64p), None if mask is None else _p(ml, _i32p))
     _check(rc, "fetch_keep")
+
+
+def score_count(q_win, k, cu_seqlens, Hkv, alpha, k_layer_rows=None, eps=None):
+    """Selection counts [L][Hkv][T] int32 under the alpha rule (and, with eps, the
+    per-key number of decisions within eps of the threshold: (counts, near))."""
+    q = _c(q_win, np.float32)
+    kk = _c(k, np.float32)
+    B, L, Hq, W, d = q.shape
+    T = kk.shape[2]
+    if k_layer_rows is None:
+        k_layer_rows = 0 if kk.shape[0] == 1 and L > 1 else Hkv * T
+    cu = _c(cu_seqlens, np.int32)
+    out = np.zeros((L, Hkv, T), dtype=np.int32)
+    near = np.zeros((L, Hkv, T), dtype=np.int32) if eps is not None else None
+    rc = _load().sgo_score_count(B, L, Hq, Hkv, d, W, _p(cu, _i32p), T, _p(q, _f32p), _p(kk, _f32p),
+                                 int(k_layer_rows), float(alpha), float(eps or 0.0), _p(out, _i32p),
+                                 None if near is None else _p(near, _i32p))
+    _check(rc, "score_count")
+    return out if eps is None else (out, near)
+
+
+def decode_select(q, k, cu_seqlens, Hkv, cu_cap, alpha, k_layer_rows=None):
+    """Decode-time selection: (idx [L][Hkv][K_cap] int32, n_sel [B][L][Hkv] int32,
+    r [L][Hkv][T] float64).  q [B][L][Hq][d]; k [Lkv][Hkv][T][d]."""
+    qq = _c(q, np.float32)
+    kk = _c(k, np.float32)
+    B, L, Hq, d = qq.shape
+    T = kk.shape[2]
+    if k_layer_rows is None:
+        k_layer_rows = 0 if kk.shape[0] == 1 and L > 1 else Hkv * T
+    cu = _c(cu_seqlens, np.int32)
+    cc = _c(cu_cap, np.int32)
+    K_cap = int(cc[-1])
+    idx = np.full((L, Hkv, max(K_cap, 1)), -7, dtype=np.int32)
+    n_sel = np.zeros((B, L, Hkv), dtype=np.int32)
+    r = np.full((L, Hkv, max(T, 1)), np.nan)
+    rc = _load().sgo_decode_select(B, L, Hq, Hkv, d, _p(qq, _f32p), _p(cu, _i32p), T, _p(kk, _f32p),
+                                   int(k_layer_rows), _p(cc, _i32p), K_cap, float(alpha), _p(idx, _i32p),
+                                   _p(n_sel, _i32p), _p(r, _f64p))
+    _check(rc, "decode_select")
+    return idx[:, :, :K_cap], n_sel, r[:, :, :T]

@@ -531,3 +531,150 @@ int sgo_fetch_keep(int rows, int esize, int d, const int32_t *row_off, const int
     }
     return SGO_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Selection-frequency score under a threshold selector (Section 4.1 defines a
+ * KV entry's importance as how often the decode-time selector picks it; the
+ * selector of the evaluation, InfiniGen with alpha = 5 (Section 5.1), picks
+ * the keys whose attention logit is within alpha of the row's maximum).  The
+ * window rows stand in for decode queries, as in sgo_score:
+ *     z_j = (1/sqrt(d)) * q[g][w] . K[h][j]  for j <= p,   m = max_j z_j,
+ *     count_j += [z_j >= m - alpha]
+ * over the G q heads of the group and the W rows, an integer in [0, G*W].
+ * When `near` is given, near_j counts the rows with |z_j - (m - alpha)| <= eps:
+ * the decisions that rounding of z could flip.
+ */
+int sgo_score_count(int B, int L, int Hq, int Hkv, int d, int W,
+                    const int32_t *cu_seqlens, int64_t T,
+                    const float *q_win, const float *k, int64_t k_layer_rows,
+                    double alpha, double eps, int32_t *counts, int32_t *near)
+{
+    if (B <= 0 || L <= 0 || Hkv <= 0 || Hq % Hkv != 0 || d <= 0 || W <= 0 || !(alpha >= 0.0)) return SGO_EINVAL;
+    const int G = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)d);
+    for (int b = 0; b < B; ++b)
+        if (cu_seqlens[b + 1] - cu_seqlens[b] < W) return SGO_EINVAL;
+    const int nunits = L * Hkv * B;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int u = 0; u < nunits; ++u) {
+        const int b = u % B;
+        const int h = (u / B) % Hkv;
+        const int l = u / (B * Hkv);
+        const int64_t N = cu_seqlens[b + 1] - cu_seqlens[b];
+        const float *K = k + ((int64_t)l * k_layer_rows + (int64_t)h * T + cu_seqlens[b]) * d;
+        int32_t *C = counts + ((int64_t)l * Hkv + h) * T + cu_seqlens[b];
+        int32_t *E = near ? near + ((int64_t)l * Hkv + h) * T + cu_seqlens[b] : NULL;
+        double *z = (double *)malloc(sizeof(double) * (size_t)N);
+        for (int64_t j = 0; j < N; ++j) {
+            C[j] = 0;
+            if (E) E[j] = 0;
+        }
+        for (int g = h * G; g < (h + 1) * G; ++g)
+            for (int w = 0; w < W; ++w) {
+                const float *q = q_win + ((((int64_t)b * L + l) * Hq + g) * W + w) * d;
+                const int64_t p = N - W + w;
+                double m = -INFINITY;
+                for (int64_t j = 0; j <= p; ++j) {
+                    double acc = 0.0;
+                    for (int c = 0; c < d; ++c) acc += (double)q[c] * (double)K[j * d + c];
+                    z[j] = acc * scale;
+                    if (z[j] > m) m = z[j];
+                }
+                const double thr = m - alpha;
+                for (int64_t j = 0; j <= p; ++j) {
+                    if (z[j] >= thr) C[j] += 1;
+                    if (E && fabs(z[j] - thr) <= eps) E[j] += 1;
+                }
+            }
+        free(z);
+    }
+    return SGO_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Decode-time dynamic selection (Section 2.3: the selector picks each step's
+ * KV entries from the decode query; Section 5.1: alpha = 5 and a maximum KV
+ * selection ratio of 20%).  For request b, layer l and KV head h, with the G q
+ * heads of its group and the request's N keys:
+ *     z[g][j] = (1/sqrt(d)) * q[b][l][g] . K[h][j],   m_g = max_j z[g][j]
+ *     r_j     = max_g (z[g][j] - m_g)          (<= 0, and 0 at each head's maximum)
+ *     S       = { j : r_j >= -alpha }          (some head of the group picks j)
+ * If |S| exceeds cap_b = cu_cap[b+1] - cu_cap[b], the cap_b entries of S with
+ * the largest r_j are kept (ties: lower j).  The kept ids go ascending to
+ * idx[l][h][cu_cap[b] ...], n_sel[(b*L + l)*Hkv + h] counts them, and the rest
+ * of the segment is -1.  r_out ([L][Hkv][T], optional) receives r.
+ * q: [B][L][Hq][d]; K: [Lkv][Hkv][T][d] with the given layer stride.
+ */
+typedef struct { double r; int32_t j; } sgo_rj;
+
+static int sgo_rj_cmp(const void *pa, const void *pb) {
+    const sgo_rj *a = (const sgo_rj *)pa, *b = (const sgo_rj *)pb;
+    if (a->r > b->r) return -1;
+    if (a->r < b->r) return 1;
+    return (a->j < b->j) ? -1 : (a->j > b->j);
+}
+
+static int sgo_i32_cmp(const void *pa, const void *pb) {
+    const int32_t a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+    return (a > b) - (a < b);
+}
+
+int sgo_decode_select(int B, int L, int Hq, int Hkv, int d, const float *q,
+                      const int32_t *cu_seqlens, int64_t T, const float *k, int64_t k_layer_rows,
+                      const int32_t *cu_cap, int64_t K_cap, double alpha,
+                      int32_t *idx, int32_t *n_sel, double *r_out)
+{
+    if (B <= 0 || L <= 0 || Hkv <= 0 || Hq % Hkv != 0 || d <= 0 || !(alpha >= 0.0)) return SGO_EINVAL;
+    const int G = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)d);
+    const int nunits = L * Hkv * B;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int u = 0; u < nunits; ++u) {
+        const int b = u % B;
+        const int h = (u / B) % Hkv;
+        const int l = u / (B * Hkv);
+        const int64_t N = cu_seqlens[b + 1] - cu_seqlens[b];
+        const int64_t cap = cu_cap[b + 1] - cu_cap[b];
+        const float *K = k + ((int64_t)l * k_layer_rows + (int64_t)h * T + cu_seqlens[b]) * d;
+        int32_t *out = idx + ((int64_t)l * Hkv + h) * K_cap + cu_cap[b];
+        double *r = (double *)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+        double *z = (double *)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+        for (int64_t j = 0; j < N; ++j) r[j] = -INFINITY;
+        for (int g = h * G; g < (h + 1) * G; ++g) {
+            const float *qg = q + (((int64_t)b * L + l) * Hq + g) * d;
+            double m = -INFINITY;
+            for (int64_t j = 0; j < N; ++j) {
+                double acc = 0.0;
+                for (int c = 0; c < d; ++c) acc += (double)qg[c] * (double)K[j * d + c];
+                z[j] = acc * scale;
+                if (z[j] > m) m = z[j];
+            }
+            for (int64_t j = 0; j < N; ++j)
+                if (z[j] - m > r[j]) r[j] = z[j] - m;
+        }
+        if (r_out)
+            for (int64_t j = 0; j < N; ++j) r_out[((int64_t)l * Hkv + h) * T + cu_seqlens[b] + j] = r[j];
+        sgo_rj *s = (sgo_rj *)malloc(sizeof(sgo_rj) * (size_t)(N > 0 ? N : 1));
+        int64_t ns = 0;
+        for (int64_t j = 0; j < N; ++j)
+            if (r[j] >= -alpha) {
+                s[ns].r = r[j];
+                s[ns].j = (int32_t)j;
+                ++ns;
+            }
+        if (ns > cap) {
+            qsort(s, (size_t)ns, sizeof(sgo_rj), sgo_rj_cmp);
+            ns = cap;
+        }
+        int32_t *ids = (int32_t *)malloc(sizeof(int32_t) * (size_t)(ns > 0 ? ns : 1));
+        for (int64_t i = 0; i < ns; ++i) ids[i] = s[i].j;
+        qsort(ids, (size_t)ns, sizeof(int32_t), sgo_i32_cmp);
+        for (int64_t i = 0; i < cap; ++i) out[i] = i < ns ? ids[i] : -1;
+        n_sel[((int64_t)b * L + l) * Hkv + h] = (int32_t)ns;
+        free(ids);
+        free(s);
+        free(z);
+        free(r);
+    }
+    return SGO_OK;
+}

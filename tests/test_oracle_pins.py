@@ -732,3 +732,96 @@ def test_fetch_keep_brute_force_and_reuse():
     assert (nr2 == 0).all()
     np.testing.assert_array_equal(nl2, lens)
     np.testing.assert_array_equal(loc2, index)
+
+
+# ----------------------------------------------------------------------------- selector variants
+
+def test_score_count_worked_examples():
+    for c in _golden("selector_worked.json")["count"]:
+        k = np.array(c["k"], np.float32).reshape(1, 1, -1, 1)
+        q = np.array(c["q"], np.float32).reshape(1, 1, 1, c["W"], 1)
+        got = oracle.score_count(q, k, [0, len(c["k"])], 1, c["alpha"])
+        np.testing.assert_array_equal(got[0, 0], c["expect"], err_msg=c["name"])
+
+
+def _brute_counts(q, k, N, W, G, alpha):
+    d = k.shape[-1]
+    out = np.zeros(N, np.int64)
+    for g in range(G):
+        for w in range(W):
+            p = N - W + w
+            z = (k[:p + 1].astype(np.float64) @ q[g, w].astype(np.float64)) / math.sqrt(d)
+            out[:p + 1] += z >= z.max() - alpha
+    return out
+
+
+@pytest.mark.parametrize("alpha", [0.5, 2.0, 5.0])
+def test_score_count_brute_force(alpha):
+    G, W, d, N = 3, 5, 8, 40
+    q = _rand((1, 1, G, W, d), 21)
+    k = _rand((1, 1, N, d), 22)
+    got = oracle.score_count(q, k, [0, N], 1, alpha)[0, 0]
+    np.testing.assert_array_equal(got, _brute_counts(q[0, 0], k[0, 0], N, W, G, alpha))
+    assert got.sum() >= G * W                                  # every row picks at least its maximum
+
+
+def test_score_count_limits():
+    G, W, d, N = 2, 6, 4, 30
+    q = _rand((1, 1, G, W, d), 23)
+    k = _rand((1, 1, N, d), 24)
+    # alpha beyond every logit gap: each row picks all it sees, G * #{w : N - W + w >= j}
+    seen = np.array([G * sum(1 for w in range(W) if N - W + w >= j) for j in range(N)])
+    np.testing.assert_array_equal(oracle.score_count(q, k, [0, N], 1, 1e9)[0, 0], seen)
+    # equal keys tie at the maximum: the same closed form at any alpha
+    keq = np.repeat(k[:, :, :1], N, axis=2)
+    np.testing.assert_array_equal(oracle.score_count(q, keq, [0, N], 1, 0.0)[0, 0], seen)
+    # alpha = 0 with distinct logits: each row picks its argmax only
+    want = np.zeros(N, np.int64)
+    for g in range(G):
+        for w in range(W):
+            p = N - W + w
+            want[np.argmax(k[0, 0, :p + 1].astype(np.float64) @ q[0, 0, g, w].astype(np.float64))] += 1
+    np.testing.assert_array_equal(oracle.score_count(q, k, [0, N], 1, 0.0)[0, 0], want)
+    # the near-threshold count is exact ties when eps = 0
+    _, near = oracle.score_count(q, keq, [0, N], 1, 0.0, eps=0.0)
+    np.testing.assert_array_equal(near[0, 0], seen)
+
+
+def test_decode_select_worked_examples():
+    for c in _golden("selector_worked.json")["select"]:
+        k = np.array(c["k"], np.float32).reshape(1, 1, -1, 1)
+        q = np.array(c["q"], np.float32).reshape(1, 1, 2, 1)
+        N = len(c["k"])
+        idx, n, _ = oracle.decode_select(q, k, [0, N], 1, [0, c["cap"]], c["alpha"])
+        assert n[0, 0, 0] == c["n"], c["name"]
+        np.testing.assert_array_equal(idx[0, 0, :c["n"]], c["expect"], err_msg=c["name"])
+        assert (idx[0, 0, c["n"]:] == -1).all()
+
+
+@pytest.mark.parametrize("alpha,cap_frac", [(5.0, 0.2), (1.0, 1.0), (3.0, 0.05), (0.0, 0.2)])
+def test_decode_select_brute_force(alpha, cap_frac):
+    B, L, Hq, Hkv, d = 2, 2, 4, 2, 16
+    lens = [50, 23]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    q = _rand((B, L, Hq, d), 25, scale=2.0)
+    k = _rand((L, Hkv, T, d), 26)
+    caps = [max(1, int(n * cap_frac)) for n in lens]
+    cc = np.concatenate([[0], np.cumsum(caps)])
+    idx, n_sel, r = oracle.decode_select(q, k, cu, Hkv, cc, alpha)
+    G = Hq // Hkv
+    for b in range(B):
+        for l in range(L):
+            for h in range(Hkv):
+                kb = k[l, h, cu[b]:cu[b + 1]].astype(np.float64)
+                z = np.stack([kb @ q[b, l, g].astype(np.float64) / math.sqrt(d) for g in range(h * G, (h + 1) * G)])
+                rr = (z - z.max(axis=1, keepdims=True)).max(axis=0)
+                np.testing.assert_allclose(r[l, h, cu[b]:cu[b + 1]], rr, rtol=0, atol=1e-12)
+                cand = [j for j in range(lens[b]) if rr[j] >= -alpha]
+                cand = sorted(cand, key=lambda j: (-rr[j], j))[:caps[b]]
+                seg = idx[l, h, cc[b]:cc[b + 1]]
+                assert n_sel[b, l, h] == len(cand)
+                np.testing.assert_array_equal(seg[:len(cand)], sorted(cand))
+                assert (seg[len(cand):] == -1).all()
+                # each head's maximum passes the rule (r = 0), so at least one entry is picked
+                assert n_sel[b, l, h] >= 1
