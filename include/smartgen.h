@@ -19,6 +19,10 @@
  *                   importance, eq. 2 block budget, and the push of the chosen
  *                   KV blocks (Section 4.1); the global top-K_r of the blocks
  *                   is sg_topk over one row of L * M importances per request
+ *   sg_score_count  selection-frequency importance under the alpha-threshold
+ *                   selector (Section 4.1, Section 5.1)
+ *   sg_decode_select  decode-time dynamic selection: alpha rule, capped
+ *                   (Section 2.3, Section 5.1)
  *   sg_fetch_keep   on-demand fetch that keeps fetched rows in the decode
  *                   side's store and marks them local (reuse, Section 4.2)
  *   sg_spec_quota, sg_spec_push
@@ -105,6 +109,28 @@ int sg_score(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, in
              const int32_t *cu_seqlens, int64_t T, int max_seqlen,
              const void *q_win, const void *k, int64_t k_layer_rows,
              const float *lse_in, float *scores, void *ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------- sg_score_count
+ * Selection-frequency importance under a threshold selector (Section 4.1
+ * defines importance as how often the decode-time selector picks an entry;
+ * Section 5.1 runs InfiniGen with alpha = 5, which picks the keys whose logit
+ * is within alpha of the row's maximum).  The window rows stand in for decode
+ * queries as in sg_score:
+ *
+ *   z_j = q_w . k_j / sqrt(d) (j <= position of row w),  m_w = max_j z_j
+ *   counts[l][h][s0 + j] = number of (q head, window row) pairs with
+ *                          z_j >= m_w - alpha
+ *
+ * an integer in [0, G * W] stored as float (so sg_topk ranks it directly;
+ * equal counts go to the lower index).  The decision is taken in fp32 on the
+ * raw products: q . k_j >= max_j' q . k_j' - alpha * sqrt(d).
+ * Arguments, layout and workspace as sg_score (lse_in does not apply; the
+ * workspace is required).  alpha must be finite and >= 0.
+ */
+int sg_score_count(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
+                   const int32_t *cu_seqlens, int64_t T, int max_seqlen,
+                   const void *q_win, const void *k, int64_t k_layer_rows,
+                   float alpha, float *counts, void *ws, size_t ws_bytes);
 
 /* ---------------------------------------------------------------- sg_topk
  * Exact top-k of every unit row (Section 2.3: each head of each request keeps
@@ -304,6 +330,37 @@ size_t sg_pack_blocks_bytes(sg_dtype dt, int Hkv, int d, int64_t N, int M, int n
 int sg_pack_blocks(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, int64_t s0, int64_t N, int M,
                    const void *k, const void *v, int64_t kv_layer_rows, int nblk, const int32_t *ids,
                    void *dst, size_t dst_bytes);
+
+/* ---------------------------------------------------------------- sg_decode_select
+ * Decode-time dynamic KV selection (Section 2.3: each decode step's selector
+ * picks KV entries from the step's query; Section 5.1: InfiniGen's alpha = 5
+ * and a maximum KV selection ratio of 20%).  For request b, layer l and KV
+ * head h, with the G q heads of its group and the request's N = N_b keys:
+ *
+ *   z[g][j] = q[b][l][g] . K[l][h][j] / sqrt(d),   m_g = max_j z[g][j]
+ *   r_j     = max over g of (z[g][j] - m_g)        (<= 0; 0 at each maximum)
+ *   S       = { j : r_j >= -alpha }                (some head of the group picks j)
+ *
+ * If |S| exceeds cap_b = cu_cap[b+1] - cu_cap[b], the cap_b entries with the
+ * largest r_j are kept (ties: lower j).  The kept ids go ascending to
+ * idx[l][h][cu_cap[b] ...], n_sel[b][l][h] counts them, and the rest of the
+ * segment is -1 (which sg_split drops as a pad).  r and the rule are computed
+ * in fp32.
+ *
+ *   q       device, dtype, [B][L][Hq][d] (the step's queries).
+ *   k       device, dtype, rows of d; unit (b, l, h) token j is row
+ *           l * k_layer_rows + h * T + cu_seqlens[b] + j.
+ *   cu_cap  device int32 [B+1]; idx device int32 [L][Hkv][K_cap] (output);
+ *   n_sel   device int32 [B][L][Hkv] (output).
+ *   ws      device workspace of sg_decode_select_workspace_size(...) bytes
+ *           (the logits of every q head).
+ * Requirements: G in {1, 2, 4, 8}, max_seqlen <= 32768, alpha finite and >= 0.
+ */
+size_t sg_decode_select_workspace_size(int B, int L, int Hq, int max_seqlen);
+int sg_decode_select(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, const void *q,
+                     const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *k, int64_t k_layer_rows,
+                     float alpha, const int32_t *cu_cap, int64_t K_cap, int32_t *idx, int32_t *n_sel,
+                     void *ws, size_t ws_bytes);
 
 /* ---------------------------------------------------------------- speculative transfer
  * Speculative transfer (Section 4.3): while the decode side computes

@@ -230,7 +230,29 @@ struct StatsFast {
     }
 };
 
-template <typename T, int D, int NW>
+// Count mode: only each row's exact maximum of the raw products q . k over
+// its visible keys (all keys unless MASK).
+template <typename T, int D, bool MASK>
+struct StatsMax {
+    static constexpr int NRB = QFrags<T, D>::NRB;
+    float (&m)[NRB];
+    int lane, wave, key0, N, W, R;
+    __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
+        using M = MT<T, D>;
+        int pos = N;
+        if (MASK) {
+            const int row = wave * 64 + rb * M::BM + lane % M::BM;
+            pos = row < R ? N - W + row % W : -1;
+        }
+        float mx = m[rb];
+#pragma unroll
+        for (int v = 0; v < M::NV; ++v)
+            mx = fmaxf(mx, (!MASK || key0 + kb * M::BM + M::crow(v, lane) <= pos) ? acc[v] : -INFINITY);
+        m[rb] = mx;
+    }
+};
+
+template <typename T, int D, int NW, bool MAXONLY>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void score_stats_kernel(
     int B, int L, int Hq, int Hkv, int W, const int32_t *__restrict__ cu_seqlens, int64_t T_,
     const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, float c2, int nchunk, int chunk_keys,
@@ -264,9 +286,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) zero[rb] = M::zero();
     // (reference, sum) of row wave * 64 + rb * BM + lane % BM over this lane's keys, log2 units
+    // (count mode: the row's maximum raw product, and no sum)
     float m[NRB], s[NRB];
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) { m[rb] = 0.f; s[rb] = 0.f; }
+    for (int rb = 0; rb < NRB; ++rb) { m[rb] = MAXONLY ? -INFINITY : 0.f; s[rb] = 0.f; }
     // one tile (in kbA when t is even, kbB when odd): wait for it, release the
     // other buffer, load the next tile, then `work`
     auto step = [&](int t, char *cur, char *nxt, auto &&work) {
@@ -276,13 +299,22 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
         work(cur, key0);
     };
     auto full = [&](const char *buf, int key0) {       // every row sees every key of the tile
-        unsigned need = 0u;
-        tile_sweep<T, D, true>(buf, q, zero, lane, StatsFast<T, D>{m, s, need, c2});
-        if (__any(need != 0u))             // rare: those blocks again, exactly
-            tile_sweep<T, D, true>(buf, q, zero, lane, StatsExact<T, D, false>{m, s, need, lane, wave, key0, N, W, R, c2});
+        if constexpr (MAXONLY) {
+            tile_sweep<T, D, true>(buf, q, zero, lane, StatsMax<T, D, false>{m, lane, wave, key0, N, W, R});
+        } else {
+            unsigned need = 0u;
+            tile_sweep<T, D, true>(buf, q, zero, lane, StatsFast<T, D>{m, s, need, c2});
+            if (__any(need != 0u))             // rare: those blocks again, exactly
+                tile_sweep<T, D, true>(buf, q, zero, lane,
+                                       StatsExact<T, D, false>{m, s, need, lane, wave, key0, N, W, R, c2});
+        }
     };
     auto masked = [&](const char *buf, int key0) {     // causal limit and prompt end (or a leftover full tile)
-        tile_sweep_plain<T, D, true>(buf, q, zero, lane, StatsExact<T, D, true>{m, s, ~0u, lane, wave, key0, N, W, R, c2});
+        if constexpr (MAXONLY)
+            tile_sweep_plain<T, D, true>(buf, q, zero, lane, StatsMax<T, D, true>{m, lane, wave, key0, N, W, R});
+        else
+            tile_sweep_plain<T, D, true>(buf, q, zero, lane,
+                                         StatsExact<T, D, true>{m, s, ~0u, lane, wave, key0, N, W, R, c2});
     };
     const int nfull = full_tiles(key_begin, ntile, KT::TK, N, W);
     int t = 0;
@@ -303,7 +335,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int off = M::BM; off < 64; off <<= 1) {
             const float mo = __shfl_xor(m[rb], off, 64), so = __shfl_xor(s[rb], off, 64);
             const float mn = fmaxf(m[rb], mo);
-            s[rb] = s[rb] * __builtin_amdgcn_exp2f(m[rb] - mn) + so * __builtin_amdgcn_exp2f(mo - mn);
+            if constexpr (!MAXONLY)
+                s[rb] = s[rb] * __builtin_amdgcn_exp2f(m[rb] - mn) + so * __builtin_amdgcn_exp2f(mo - mn);
             m[rb] = mn;
         }
         const int row = wave * 64 + rb * M::BM + lane;
@@ -317,7 +350,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
 // Column sums of one block: cs[kb] += sum over the lane's rows of
 // exp2(c2 * acc), where the products were accumulated onto minus each row's
 // normaliser (divided by c2), so acc * c2 = z * c2 - LSE_row in log2 units.
-template <typename T, int D, bool MASK>
+// Count mode (COUNT): the accumulators start at minus the row's threshold in
+// raw product units, and a key adds 1 where the row picks it (acc >= 0).
+template <typename T, int D, bool MASK, bool COUNT>
 struct ColsumStep {
     float (&cs)[KTile<T, D>::NKB];
     const int *poss;    // window position of every row of the unit (-1 for padded rows), LDS
@@ -336,7 +371,8 @@ struct ColsumStep {
             const int ps[4] = {pos.x, pos.y, pos.z, pos.w};
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float p = __builtin_amdgcn_exp2f(acc[4 * g4 + i] * c2);
+                const float p = COUNT ? (acc[4 * g4 + i] >= 0.f ? 1.f : 0.f)
+                                      : __builtin_amdgcn_exp2f(acc[4 * g4 + i] * c2);
                 t[i] += (!MASK || key <= ps[i]) ? p : 0.f;
             }
         }
@@ -344,11 +380,11 @@ struct ColsumStep {
     }
 };
 
-template <typename T, int D, int NW>
+template <typename T, int D, int NW, bool COUNT>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void score_colsum_kernel(
     int B, int L, int Hq, int Hkv, int W, const int32_t *__restrict__ cu_seqlens, int64_t T_,
     const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, float c2, int nchunk, int chunk_keys,
-    const float2 *__restrict__ part, const float *__restrict__ lse_in, float *__restrict__ scores) {
+    const float2 *__restrict__ part, const float *__restrict__ lse_in, float thr_off, float *__restrict__ scores) {
     using M = MT<T, D>;
     using KT = KTile<T, D>;
     constexpr int NRB = QFrags<T, D>::NRB, NKB = KT::NKB;
@@ -381,6 +417,20 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
     q.load(q_win + rbase * D, R, wave, lane);
     // row normalisers in log2 units: the caller's LSE, or the merge of the chunk statistics
     for (int r = threadIdx.x; r < NW * 64; r += 64 * NW) {
+        if constexpr (COUNT) {
+            // the row picks key j when q . k_j >= max - alpha sqrt(d) (raw units)
+            float start = -INFINITY;             // padded rows pick nothing
+            if (r < R) {
+                const int nc = (int)min<int64_t>(ceil_div(N, chunk_keys), nchunk);
+                const float2 *pr = part + u * nchunk * (int64_t)R + r;
+                float Mx = -INFINITY;
+                for (int c = 0; c < nc; ++c) Mx = fmaxf(Mx, pr[(int64_t)c * R].x);
+                start = -(Mx - thr_off);
+            }
+            nl2s[r] = start;
+            poss[r] = r < R ? N - W + r % W : -1;
+            continue;
+        }
         float l2 = INFINITY;                     // padded rows contribute exp2(-inf) = 0
         if (r < R) {
             if (lse_in) {
@@ -432,9 +482,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb) cs[kb] = 0.f;
         if (MASK)
-            tile_sweep_plain<T, D, false>(cur, q, c0, lane, ColsumStep<T, D, true>{cs, poss, lane, wave, key0, c2});
+            tile_sweep_plain<T, D, false>(cur, q, c0, lane, ColsumStep<T, D, true, COUNT>{cs, poss, lane, wave, key0, c2});
         else
-            tile_sweep<T, D, false>(cur, q, c0, lane, ColsumStep<T, D, false>{cs, poss, lane, wave, key0, c2});
+            tile_sweep<T, D, false>(cur, q, c0, lane, ColsumStep<T, D, false, COUNT>{cs, poss, lane, wave, key0, c2});
         // lanes holding the same key (different rows) add up; every such lane
         // then holds the total and stores it (same value, same address: no
         // branch, so the exponentials are not moved behind one)
@@ -479,35 +529,46 @@ static ScorePlan score_plan(int B, int L, int Hkv, int max_seqlen) {
     return p;
 }
 
+// thr_off < 0: probabilities; thr_off >= 0: count mode with the threshold
+// max - thr_off in raw product units (thr_off = alpha * sqrt(d)).
 template <typename T, int D, int NW>
 static void launch_passes(hipStream_t s, const ScorePlan &p, int B, int L, int Hq, int Hkv, int W,
                           const int32_t *cu_seqlens, int64_t ntok, const void *q_win, const void *k,
-                          int64_t k_layer_rows, float c2, const float *lse_in, float *scores, void *ws) {
+                          int64_t k_layer_rows, float c2, const float *lse_in, float thr_off, float *scores,
+                          void *ws) {
     float2 *part = reinterpret_cast<float2 *>(ws);
     const T *q = reinterpret_cast<const T *>(q_win);
     const T *kk = reinterpret_cast<const T *>(k);
     const dim3 grid((unsigned)((int64_t)L * Hkv * B * p.nchunk));
+    if (thr_off >= 0.f) {
+        score_stats_kernel<T, D, NW, true><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                                   k_layer_rows, c2, p.nchunk, p.chunk_keys, part);
+        score_colsum_kernel<T, D, NW, true><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                                    k_layer_rows, c2, p.nchunk, p.chunk_keys, part,
+                                                                    nullptr, thr_off, scores);
+        return;
+    }
     if (!lse_in)
-        score_stats_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
-                                                             k_layer_rows, c2, p.nchunk, p.chunk_keys, part);
-    score_colsum_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
-                                                          k_layer_rows, c2, p.nchunk, p.chunk_keys, part, lse_in,
-                                                          scores);
+        score_stats_kernel<T, D, NW, false><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                                    k_layer_rows, c2, p.nchunk, p.chunk_keys, part);
+    score_colsum_kernel<T, D, NW, false><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                                 k_layer_rows, c2, p.nchunk, p.chunk_keys, part,
+                                                                 lse_in, thr_off, scores);
 }
 
 template <typename T, int D>
-static int launch_score(hipStream_t s, int B, int L, int Hq, int Hkv, int W, const int32_t *cu_seqlens, int64_t ntok,
-                        int max_seqlen, const void *q_win, const void *k, int64_t k_layer_rows,
-                        const float *lse_in, float *scores, void *ws) {
+static int launch_score(const char *name, hipStream_t s, int B, int L, int Hq, int Hkv, int W,
+                        const int32_t *cu_seqlens, int64_t ntok, int max_seqlen, const void *q_win, const void *k,
+                        int64_t k_layer_rows, const float *lse_in, float thr_off, float *scores, void *ws) {
     const int R = (Hq / Hkv) * W;
     const int nw = (int)ceil_div(R, 64);
     const ScorePlan p = score_plan(B, L, Hkv, max_seqlen);
     const float c2 = SC_LOG2E / sqrtf((float)D);
-    if (nw <= 1) launch_passes<T, D, 1>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, scores, ws);
-    else if (nw <= 2) launch_passes<T, D, 2>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, scores, ws);
-    else if (nw <= 4) launch_passes<T, D, 4>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, scores, ws);
-    else launch_passes<T, D, 8>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, scores, ws);
-    return launch_status("sg_score");
+    if (nw <= 1) launch_passes<T, D, 1>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, thr_off, scores, ws);
+    else if (nw <= 2) launch_passes<T, D, 2>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, thr_off, scores, ws);
+    else if (nw <= 4) launch_passes<T, D, 4>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, thr_off, scores, ws);
+    else launch_passes<T, D, 8>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, c2, lse_in, thr_off, scores, ws);
+    return launch_status(name);
 }
 
 }  // namespace sg
@@ -521,33 +582,49 @@ extern "C" size_t sg_score_workspace_size(int B, int L, int Hq, int Hkv, int d, 
     return (size_t)((int64_t)L * Hkv * B * p.nchunk * R) * sizeof(float2);
 }
 
-extern "C" int sg_score(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
-                        const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *q_win, const void *k,
-                        int64_t k_layer_rows, const float *lse_in, float *scores, void *ws, size_t ws_bytes) {
-    SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "sg_score: unknown dtype %d", (int)dt);
+static int score_entry(const char *name, void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
+                       const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *q_win, const void *k,
+                       int64_t k_layer_rows, const float *lse_in, float thr_off, float *scores, void *ws,
+                       size_t ws_bytes) {
+    SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "%s: unknown dtype %d", name, (int)dt);
     SG_REQUIRE(B >= 1 && L >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0, SG_EINVAL,
-               "sg_score: need B, L, Hq, Hkv >= 1 and Hq %% Hkv == 0");
-    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "sg_score: head dimension %d not supported (64 or 128)", d);
-    SG_REQUIRE(W >= 1, SG_EINVAL, "sg_score: window must be >= 1");
-    SG_REQUIRE((int64_t)(Hq / Hkv) * W <= SC_MAXR, SG_EUNSUPPORTED, "sg_score: G*W = %d above %d",
-               (Hq / Hkv) * W, SC_MAXR);
-    SG_REQUIRE(T >= 0 && max_seqlen >= 0 && k_layer_rows >= 0, SG_EINVAL, "sg_score: negative size");
-    SG_REQUIRE(max_seqlen <= (1 << 30), SG_EINVAL, "sg_score: max_seqlen too large");
+               "%s: need B, L, Hq, Hkv >= 1 and Hq %% Hkv == 0", name);
+    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "%s: head dimension %d not supported (64 or 128)", name, d);
+    SG_REQUIRE(W >= 1, SG_EINVAL, "%s: window must be >= 1", name);
+    SG_REQUIRE((int64_t)(Hq / Hkv) * W <= SC_MAXR, SG_EUNSUPPORTED, "%s: G*W = %d above %d", name, (Hq / Hkv) * W,
+               SC_MAXR);
+    SG_REQUIRE(T >= 0 && max_seqlen >= 0 && k_layer_rows >= 0, SG_EINVAL, "%s: negative size", name);
+    SG_REQUIRE(max_seqlen <= (1 << 30), SG_EINVAL, "%s: max_seqlen too large", name);
     if (T == 0 || max_seqlen == 0) return SG_OK;
-    SG_REQUIRE(cu_seqlens && q_win && k && scores, SG_EINVAL, "sg_score: null pointer");
-    SG_REQUIRE(aligned16(q_win) && aligned16(k), SG_EINVAL, "sg_score: q_win and k must be 16-byte aligned");
+    SG_REQUIRE(cu_seqlens && q_win && k && scores, SG_EINVAL, "%s: null pointer", name);
+    SG_REQUIRE(aligned16(q_win) && aligned16(k), SG_EINVAL, "%s: q_win and k must be 16-byte aligned", name);
     const int64_t units = (int64_t)L * Hkv * B;
-    SG_REQUIRE(units * ceil_div(max_seqlen, 128) <= 0x7fffffff, SG_EINVAL, "sg_score: grid too large");
+    SG_REQUIRE(units * ceil_div(max_seqlen, 128) <= 0x7fffffff, SG_EINVAL, "%s: grid too large", name);
     if (!lse_in) {
         const size_t need = sg_score_workspace_size(B, L, Hq, Hkv, d, W, max_seqlen);
-        SG_REQUIRE(ws && ws_bytes >= need, SG_EWORKSPACE, "sg_score: workspace %zu < %zu", ws_bytes, need);
-        SG_REQUIRE(aligned16(ws), SG_EINVAL, "sg_score: workspace must be 16-byte aligned");
+        SG_REQUIRE(ws && ws_bytes >= need, SG_EWORKSPACE, "%s: workspace %zu < %zu", name, ws_bytes, need);
+        SG_REQUIRE(aligned16(ws), SG_EINVAL, "%s: workspace must be 16-byte aligned", name);
     }
     hipStream_t s = as_stream(stream);
     if (dt == SG_BF16) {
-        if (d == 128) return launch_score<uint16_t, 128>(s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, lse_in, scores, ws);
-        return launch_score<uint16_t, 64>(s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, lse_in, scores, ws);
+        if (d == 128) return launch_score<uint16_t, 128>(name, s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, lse_in, thr_off, scores, ws);
+        return launch_score<uint16_t, 64>(name, s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, lse_in, thr_off, scores, ws);
     }
-    if (d == 128) return launch_score<float, 128>(s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, lse_in, scores, ws);
-    return launch_score<float, 64>(s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, lse_in, scores, ws);
+    if (d == 128) return launch_score<float, 128>(name, s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, lse_in, thr_off, scores, ws);
+    return launch_score<float, 64>(name, s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, lse_in, thr_off, scores, ws);
+}
+
+extern "C" int sg_score(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
+                        const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *q_win, const void *k,
+                        int64_t k_layer_rows, const float *lse_in, float *scores, void *ws, size_t ws_bytes) {
+    return score_entry("sg_score", stream, dt, B, L, Hq, Hkv, d, W, cu_seqlens, T, max_seqlen, q_win, k,
+                       k_layer_rows, lse_in, -1.f, scores, ws, ws_bytes);
+}
+
+extern "C" int sg_score_count(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
+                              const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *q_win, const void *k,
+                              int64_t k_layer_rows, float alpha, float *counts, void *ws, size_t ws_bytes) {
+    SG_REQUIRE(alpha >= 0.f && alpha < INFINITY, SG_EINVAL, "sg_score_count: alpha must be finite and >= 0");
+    return score_entry("sg_score_count", stream, dt, B, L, Hq, Hkv, d, W, cu_seqlens, T, max_seqlen, q_win, k,
+                       k_layer_rows, nullptr, (float)((double)alpha * sqrt((double)d)), counts, ws, ws_bytes);
 }

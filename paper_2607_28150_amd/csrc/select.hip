@@ -1,0 +1,257 @@
+// sg_decode_select: decode-time dynamic KV selection (Section 2.3: each step
+// the selector picks KV entries from the decode query; Section 5.1: InfiniGen's
+// alpha = 5 and a maximum KV selection ratio of 20%).
+//
+// select_logits: z[u][g][j] = scale * q[b][l][g] . k_j for the G q heads of
+//   unit u = (b, l, h) and every key j < N_b.  One pass over the unit's keys:
+//   LPR lanes per key row, each holding VPL 16-byte slices of it (4 lanes per
+//   bf16 row of 128), all of a pass's rows loaded before any use (non-
+//   temporal), G dot products per row summed over the lane group by xor
+//   shuffles.  Bound by reading K.
+// select_thresh: one 1024-thread workgroup per unit holds its row (up to
+//   32 x 1024 keys) in registers: m_g = max_j z[g][j]; r_j = max_g (z[g][j] - m_g); the count of
+//   r_j >= -alpha; k = min(count, cap); the exact top-k of r (ties: lower j,
+//   select_common.h), ids ascending, the rest of the segment -1.
+#include "select_common.h"
+
+namespace sg {
+
+constexpr int SEL_THREADS = 256;
+constexpr int SEL_CHUNK = 2048;   // keys per workgroup of the logits pass
+constexpr int SEL_UNROLL = 4;     // key rows in flight per lane group
+constexpr int SEL_MAX_G = 8;
+
+template <typename T, int D>
+struct SelShape {
+    static constexpr int VPR = D * (int)sizeof(T) / 16;            // 16-byte slices per row
+    static constexpr int LPR = VPR / 4 >= 4 ? VPR / 4 : 4;          // lanes per row
+    static constexpr int VPL = VPR / LPR;                           // slices per lane
+    static constexpr int RPB = SEL_THREADS / LPR;                   // rows per workgroup step
+};
+
+struct SelUnit {
+    int b, l, h;
+    int64_t s0, N;
+};
+
+__device__ __forceinline__ SelUnit sel_unit(int64_t u, int B, int Hkv, const int32_t *cu_seqlens, int64_t T) {
+    SelUnit g;
+    g.b = (int)(u % B);
+    const int64_t lh = u / B;
+    g.l = (int)(lh / Hkv);
+    g.h = (int)(lh % Hkv);
+    const int64_t s0 = cu_seqlens[g.b], s1 = cu_seqlens[g.b + 1];
+    g.s0 = s0;
+    g.N = (s0 >= 0 && s1 >= s0 && s1 <= T) ? s1 - s0 : 0;   // bad metadata: an empty request
+    return g;
+}
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(SEL_THREADS) void select_logits_kernel(int B, int L, int Hq, int Hkv,
+                                                                      const int32_t *__restrict__ cu_seqlens,
+                                                                      int64_t T_, const T *__restrict__ q,
+                                                                      const T *__restrict__ k, int64_t k_layer_rows,
+                                                                      float scale, int nchunk, int ldz,
+                                                                      float *__restrict__ z) {
+    using S = SelShape<T, D>;
+    const int64_t u = blockIdx.x / nchunk;
+    const int chunk = blockIdx.x % nchunk;
+    const SelUnit g = sel_unit(u, B, Hkv, cu_seqlens, T_);
+    const int N = (int)min<int64_t>(g.N, ldz);
+    const int j0 = chunk * SEL_CHUNK;
+    if (j0 >= N) return;
+    const int j1 = min(N, j0 + SEL_CHUNK);
+    const int lv = threadIdx.x % S::LPR;
+    const int rsub = threadIdx.x / S::LPR;
+    const v4u *qb = reinterpret_cast<const v4u *>(q + (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * D);
+    v4u qs[G][S::VPL];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+        for (int v = 0; v < S::VPL; ++v) qs[hh][v] = qb[hh * S::VPR + lv + v * S::LPR];
+    const v4u *ku = reinterpret_cast<const v4u *>(k + ((int64_t)g.l * k_layer_rows + (int64_t)g.h * T_ + g.s0) * D);
+    float *zu = z + u * G * (int64_t)ldz;
+    for (int base = j0 + rsub; base < j1; base += S::RPB * SEL_UNROLL) {
+        v4u kr[SEL_UNROLL][S::VPL];
+#pragma unroll
+        for (int r = 0; r < SEL_UNROLL; ++r) {
+            const int j = min(base + r * S::RPB, j1 - 1);
+#pragma unroll
+            for (int v = 0; v < S::VPL; ++v)
+                kr[r][v] = __builtin_nontemporal_load(ku + (int64_t)j * S::VPR + lv + v * S::LPR);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int r = 0; r < SEL_UNROLL; ++r) {
+            float acc[G];
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) {
+                acc[hh] = 0.f;
+#pragma unroll
+                for (int v = 0; v < S::VPL; ++v) acc[hh] = SliceDot<T>::run(qs[hh][v], kr[r][v], acc[hh]);
+            }
+#pragma unroll
+            for (int o = 1; o < S::LPR; o <<= 1)
+#pragma unroll
+                for (int hh = 0; hh < G; ++hh) acc[hh] += __shfl_xor(acc[hh], o, 64);
+            const int j = base + r * S::RPB;
+            if (j < j1) {
+#pragma unroll
+                for (int hh = 0; hh < G; ++hh)
+                    if (hh % S::LPR == lv) zu[(int64_t)hh * ldz + j] = scale * acc[hh];
+            }
+        }
+    }
+}
+
+template <int ITEMS>
+__global__ __launch_bounds__(TOPK_THREADS) void select_thresh_kernel(int B, int L, int Hkv, int G,
+                                                                       const int32_t *__restrict__ cu_seqlens,
+                                                                       int64_t T_, int ldz,
+                                                                       const float *__restrict__ z, float alpha,
+                                                                       const int32_t *__restrict__ cu_cap,
+                                                                       int64_t K_cap, int32_t *__restrict__ idx,
+                                                                       int32_t *__restrict__ n_sel) {
+    __shared__ SelectSmem sm;
+    __shared__ float gmax[TOPK_WAVES][SEL_MAX_G];
+    const int64_t u = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+    const SelUnit g = sel_unit(u, B, Hkv, cu_seqlens, T_);
+    const int64_t lh = u / B;
+    int32_t *ns = n_sel + (int64_t)g.b * L * Hkv + lh;
+    const int64_t c0 = cu_cap[g.b], c1 = cu_cap[g.b + 1];
+    if (c0 < 0 || c1 < c0 || c1 > K_cap) {   // no writable segment
+        if (tid == 0) *ns = 0;
+        return;
+    }
+    int32_t *out = idx + lh * K_cap + c0;
+    const int64_t cap = c1 - c0;
+    const int N = (int)g.N;
+    if (cap == 0 || N == 0 || N > ldz || N > ITEMS * TOPK_THREADS) {
+        for (int64_t i = tid; i < cap; i += TOPK_THREADS) out[i] = -1;
+        if (tid == 0) *ns = 0;
+        return;
+    }
+    const float *zu = z + u * G * (int64_t)ldz;
+    const int first = tid * ITEMS;
+    const int nv = max(0, min(ITEMS, N - first));
+    // each head's maximum over the unit's keys
+    float mg[SEL_MAX_G];
+#pragma unroll
+    for (int hh = 0; hh < SEL_MAX_G; ++hh) {
+        if (hh < G) {
+            float m = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < ITEMS; ++i)
+                if (i < nv) m = fmaxf(m, zu[(int64_t)hh * ldz + first + i]);
+            m = wave_max(m);
+            if (lane == 0) gmax[wave][hh] = m;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int hh = 0; hh < SEL_MAX_G; ++hh) {
+        float m = -INFINITY;
+        if (hh < G)
+#pragma unroll
+            for (int w = 0; w < TOPK_WAVES; ++w) m = fmaxf(m, gmax[w][hh]);
+        mg[hh] = m;
+    }
+    // r_j = the best margin over the group's heads; the rule's count
+    uint32_t key[ITEMS];
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+        float r = -INFINITY;
+        if (i < nv) {
+#pragma unroll
+            for (int hh = 0; hh < SEL_MAX_G; ++hh)
+                if (hh < G) r = fmaxf(r, zu[(int64_t)hh * ldz + first + i] - mg[hh]);
+        }
+        key[i] = i < nv ? order_key(r) : 0u;
+        cnt += (i < nv && r >= -alpha) ? 1 : 0;
+    }
+    int total;
+    block_scan_incl(cnt, sm.wsum, total);
+    const int kk = (int)min<int64_t>(total, cap);
+    if (kk > 0) select_top<ITEMS>(key, nv, first, kk, out, sm);
+    for (int64_t i = kk + tid; i < cap; i += TOPK_THREADS) out[i] = -1;
+    if (tid == 0) *ns = kk;
+}
+
+template <typename E, int D, int G>
+static void launch_logits(hipStream_t s, int B, int L, int Hq, int Hkv, const int32_t *cu_seqlens, int64_t T,
+                          int max_seqlen, const void *q, const void *k, int64_t k_layer_rows, float *z) {
+    const int nchunk = (int)ceil_div(max_seqlen, SEL_CHUNK);
+    const int64_t grid = (int64_t)B * L * Hkv * nchunk;
+    select_logits_kernel<E, D, G><<<(unsigned)grid, SEL_THREADS, 0, s>>>(
+        B, L, Hq, Hkv, cu_seqlens, T, reinterpret_cast<const E *>(q), reinterpret_cast<const E *>(k), k_layer_rows,
+        1.0f / sqrtf((float)D), nchunk, max_seqlen, z);
+}
+
+template <typename E, int D>
+static void launch_logits_g(hipStream_t s, int G, int B, int L, int Hq, int Hkv, const int32_t *cu_seqlens,
+                            int64_t T, int max_seqlen, const void *q, const void *k, int64_t k_layer_rows, float *z) {
+    switch (G) {
+        case 1: launch_logits<E, D, 1>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z); break;
+        case 2: launch_logits<E, D, 2>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z); break;
+        case 4: launch_logits<E, D, 4>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z); break;
+        default: launch_logits<E, D, 8>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z); break;
+    }
+}
+
+}  // namespace sg
+
+using namespace sg;
+
+extern "C" size_t sg_decode_select_workspace_size(int B, int L, int Hq, int max_seqlen) {
+    if (B <= 0 || L <= 0 || Hq <= 0 || max_seqlen <= 0) return 0;
+    return (size_t)B * L * Hq * max_seqlen * sizeof(float);
+}
+
+extern "C" int sg_decode_select(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, const void *q,
+                                const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *k,
+                                int64_t k_layer_rows, float alpha, const int32_t *cu_cap, int64_t K_cap,
+                                int32_t *idx, int32_t *n_sel, void *ws, size_t ws_bytes) {
+    SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "sg_decode_select: unknown dtype %d", (int)dt);
+    SG_REQUIRE(B >= 1 && L >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0, SG_EINVAL,
+               "sg_decode_select: need B, L, Hq, Hkv >= 1 and Hq %% Hkv == 0");
+    const int G = Hq / Hkv;
+    SG_REQUIRE(G == 1 || G == 2 || G == 4 || G == 8, SG_EUNSUPPORTED, "sg_decode_select: group size %d (1, 2, 4, 8)",
+               G);
+    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "sg_decode_select: head dimension %d not supported", d);
+    SG_REQUIRE(alpha >= 0.f && alpha < INFINITY, SG_EINVAL, "sg_decode_select: alpha must be finite and >= 0");
+    SG_REQUIRE(T >= 0 && max_seqlen >= 0 && k_layer_rows >= 0 && K_cap >= 0, SG_EINVAL,
+               "sg_decode_select: negative size");
+    SG_REQUIRE(max_seqlen <= 32 * TOPK_THREADS, SG_EUNSUPPORTED, "sg_decode_select: max_seqlen %d above %d",
+               max_seqlen, 32 * TOPK_THREADS);
+    SG_REQUIRE(cu_seqlens && cu_cap && n_sel && (K_cap == 0 || idx), SG_EINVAL, "sg_decode_select: null pointer");
+    const int64_t units = (int64_t)B * L * Hkv;
+    SG_REQUIRE(units * std::max<int64_t>(1, ceil_div(max_seqlen, SEL_CHUNK)) <= 0x7fffffff, SG_EINVAL,
+               "sg_decode_select: grid too large");
+    const int ldz = std::max(max_seqlen, 1);
+    hipStream_t s = as_stream(stream);
+    if (max_seqlen > 0 && T > 0) {
+        SG_REQUIRE(q && k, SG_EINVAL, "sg_decode_select: null pointer");
+        SG_REQUIRE(aligned16(q) && aligned16(k), SG_EINVAL, "sg_decode_select: q and k must be 16-byte aligned");
+        const size_t need = sg_decode_select_workspace_size(B, L, Hq, max_seqlen);
+        SG_REQUIRE(ws && ws_bytes >= need, SG_EWORKSPACE, "sg_decode_select: workspace %zu < %zu", ws_bytes, need);
+        float *z = reinterpret_cast<float *>(ws);
+        if (dt == SG_BF16) {
+            if (d == 128) launch_logits_g<uint16_t, 128>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z);
+            else launch_logits_g<uint16_t, 64>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z);
+        } else {
+            if (d == 128) launch_logits_g<float, 128>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z);
+            else launch_logits_g<float, 64>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z);
+        }
+    }
+    const float *z = reinterpret_cast<const float *>(ws);
+    const unsigned grid = (unsigned)units;
+    if (max_seqlen <= 2 * TOPK_THREADS)
+        select_thresh_kernel<2><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, z, alpha, cu_cap, K_cap, idx, n_sel);
+    else if (max_seqlen <= 8 * TOPK_THREADS)
+        select_thresh_kernel<8><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, z, alpha, cu_cap, K_cap, idx, n_sel);
+    else
+        select_thresh_kernel<32><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, z, alpha, cu_cap, K_cap, idx, n_sel);
+    return launch_status("sg_decode_select");
+}

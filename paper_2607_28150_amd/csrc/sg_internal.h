@@ -48,6 +48,39 @@ __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// reinterpret a 32-bit word as two bf16 lanes (element 0 = low half); a copy
+// through a local word, not a bit_cast of a vector element
+__device__ __forceinline__ bf16x2 as_bf16x2(uint32_t w) {
+    bf16x2 r;
+    __builtin_memcpy(&r, &w, sizeof(r));
+    return r;
+}
+
+// acc + the dot product of one 16-byte slice of q with the same slice of a K
+// row (fp32 accumulation)
+template <typename T>
+struct SliceDot;
+template <>
+struct SliceDot<uint16_t> {   // bf16: four chained v_dot2_f32_bf16
+    __device__ static float run(const v4u &q, const v4u &k, float acc) {
+        acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.x), as_bf16x2(k.x), acc, false);
+        acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.y), as_bf16x2(k.y), acc, false);
+        acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.z), as_bf16x2(k.z), acc, false);
+        return __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.w), as_bf16x2(k.w), acc, false);
+    }
+};
+template <>
+struct SliceDot<float> {
+    __device__ static float run(const v4u &q, const v4u &k, float acc) {
+        acc = fmaf(__uint_as_float(q.x), __uint_as_float(k.x), acc);
+        acc = fmaf(__uint_as_float(q.y), __uint_as_float(k.y), acc);
+        acc = fmaf(__uint_as_float(q.z), __uint_as_float(k.z), acc);
+        return fmaf(__uint_as_float(q.w), __uint_as_float(k.w), acc);
+    }
+};
+
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));

@@ -28,7 +28,8 @@ EXPORTS = [
     "sg_fetch",
     "sg_decode_attn_workspace_size", "sg_decode_attn",
     "sg_block_importance", "sg_block_budget", "sg_pack_blocks_bytes", "sg_pack_blocks",
-    "sg_fetch_keep", "sg_spec_quota", "sg_spec_push",
+    "sg_fetch_keep", "sg_spec_quota", "sg_spec_push", "sg_score_count",
+    "sg_decode_select_workspace_size", "sg_decode_select",
 ]
 
 
@@ -74,11 +75,16 @@ def load() -> ctypes.CDLL:
     lib.sg_pack_blocks.argtypes = [_vp, _i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _i, _vp, _vp, _sz]
     lib.sg_fetch_keep.argtypes = [_vp, _i, _i, _i, _vp, _l, _vp, _vp, _vp, _l, _vp, _vp, _vp, _i, _i, _vp, _vp, _vp,
                                   _l, _vp, _vp, _vp, _l, _vp, _l, _vp, _vp]
+    lib.sg_score_count.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _l, _i, _vp, _vp, _l, _f, _vp, _vp, _sz]
+    lib.sg_decode_select_workspace_size.argtypes = [_i, _i, _i, _i]
+    lib.sg_decode_select_workspace_size.restype = _sz
+    lib.sg_decode_select.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _l, _i, _vp, _l, _f, _vp, _l, _vp, _vp,
+                                     _vp, _sz]
     lib.sg_spec_quota.argtypes = [_l, _i]
     lib.sg_spec_quota.restype = _l
     lib.sg_spec_push.argtypes = [_vp, _i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _vp, _vp, _l, _i, _vp, _vp, _vp]
     for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn", "sg_block_importance",
-              "sg_pack_blocks", "sg_fetch_keep", "sg_spec_push"):
+              "sg_pack_blocks", "sg_fetch_keep", "sg_spec_push", "sg_score_count", "sg_decode_select"):
         getattr(lib, f).restype = _i
     _lib = lib
     return lib
@@ -165,6 +171,48 @@ def sg_score(q_win, k, cu_seqlens, T, max_seqlen, Hkv, scores, ws=None, lse_in=N
                          _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size())
     _check("sg_score", rc)
     return scores
+
+
+def sg_score_count(q_win, k, cu_seqlens, T, max_seqlen, Hkv, counts, alpha, ws, k_layer_rows=None, stream=None):
+    """counts[L][Hkv][T] (float32 integers, written): how many (q head, window row)
+    pairs pick each key under the rule logit >= row max - alpha."""
+    B, L, Hq, W, d = q_win.shape
+    _need(k.dtype == q_win.dtype, "q_win and k must share a dtype")
+    _need(counts.dtype == torch.float32 and counts.numel() >= L * Hkv * T, "counts must be float32 [L][Hkv][T]")
+    _need(cu_seqlens.dtype == torch.int32 and cu_seqlens.numel() == B + 1, "cu_seqlens must be int32 [B+1]")
+    if k_layer_rows is None:
+        k_layer_rows = 0 if (k.dim() == 4 and k.shape[0] == 1 and L > 1) else Hkv * T
+    _need(k.numel() >= ((L - 1) * k_layer_rows + Hkv * T) * d, "k is smaller than its layout needs")
+    rc = load().sg_score_count(_stream(stream), _dtype_code(q_win), B, L, Hq, Hkv, d, W, _ptr(cu_seqlens), int(T),
+                               int(max_seqlen), _ptr(q_win), _ptr(k), int(k_layer_rows), float(alpha), _ptr(counts),
+                               _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size())
+    _check("sg_score_count", rc)
+    return counts
+
+
+def decode_select_workspace_size(B, L, Hq, max_seqlen) -> int:
+    return int(load().sg_decode_select_workspace_size(B, L, Hq, max_seqlen))
+
+
+def sg_decode_select(q, k, cu_seqlens, T, max_seqlen, Hkv, cu_cap, K_cap, idx, n_sel, alpha, ws,
+                     k_layer_rows=None, stream=None):
+    """Decode-time selection: idx [L][Hkv][K_cap] (ids ascending, then -1) and
+    n_sel [B][L][Hkv] from the step's queries q [B][L][Hq][d] and the keys."""
+    B, L, Hq, d = q.shape
+    _need(k.dtype == q.dtype, "q and k must share a dtype")
+    _need(cu_seqlens.dtype == torch.int32 and cu_seqlens.numel() == B + 1, "cu_seqlens must be int32 [B+1]")
+    _need(cu_cap.dtype == torch.int32 and cu_cap.numel() == B + 1, "cu_cap must be int32 [B+1]")
+    _need(idx.dtype == torch.int32 and idx.numel() >= L * Hkv * K_cap, "idx must be int32 [L][Hkv][K_cap]")
+    _need(n_sel.dtype == torch.int32 and n_sel.numel() >= B * L * Hkv, "n_sel must be int32 [B][L][Hkv]")
+    if k_layer_rows is None:
+        k_layer_rows = 0 if (k.dim() == 4 and k.shape[0] == 1 and L > 1) else Hkv * T
+    _need(k.numel() >= ((L - 1) * k_layer_rows + Hkv * T) * d, "k is smaller than its layout needs")
+    rc = load().sg_decode_select(_stream(stream), _dtype_code(q), B, L, Hq, Hkv, d, _ptr(q), _ptr(cu_seqlens), int(T),
+                                 int(max_seqlen), _ptr(k), int(k_layer_rows), float(alpha), _ptr(cu_cap),
+                                 int(K_cap), _ptr(idx), _ptr(n_sel), _ptr(ws),
+                                 0 if ws is None else ws.numel() * ws.element_size())
+    _check("sg_decode_select", rc)
+    return idx
 
 
 # ------------------------------------------------------------------------ topk

@@ -154,3 +154,19 @@ def test_spec_and_keep_host_checks(lib):
     rc = lib.sg_fetch_keep(None, 1, 128, 1, P, 5, P, None, P, 10, P, P, P, 1, 1, None, P, P, 10,
                            P, P, P, 10, None, 0, None, None)
     assert rc == smartgen.SG_EINVAL and "dst_start" in _err(lib)
+
+
+def test_selector_host_checks(lib):
+    rc = lib.sg_score_count(None, 1, 1, 1, 8, 8, 64, 32, P, 100, 100, P, P, 0, -1.0, P, P, 1 << 20)
+    assert rc == smartgen.SG_EINVAL and "alpha" in _err(lib)
+    rc = lib.sg_score_count(None, 1, 1, 1, 8, 8, 64, 32, P, 4096, 4096, P, P, 0, 5.0, P, P, 16)
+    assert rc == smartgen.SG_EWORKSPACE
+    assert smartgen.decode_select_workspace_size(1, 32, 32, 8192) == 32 * 32 * 8192 * 4
+    rc = lib.sg_decode_select(None, 1, 1, 1, 24, 8, 128, P, P, 100, 100, P, 0, 5.0, P, 10, P, P, P, 1 << 30)
+    assert rc == smartgen.SG_EUNSUPPORTED and "group" in _err(lib)          # G = 3
+    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 40000, 40000, P, 0, 5.0, P, 10, P, P, P, 1 << 30)
+    assert rc == smartgen.SG_EUNSUPPORTED                                   # rows above 32 x 1024
+    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 100, 100, P, 0, float("nan"), P, 10, P, P, P, 1 << 30)
+    assert rc == smartgen.SG_EINVAL
+    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 100, 100, P, 0, 5.0, P, 10, P, P, P, 64)
+    assert rc == smartgen.SG_EWORKSPACE

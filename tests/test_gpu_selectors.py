@@ -1,0 +1,174 @@
+"""GPU parity of the selector variants against the CPU oracle, through the C ABI:
+selection-frequency counts under the alpha rule (Section 4.1 importance with the
+Section 5.1 selector) and decode-time dynamic selection capped at a maximum
+ratio (Section 2.3, Section 5.1).
+
+Where fp32 and fp64 would decide a threshold differently, the inputs are
+integer-valued with d = 64 (scale 1/8) and alpha = 5.0625: every logit and
+margin is then exact on both sides and no logit can sit on the threshold, so
+the results must be identical.  With real-valued inputs the decisions within a
+rounding band of the threshold may go either way; all others must agree."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from datagen import configs, inputs
+from tests.gpu_util import cu, say
+
+pytestmark = pytest.mark.gpu
+
+ALPHA_EXACT = 5.0625          # alpha * sqrt(64) = 40.5: integer logits never tie the threshold
+
+
+def _ints(shape, lo, hi, seed, dtype):
+    x = np.random.default_rng(seed).integers(lo, hi + 1, shape).astype(np.float32)
+    return torch.from_numpy(x).to(torch.bfloat16 if dtype == "bf16" else torch.float32)
+
+
+def _count(gpu_lib, q, k, lens, Hkv, alpha):
+    B, L, Hq, W, d = q.shape
+    cus = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T = int(cus[-1])
+    ws = torch.empty(gpu_lib.score_workspace_size(B, L, Hq, Hkv, d, W, max(lens)), dtype=torch.uint8, device="cuda")
+    out = torch.full((L, Hkv, T), -1.0, device="cuda")
+    gpu_lib.sg_score_count(q.cuda(), k.cuda(), cu(cus), T, max(lens), Hkv, out, alpha, ws)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), cus
+
+
+@pytest.mark.parametrize("dtype,G,W,lens", [
+    ("f32", 4, 16, (2500, 700)),          # two chunks, a second request
+    ("bf16", 4, 64, (5000,)),
+    ("bf16", 8, 64, (64, 3000)),          # N = W
+    ("bf16", 1, 32, (4100,)),
+])
+def test_score_count_exact(gpu_lib, dtype, G, W, lens):
+    say("score count exact", dtype, G, W, lens)
+    L, Hkv, d = 2, 2, 64
+    T = sum(lens)
+    q = _ints((len(lens), L, Hkv * G, W, d), -3, 3, G + W, dtype)
+    k = _ints((L, Hkv, T, d), -3, 3, G * W + 1, dtype)
+    got, cus = _count(gpu_lib, q, k, lens, Hkv, ALPHA_EXACT)
+    ref = oracle.score_count(q.float().numpy(), k.float().numpy(), cus, Hkv, ALPHA_EXACT)
+    np.testing.assert_array_equal(got, ref.astype(np.float32))
+    assert got.min() >= 0 and got.max() <= G * W
+
+
+@pytest.mark.parametrize("G,W,lens", [(4, 64, (3000, 5000)), (8, 64, (2048,))])
+def test_score_count_band(gpu_lib, G, W, lens):
+    say("score count band", G, W, lens)
+    L, Hkv, d = 2, 2, 128
+    T = sum(lens)
+    g = np.random.default_rng(G * 100 + W)
+    q = torch.from_numpy(g.standard_normal((len(lens), L, Hkv * G, W, d), dtype=np.float32) * 1.5).to(torch.bfloat16)
+    k = torch.from_numpy(g.standard_normal((L, Hkv, T, d), dtype=np.float32)).to(torch.bfloat16)
+    got, cus = _count(gpu_lib, q, k, lens, Hkv, 5.0)
+    ref, near = oracle.score_count(q.float().numpy(), k.float().numpy(), cus, Hkv, 5.0, eps=1e-3)
+    diff = np.abs(got.astype(np.int64) - ref)
+    assert (diff <= near).all(), f"{int((diff > near).sum())} counts differ beyond the rounding band"
+    assert (got > 0).sum() > 0.05 * got.size             # the rule picks something
+
+
+def test_score_count_llama8b_8k_sampled(gpu_lib):
+    cfg = configs.get("llama8b_8k")
+    say("score count llama8b_8k")
+    pre = inputs.make_prefill(cfg, device="cuda")
+    N, T, L, Hkv, d = pre["seqlens"][0], pre["T"], cfg.L, cfg.Hkv, cfg.d
+    ws = torch.empty(gpu_lib.score_workspace_size(1, L, cfg.Hq, Hkv, d, cfg.W, N), dtype=torch.uint8, device="cuda")
+    out = torch.empty((L, Hkv, T), device="cuda")
+    gpu_lib.sg_score_count(pre["q_win"], pre["k"], cu(pre["cu_seqlens"]), T, N, Hkv, out, 5.0, ws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    for l, h in ((0, 0), (31, 7)):
+        q = pre["q_win"][:, l:l + 1, h * cfg.G:(h + 1) * cfg.G].float().cpu().numpy()
+        k = pre["k"][l:l + 1, h:h + 1].float().cpu().numpy()
+        ref, near = oracle.score_count(q, k, pre["cu_seqlens"], 1, 5.0, eps=1e-3)
+        diff = np.abs(got[l, h].astype(np.int64) - ref[0, 0])
+        assert (diff <= near[0, 0]).all()
+        heavy = pre["heavy"][(0, l, h)].cpu().numpy()
+        assert got[l, h, heavy].mean() > 2 * got[l, h].mean()     # the planted heavy hitters are picked often
+
+
+def _select(gpu_lib, q, k, lens, Hkv, caps, alpha):
+    B, L, Hq, d = q.shape
+    cus = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    cc = np.concatenate([[0], np.cumsum(caps)]).astype(np.int32)
+    T, Kc = int(cus[-1]), int(cc[-1])
+    ws = torch.empty(gpu_lib.decode_select_workspace_size(B, L, Hq, max(lens)), dtype=torch.uint8, device="cuda")
+    idx = torch.full((L, Hkv, Kc), -7, dtype=torch.int32, device="cuda")
+    n_sel = torch.full((B, L, Hkv), -7, dtype=torch.int32, device="cuda")
+    gpu_lib.sg_decode_select(q.cuda(), k.cuda(), cu(cus), T, max(lens), Hkv, cu(cc), Kc, idx, n_sel, alpha, ws)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), n_sel.cpu().numpy(), cus, cc
+
+
+@pytest.mark.parametrize("dtype,G,lens,cap_bp,alpha", [
+    ("bf16", 4, (3000, 1234), 2000, ALPHA_EXACT),     # the 20% cap
+    ("f32", 2, (5000,), 50, ALPHA_EXACT),             # the cap binds hard
+    ("bf16", 8, (700, 64, 2100), 10000, ALPHA_EXACT),
+    ("bf16", 1, (2049,), 2000, 0.0),                   # alpha 0: each head's maxima only
+])
+def test_decode_select_exact(gpu_lib, dtype, G, lens, cap_bp, alpha):
+    say("decode select exact", dtype, G, lens, cap_bp, alpha)
+    L, Hkv, d = 2, 2, 64
+    T = sum(lens)
+    q = _ints((len(lens), L, Hkv * G, d), -2, 2, G + T, dtype)
+    k = _ints((L, Hkv, T, d), -2, 2, G * T + 3, dtype)
+    caps = [max(1, n * cap_bp // 10000) for n in lens]
+    idx, n_sel, cus, cc = _select(gpu_lib, q, k, lens, Hkv, caps, alpha)
+    r_idx, r_n, _ = oracle.decode_select(q.float().numpy(), k.float().numpy(), cus, Hkv, cc, alpha)
+    np.testing.assert_array_equal(n_sel, r_n)
+    np.testing.assert_array_equal(idx, r_idx)
+
+
+def _check_band(idx, n_sel, r_idx, r_n, r, cus, cc, alpha, eps=1e-3):
+    B = len(cus) - 1
+    L, Hkv = idx.shape[0], idx.shape[1]
+    for b in range(B):
+        cap = cc[b + 1] - cc[b]
+        for l in range(L):
+            for h in range(Hkv):
+                rr = r[l, h, cus[b]:cus[b + 1]]
+                cnt_lo, cnt_hi = int((rr >= -alpha + eps).sum()), int((rr >= -alpha - eps).sum())
+                n = int(n_sel[b, l, h])
+                assert min(cnt_lo, cap) <= n <= min(cnt_hi, cap)
+                sel = idx[l, h, cc[b]:cc[b] + n]
+                assert (np.diff(sel) > 0).all() and (idx[l, h, cc[b] + n:cc[b + 1]] == -1).all()
+                order = np.sort(rr)[::-1]
+                edge = max(-alpha, order[n - 1]) if n > 0 else np.inf
+                inside = np.zeros(len(rr), bool)
+                inside[sel] = True
+                assert inside[rr > edge + eps].all(), "a clearly selected entry is missing"
+                assert not inside[rr < edge - eps].any(), "a clearly rejected entry is selected"
+
+
+@pytest.mark.parametrize("G,lens", [(4, (4000, 900)), (8, (2500,))])
+def test_decode_select_band(gpu_lib, G, lens):
+    say("decode select band", G, lens)
+    L, Hkv, d, alpha = 2, 2, 128, 5.0
+    T = sum(lens)
+    g = np.random.default_rng(G + T)
+    q = torch.from_numpy(g.standard_normal((len(lens), L, Hkv * G, d), dtype=np.float32) * 2).to(torch.bfloat16)
+    k = torch.from_numpy(g.standard_normal((L, Hkv, T, d), dtype=np.float32)).to(torch.bfloat16)
+    caps = [n // 5 for n in lens]
+    idx, n_sel, cus, cc = _select(gpu_lib, q, k, lens, Hkv, caps, alpha)
+    r_idx, r_n, r = oracle.decode_select(q.float().numpy(), k.float().numpy(), cus, Hkv, cc, alpha)
+    _check_band(idx, n_sel, r_idx, r_n, r, cus, cc, alpha)
+
+
+def test_decode_select_llama8b_32k_step(gpu_lib):
+    """One decode step of the 8B / 32K-token workload, all 32 layers; the oracle
+    checks two layers."""
+    cfg = configs.get("llama8b_32k")
+    say("decode select llama8b_32k")
+    pre = inputs.make_prefill(cfg, device="cuda", want_v=False)
+    N, T, L, Hkv = pre["seqlens"][0], pre["T"], cfg.L, cfg.Hkv
+    q = inputs.decode_queries(cfg, 0, device="cuda", mu=pre["mu"])          # [1][L][Hq][d]
+    cap = N * 2000 // 10000
+    idx, n_sel, cus, cc = _select(gpu_lib, q, pre["k"], [N], Hkv, [cap], 5.0)
+    for l in (0, 31):
+        r_idx, r_n, r = oracle.decode_select(q[:, l:l + 1].float().cpu().numpy(), pre["k"][l:l + 1].float().cpu().numpy(),
+                                             cus, Hkv, cc, 5.0)
+        _check_band(idx[l:l + 1], n_sel[:, l:l + 1], r_idx, r_n, r, cus, cc, 5.0)
+    assert (n_sel >= 1).all() and (n_sel <= cap).all()
