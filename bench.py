@@ -203,6 +203,9 @@ def main():
     # layer, transfer time 6.5x the prefill time), timed on its own
     blk = block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize)
 
+    # selector variants: alpha-rule counts, decode-time selection, on-demand ratio
+    sel_ops = selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx)
+
     # the decode side of the 32K-token workload: two lanes, reuse, speculative transfer
     dside = None if args.no_decode_side else decode_side(sg)
 
@@ -236,6 +239,7 @@ def main():
                          "note": "one pass: row normalisers supplied by the prefill attention"},
         "block_mode": blk,
         "decode_side": dside,
+        "selectors": sel_ops,
         "topk": {"ms": round(t_topk, 4),
                  "gbs": round((scores.numel() * 4 + idx.numel() * 4) / (t_topk * 1e-3) / 1e9, 1)},
         "pack": {"ms": round(t_pack, 4), "gbs": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9, 1),
@@ -518,6 +522,86 @@ def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
     del pre, src_k, src_v, store_k, store_v
     torch.cuda.synchronize()
     return res
+
+
+def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=5.0, cap_bp=2000, nrep=10):
+    """Selector variants on the request of the main step: the alpha-rule
+    selection-frequency score (Section 4.1 importance under the Section 5.1
+    selector) and decode-time dynamic selection (Section 2.3; alpha 5, at most
+    20% of the tokens), each timed on its own; then the on-demand ratio
+    (Section 3: entries the decode step selects that were not sent at prefill)
+    seen by that decode-time selector over `nsteps` steps, for four proactive
+    choices of the same budget: top-k of the window score, top-k of the
+    alpha-rule counts, the first tokens, and a random set."""
+    import numpy as np
+    import torch
+    from datagen import inputs
+
+    dev = "cuda"
+    L, Hq, Hkv, d, W = cfg.L, cfg.Hq, cfg.Hkv, cfg.d, cfg.W
+    esize = pre["k"].element_size()
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    units = L * Hkv
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record()
+        for _ in range(nrep):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / nrep
+
+    counts = torch.empty((L, Hkv, T), device=dev)
+    ws = torch.empty(sg.score_workspace_size(1, L, Hq, Hkv, d, W, N), dtype=torch.uint8, device=dev)
+    t_count = timed(lambda: sg.sg_score_count(pre["q_win"], pre["k"], cus, T, N, Hkv, counts, alpha, ws))
+    idx_count = torch.empty_like(idx_score)
+    sg.sg_topk(counts, cus, T, N, cuk, K_total, idx_count)
+    cap = N * cap_bp // 10000
+    cu_cap = torch.tensor([0, cap], dtype=torch.int32, device=dev)
+    ws_sel = torch.empty(sg.decode_select_workspace_size(1, L, Hq, N), dtype=torch.uint8, device=dev)
+    idx_dec = torch.empty((L, Hkv, cap), dtype=torch.int32, device=dev)
+    n_sel = torch.empty((1, L, Hkv), dtype=torch.int32, device=dev)
+    qs = [inputs.decode_queries(cfg, s, device=dev, mu=pre["mu"]) for s in range(nsteps)]     # [1][L][Hq][d]
+    t_sel = timed(lambda: sg.sg_decode_select(qs[0], pre["k"], cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha,
+                                              ws_sel))
+    score_flops = 2.0 * d * cfg.G * (W * N - W * (W - 1) / 2) * units
+    k_bytes = units * N * d * esize
+    # on-demand ratio by proactive choice
+    seq = torch.arange(K_total, device=dev, dtype=torch.int32).expand(L, Hkv, K_total).contiguous()
+    rnd = inputs.random_selection(cfg, [N], [K_total], device=dev, tag_extra=7)
+    row_off = (torch.arange(units + 1, device=dev) * cap).to(torch.int32)
+    mask_off = torch.arange(units, device=dev, dtype=torch.int64) * N
+    mask_len = torch.full((units,), N, dtype=torch.int32, device=dev)
+    loc = torch.empty(units * cap, dtype=torch.int32, device=dev)
+    rem = torch.empty_like(loc)
+    nl = torch.empty(units, dtype=torch.int32, device=dev)
+    nr = torch.empty_like(nl)
+    nk = torch.empty_like(nl)
+    ratios = {}
+    sel_frac = []
+    for name, sel in (("score", idx_score), ("count", idx_count), ("sequential", seq), ("random", rnd)):
+        mask = torch.full((units, N), 2, dtype=torch.int8, device=dev)
+        mask.scatter_(1, sel.view(units, K_total).long(), 1)
+        rs = []
+        for s in range(nsteps):
+            sg.sg_decode_select(qs[s], pre["k"], cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha, ws_sel)
+            sg.sg_split(row_off, idx_dec.view(-1), mask.view(-1), mask_off, mask_len, 0, loc, rem, nl, nr, n_kept=nk)
+            rs.append(nr.sum().item() / max(1, nk.sum().item()))
+            if name == "score":
+                sel_frac.append(n_sel.float().mean().item() / N)
+        ratios[name] = round(float(np.mean(rs)), 4)
+    return {"alpha": alpha, "count_score": {"ms": round(t_count, 4),
+                                            "tflops": round(score_flops / (t_count * 1e-3) / 1e12, 2),
+                                            "frac_mfma_peak": round(score_flops / (t_count * 1e-3) / 1e12
+                                                                    / BF16_MFMA_PEAK_TFLOPS, 4)},
+            "decode_select": {"ms": round(t_sel, 4), "cap": cap,
+                              "k_read_gbs": round(k_bytes / (t_sel * 1e-3) / 1e9, 1),
+                              "frac_hbm_peak": round(k_bytes / (t_sel * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                              "selected_fraction": round(float(np.mean(sel_frac)), 4)},
+            "on_demand_ratio_by_proactive_choice": ratios, "budget_k": K_total, "steps": nsteps}
 
 
 def window_lse(q_win, k, N, Hkv, W, d):
