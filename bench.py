@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--decode-steps", type=int, default=None, help="decode steps per step (default: workload's)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode-side", action="store_true", help="skip the 32K-token decode-side section")
+    p.add_argument("--only", choices=["decode_side"], default=None,
+                   help="run one section on its own and print its JSON line (profiling one workload)")
     p.add_argument("--cpu-layers", type=int, default=0, help="layers the oracle is timed on (0 = all)")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="repeat the oracle sample to at least this long")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -88,6 +90,9 @@ def main():
         hip_build.build()
     sg.load()
     assert torch.cuda.is_available(), "bench needs a GPU"
+    if args.only == "decode_side":
+        print(json.dumps({"section": "decode_side", "n_gpus": 1, "decode_side": decode_side(sg)}), flush=True)
+        return
     dev = "cuda"
     cfg = get(args.workload)
     assert cfg.B == 1 and cfg.extra_bp == 0, "the bench step covers single-request workloads without extras"
