@@ -5,9 +5,10 @@
 // select_logits: z[u][g][j] = scale * q[b][l][g] . k_j for the G q heads of
 //   unit u = (b, l, h) and every key j < N_b.  One pass over the unit's keys:
 //   LPR lanes per key row, each holding VPL 16-byte slices of it (4 lanes per
-//   bf16 row of 128), all of a pass's rows loaded before any use (non-
-//   temporal), G dot products per row summed over the lane group by xor
-//   shuffles.  Bound by reading K.
+//   bf16 row of 128), all of a pass's rows loaded before any use, G dot
+//   products per row summed over the lane group by xor shuffles; a wavefront
+//   owns consecutive rows and writes each head's logits of them as whole
+//   256-byte pieces.  Bound by reading K.
 // select_thresh: one 1024-thread workgroup per unit holds its row (up to
 //   32 x 1024 keys) in registers: m_g = max_j z[g][j]; r_j = max_g (z[g][j] - m_g); the count of
 //   r_j >= -alpha; k = min(count, cap); the exact top-k of r (ties: lower j,
@@ -17,7 +18,7 @@
 namespace sg {
 
 constexpr int SEL_THREADS = 256;
-constexpr int SEL_CHUNK = 2048;   // keys per workgroup of the logits pass
+constexpr int SEL_CHUNK = 512;    // keys per workgroup of the logits pass (many rounds of workgroups)
 constexpr int SEL_UNROLL = 4;     // key rows in flight per lane group
 constexpr int SEL_MAX_G = 8;
 
@@ -52,8 +53,10 @@ __global__ __launch_bounds__(SEL_THREADS) void select_logits_kernel(int B, int L
                                                                       int64_t T_, const T *__restrict__ q,
                                                                       const T *__restrict__ k, int64_t k_layer_rows,
                                                                       float scale, int nchunk, int ldz,
-                                                                      float *__restrict__ z) {
+                                                                      float *__restrict__ z,
+                                                                      float *__restrict__ zmax) {
     using S = SelShape<T, D>;
+    __shared__ float wmax[SEL_THREADS / 64][G];
     const int64_t u = blockIdx.x / nchunk;
     const int chunk = blockIdx.x % nchunk;
     const SelUnit g = sel_unit(u, B, Hkv, cu_seqlens, T_);
@@ -61,8 +64,14 @@ __global__ __launch_bounds__(SEL_THREADS) void select_logits_kernel(int B, int L
     const int j0 = chunk * SEL_CHUNK;
     if (j0 >= N) return;
     const int j1 = min(N, j0 + SEL_CHUNK);
+    // a wavefront owns GPW * SEL_UNROLL consecutive rows of every step: lane
+    // group grp (LPR lanes) takes rows grp, grp + GPW, ...
+    constexpr int GPW = 64 / S::LPR;
+    constexpr int WROWS = GPW * SEL_UNROLL;
     const int lv = threadIdx.x % S::LPR;
-    const int rsub = threadIdx.x / S::LPR;
+    const int lane = threadIdx.x % 64;
+    const int grp = lane / S::LPR;
+    const int wave = threadIdx.x / 64;
     const v4u *qb = reinterpret_cast<const v4u *>(q + (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * D);
     v4u qs[G][S::VPL];
 #pragma unroll
@@ -71,16 +80,19 @@ __global__ __launch_bounds__(SEL_THREADS) void select_logits_kernel(int B, int L
         for (int v = 0; v < S::VPL; ++v) qs[hh][v] = qb[hh * S::VPR + lv + v * S::LPR];
     const v4u *ku = reinterpret_cast<const v4u *>(k + ((int64_t)g.l * k_layer_rows + (int64_t)g.h * T_ + g.s0) * D);
     float *zu = z + u * G * (int64_t)ldz;
-    for (int base = j0 + rsub; base < j1; base += S::RPB * SEL_UNROLL) {
+    float mx[G];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) mx[hh] = -INFINITY;
+    for (int w0 = j0 + wave * WROWS; w0 < j1; w0 += (SEL_THREADS / 64) * WROWS) {   // uniform per wavefront
         v4u kr[SEL_UNROLL][S::VPL];
 #pragma unroll
         for (int r = 0; r < SEL_UNROLL; ++r) {
-            const int j = min(base + r * S::RPB, j1 - 1);
+            const int j = min(w0 + r * GPW + grp, j1 - 1);
 #pragma unroll
-            for (int v = 0; v < S::VPL; ++v)
-                kr[r][v] = __builtin_nontemporal_load(ku + (int64_t)j * S::VPR + lv + v * S::LPR);
+            for (int v = 0; v < S::VPL; ++v) kr[r][v] = ku[(int64_t)j * S::VPR + lv + v * S::LPR];
         }
         __builtin_amdgcn_sched_barrier(0);
+        float zs[SEL_UNROLL][G];
 #pragma unroll
         for (int r = 0; r < SEL_UNROLL; ++r) {
             float acc[G];
@@ -94,26 +106,53 @@ __global__ __launch_bounds__(SEL_THREADS) void select_logits_kernel(int B, int L
             for (int o = 1; o < S::LPR; o <<= 1)
 #pragma unroll
                 for (int hh = 0; hh < G; ++hh) acc[hh] += __shfl_xor(acc[hh], o, 64);
-            const int j = base + r * S::RPB;
-            if (j < j1) {
+            const bool live = w0 + r * GPW + grp < j1;
 #pragma unroll
-                for (int hh = 0; hh < G; ++hh)
-                    if (hh % S::LPR == lv) zu[(int64_t)hh * ldz + j] = scale * acc[hh];
+            for (int hh = 0; hh < G; ++hh) {
+                zs[r][hh] = scale * acc[hh];
+                if (live) mx[hh] = fmaxf(mx[hh], zs[r][hh]);
             }
         }
+        // lane L stores row w0 + L of every head (whole 256-byte pieces): that
+        // value sits in lane group L % GPW, unroll slot L / GPW
+        const int jw = w0 + lane;
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            float v = 0.f;
+#pragma unroll
+            for (int r = 0; r < SEL_UNROLL; ++r) {
+                const float t = __shfl(zs[r][hh], (lane % GPW) * S::LPR, 64);
+                v = lane / GPW == r ? t : v;
+            }
+            if (lane < WROWS && jw < j1) zu[(int64_t)hh * ldz + jw] = v;
+        }
+    }
+    // the chunk's maximum of every head (exact: a maximum of the stored values)
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) {
+        const float m = wave_max(mx[hh]);
+        if (threadIdx.x % 64 == 0) wmax[wave][hh] = m;
+    }
+    __syncthreads();
+    if (threadIdx.x < G) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < SEL_THREADS / 64; ++w) m = fmaxf(m, wmax[w][threadIdx.x]);
+        zmax[(u * nchunk + chunk) * G + threadIdx.x] = m;
     }
 }
 
 template <int ITEMS>
 __global__ __launch_bounds__(TOPK_THREADS) void select_thresh_kernel(int B, int L, int Hkv, int G,
                                                                        const int32_t *__restrict__ cu_seqlens,
-                                                                       int64_t T_, int ldz,
-                                                                       const float *__restrict__ z, float alpha,
+                                                                       int64_t T_, int ldz, int nchunk,
+                                                                       const float *__restrict__ z,
+                                                                       const float *__restrict__ zmax, float alpha,
                                                                        const int32_t *__restrict__ cu_cap,
                                                                        int64_t K_cap, int32_t *__restrict__ idx,
                                                                        int32_t *__restrict__ n_sel) {
     __shared__ SelectSmem sm;
-    __shared__ float gmax[TOPK_WAVES][SEL_MAX_G];
+    __shared__ float gmax[1][SEL_MAX_G];
     const int64_t u = blockIdx.x;
     const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
     const SelUnit g = sel_unit(u, B, Hkv, cu_seqlens, T_);
@@ -135,28 +174,20 @@ __global__ __launch_bounds__(TOPK_THREADS) void select_thresh_kernel(int B, int 
     const float *zu = z + u * G * (int64_t)ldz;
     const int first = tid * ITEMS;
     const int nv = max(0, min(ITEMS, N - first));
-    // each head's maximum over the unit's keys
-    float mg[SEL_MAX_G];
-#pragma unroll
-    for (int hh = 0; hh < SEL_MAX_G; ++hh) {
-        if (hh < G) {
+    // each head's maximum over the unit's keys, from the logits pass's chunk maxima
+    const int nc = (int)ceil_div(N, SEL_CHUNK);
+    if (wave == 0) {
+        for (int hh = 0; hh < G; ++hh) {
             float m = -INFINITY;
-#pragma unroll
-            for (int i = 0; i < ITEMS; ++i)
-                if (i < nv) m = fmaxf(m, zu[(int64_t)hh * ldz + first + i]);
+            for (int c = lane; c < nc; c += 64) m = fmaxf(m, zmax[(u * nchunk + c) * G + hh]);
             m = wave_max(m);
-            if (lane == 0) gmax[wave][hh] = m;
+            if (lane == 0) gmax[0][hh] = m;
         }
     }
     __syncthreads();
+    float mg[SEL_MAX_G];
 #pragma unroll
-    for (int hh = 0; hh < SEL_MAX_G; ++hh) {
-        float m = -INFINITY;
-        if (hh < G)
-#pragma unroll
-            for (int w = 0; w < TOPK_WAVES; ++w) m = fmaxf(m, gmax[w][hh]);
-        mg[hh] = m;
-    }
+    for (int hh = 0; hh < SEL_MAX_G; ++hh) mg[hh] = hh < G ? gmax[0][hh] : -INFINITY;
     // r_j = the best margin over the group's heads; the rule's count
     uint32_t key[ITEMS];
     int cnt = 0;
@@ -181,22 +212,23 @@ __global__ __launch_bounds__(TOPK_THREADS) void select_thresh_kernel(int B, int 
 
 template <typename E, int D, int G>
 static void launch_logits(hipStream_t s, int B, int L, int Hq, int Hkv, const int32_t *cu_seqlens, int64_t T,
-                          int max_seqlen, const void *q, const void *k, int64_t k_layer_rows, float *z) {
+                          int max_seqlen, const void *q, const void *k, int64_t k_layer_rows, float *z, float *zmax) {
     const int nchunk = (int)ceil_div(max_seqlen, SEL_CHUNK);
     const int64_t grid = (int64_t)B * L * Hkv * nchunk;
     select_logits_kernel<E, D, G><<<(unsigned)grid, SEL_THREADS, 0, s>>>(
         B, L, Hq, Hkv, cu_seqlens, T, reinterpret_cast<const E *>(q), reinterpret_cast<const E *>(k), k_layer_rows,
-        1.0f / sqrtf((float)D), nchunk, max_seqlen, z);
+        1.0f / sqrtf((float)D), nchunk, max_seqlen, z, zmax);
 }
 
 template <typename E, int D>
 static void launch_logits_g(hipStream_t s, int G, int B, int L, int Hq, int Hkv, const int32_t *cu_seqlens,
-                            int64_t T, int max_seqlen, const void *q, const void *k, int64_t k_layer_rows, float *z) {
+                            int64_t T, int max_seqlen, const void *q, const void *k, int64_t k_layer_rows, float *z,
+                            float *zmax) {
     switch (G) {
-        case 1: launch_logits<E, D, 1>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z); break;
-        case 2: launch_logits<E, D, 2>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z); break;
-        case 4: launch_logits<E, D, 4>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z); break;
-        default: launch_logits<E, D, 8>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z); break;
+        case 1: launch_logits<E, D, 1>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zmax); break;
+        case 2: launch_logits<E, D, 2>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zmax); break;
+        case 4: launch_logits<E, D, 4>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zmax); break;
+        default: launch_logits<E, D, 8>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zmax); break;
     }
 }
 
@@ -204,9 +236,11 @@ static void launch_logits_g(hipStream_t s, int G, int B, int L, int Hq, int Hkv,
 
 using namespace sg;
 
+// Workspace: the logits z [units][G][max_seqlen], then the chunk maxima
+// [units][nchunk][G] (units * G = B * L * Hq).
 extern "C" size_t sg_decode_select_workspace_size(int B, int L, int Hq, int max_seqlen) {
     if (B <= 0 || L <= 0 || Hq <= 0 || max_seqlen <= 0) return 0;
-    return (size_t)B * L * Hq * max_seqlen * sizeof(float);
+    return (size_t)B * L * Hq * ((size_t)max_seqlen + ceil_div(max_seqlen, SEL_CHUNK)) * sizeof(float);
 }
 
 extern "C" int sg_decode_select(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, const void *q,
@@ -237,21 +271,24 @@ extern "C" int sg_decode_select(void *stream, sg_dtype dt, int B, int L, int Hq,
         const size_t need = sg_decode_select_workspace_size(B, L, Hq, max_seqlen);
         SG_REQUIRE(ws && ws_bytes >= need, SG_EWORKSPACE, "sg_decode_select: workspace %zu < %zu", ws_bytes, need);
         float *z = reinterpret_cast<float *>(ws);
+        float *zm = z + (int64_t)B * L * Hq * max_seqlen;
         if (dt == SG_BF16) {
-            if (d == 128) launch_logits_g<uint16_t, 128>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z);
-            else launch_logits_g<uint16_t, 64>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z);
+            if (d == 128) launch_logits_g<uint16_t, 128>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zm);
+            else launch_logits_g<uint16_t, 64>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zm);
         } else {
-            if (d == 128) launch_logits_g<float, 128>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z);
-            else launch_logits_g<float, 64>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z);
+            if (d == 128) launch_logits_g<float, 128>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zm);
+            else launch_logits_g<float, 64>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zm);
         }
     }
     const float *z = reinterpret_cast<const float *>(ws);
+    const float *zm = z + (int64_t)B * L * Hq * std::max(max_seqlen, 0);
+    const int nchunk = (int)std::max<int64_t>(1, ceil_div(max_seqlen, SEL_CHUNK));
     const unsigned grid = (unsigned)units;
     if (max_seqlen <= 2 * TOPK_THREADS)
-        select_thresh_kernel<2><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, z, alpha, cu_cap, K_cap, idx, n_sel);
+        select_thresh_kernel<2><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, nchunk, z, zm, alpha, cu_cap, K_cap, idx, n_sel);
     else if (max_seqlen <= 8 * TOPK_THREADS)
-        select_thresh_kernel<8><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, z, alpha, cu_cap, K_cap, idx, n_sel);
+        select_thresh_kernel<8><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, nchunk, z, zm, alpha, cu_cap, K_cap, idx, n_sel);
     else
-        select_thresh_kernel<32><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, z, alpha, cu_cap, K_cap, idx, n_sel);
+        select_thresh_kernel<32><<<grid, TOPK_THREADS, 0, s>>>(B, L, Hkv, G, cu_seqlens, T, ldz, nchunk, z, zm, alpha, cu_cap, K_cap, idx, n_sel);
     return launch_status("sg_decode_select");
 }
