@@ -52,7 +52,7 @@ def _load():
     lib.sgo_score_count.argtypes = [_i, _i, _i, _i, _i, _i, _i32p, _l, _f32p, _f32p, _l, ctypes.c_double,
                                     ctypes.c_double, _i32p, _i32p]
     lib.sgo_decode_select.argtypes = [_i, _i, _i, _i, _i, _f32p, _i32p, _l, _f32p, _l, _i32p, _l, ctypes.c_double,
-                                      _i32p, _i32p, _f64p]
+                                      ctypes.c_double, _i32p, _i32p, _f64p]
     for f in ("sgo_score", "sgo_topk", "sgo_pack", "sgo_split", "sgo_fetch", "sgo_decode_attn", "sgo_threads",
               "sgo_block_importance", "sgo_pack_blocks", "sgo_spec_push", "sgo_fetch_keep", "sgo_score_count",
               "sgo_decode_select"):
@@ -335,9 +335,10 @@ def score_count(q_win, k, cu_seqlens, Hkv, alpha, k_layer_rows=None, eps=None):
     return out if eps is None else (out, near)
 
 
-def decode_select(q, k, cu_seqlens, Hkv, cu_cap, alpha, k_layer_rows=None):
+def decode_select(q, k, cu_seqlens, Hkv, cu_cap, alpha, k_layer_rows=None, scale=None):
     """Decode-time selection: (idx [L][Hkv][K_cap] int32, n_sel [B][L][Hkv] int32,
-    r [L][Hkv][T] float64).  q [B][L][Hq][d]; k [Lkv][Hkv][T][d]."""
+    r [L][Hkv][T] float64).  q [B][L][Hq][d]; k [Lkv][Hkv][T][d]; scale defaults
+    to 1/sqrt(d) (pass the full head's for partial channels)."""
     qq = _c(q, np.float32)
     kk = _c(k, np.float32)
     B, L, Hq, d = qq.shape
@@ -351,7 +352,8 @@ def decode_select(q, k, cu_seqlens, Hkv, cu_cap, alpha, k_layer_rows=None):
     n_sel = np.zeros((B, L, Hkv), dtype=np.int32)
     r = np.full((L, Hkv, max(T, 1)), np.nan)
     rc = _load().sgo_decode_select(B, L, Hq, Hkv, d, _p(qq, _f32p), _p(cu, _i32p), T, _p(kk, _f32p),
-                                   int(k_layer_rows), _p(cc, _i32p), K_cap, float(alpha), _p(idx, _i32p),
+                                   int(k_layer_rows), _p(cc, _i32p), K_cap, float(alpha),
+                                   float(d ** -0.5 if scale is None else scale), _p(idx, _i32p),
                                    _p(n_sel, _i32p), _p(r, _f64p))
     _check(rc, "decode_select")
     return idx[:, :, :K_cap], n_sel, r[:, :, :T]

@@ -603,7 +603,10 @@ int sgo_score_count(int B, int L, int Hq, int Hkv, int d, int W,
  * the largest r_j are kept (ties: lower j).  The kept ids go ascending to
  * idx[l][h][cu_cap[b] ...], n_sel[(b*L + l)*Hkv + h] counts them, and the rest
  * of the segment is -1.  r_out ([L][Hkv][T], optional) receives r.
- * q: [B][L][Hq][d]; K: [Lkv][Hkv][T][d] with the given layer stride.
+ * q: [B][L][Hq][d]; K: [Lkv][Hkv][T][d] with the given layer stride.  The
+ * logit scale is an argument: 1/sqrt(d) for whole rows; for a partial set of
+ * channels (InfiniGen speculates with 30% of them, Section 5.1) the rows hold
+ * only those channels and the scale stays that of the full head.
  */
 typedef struct { double r; int32_t j; } sgo_rj;
 
@@ -621,12 +624,12 @@ static int sgo_i32_cmp(const void *pa, const void *pb) {
 
 int sgo_decode_select(int B, int L, int Hq, int Hkv, int d, const float *q,
                       const int32_t *cu_seqlens, int64_t T, const float *k, int64_t k_layer_rows,
-                      const int32_t *cu_cap, int64_t K_cap, double alpha,
+                      const int32_t *cu_cap, int64_t K_cap, double alpha, double scale,
                       int32_t *idx, int32_t *n_sel, double *r_out)
 {
-    if (B <= 0 || L <= 0 || Hkv <= 0 || Hq % Hkv != 0 || d <= 0 || !(alpha >= 0.0)) return SGO_EINVAL;
+    if (B <= 0 || L <= 0 || Hkv <= 0 || Hq % Hkv != 0 || d <= 0 || !(alpha >= 0.0) || !(scale > 0.0))
+        return SGO_EINVAL;
     const int G = Hq / Hkv;
-    const double scale = 1.0 / sqrt((double)d);
     const int nunits = L * Hkv * B;
 #pragma omp parallel for schedule(dynamic, 1)
     for (int u = 0; u < nunits; ++u) {

@@ -825,3 +825,19 @@ def test_decode_select_brute_force(alpha, cap_frac):
                 assert (seg[len(cand):] == -1).all()
                 # each head's maximum passes the rule (r = 0), so at least one entry is picked
                 assert n_sel[b, l, h] >= 1
+
+
+def test_decode_select_partial_channels_is_a_scaled_subset():
+    """Selection on a subset of channels with the full head's scale equals the
+    selection of a query zeroed outside the subset (scale 1/sqrt(d_full))."""
+    B, L, Hq, Hkv, d, ds = 1, 1, 4, 1, 16, 6
+    N = 40
+    q = _rand((B, L, Hq, d), 27, scale=3.0)
+    k = _rand((L, Hkv, N, d), 28)
+    qz = q.copy()
+    qz[..., ds:] = 0.0
+    full = oracle.decode_select(qz, k, [0, N], Hkv, [0, 9], 2.0)
+    part = oracle.decode_select(q[..., :ds].copy(), k[..., :ds].copy(), [0, N], Hkv, [0, 9], 2.0, scale=d ** -0.5)
+    np.testing.assert_array_equal(part[0], full[0])
+    np.testing.assert_array_equal(part[1], full[1])
+    np.testing.assert_allclose(part[2], full[2], rtol=0, atol=1e-12)
