@@ -572,6 +572,15 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     qs = [inputs.decode_queries(cfg, s, device=dev, mu=pre["mu"]) for s in range(nsteps)]     # [1][L][Hq][d]
     t_sel = timed(lambda: sg.sg_decode_select(qs[0], pre["k"], cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha,
                                               ws_sel))
+    # InfiniGen's partial ratio 0.3: 40 of the 128 channels (here the first 40;
+    # the paper's selector picks them with skewing matrices from the weights),
+    # kept as a contiguous partial-key cache, with the full head's scale
+    dp = 40
+    k_part = pre["k"][..., :dp].contiguous()
+    qp = [x[..., :dp].contiguous() for x in qs]
+    t_sel_p = timed(lambda: sg.sg_decode_select(qp[0], k_part, cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha,
+                                                ws_sel, scale=d ** -0.5))
+    kp_bytes = units * N * dp * esize
     score_flops = 2.0 * d * cfg.G * (W * N - W * (W - 1) / 2) * units
     k_bytes = units * N * d * esize
     # on-demand ratio by proactive choice
@@ -587,12 +596,17 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     nk = torch.empty_like(nl)
     ratios = {}
     sel_frac = []
-    for name, sel in (("score", idx_score), ("count", idx_count), ("sequential", seq), ("random", rnd)):
+    for name, sel, partial in (("score", idx_score, False), ("count", idx_count, False),
+                               ("sequential", seq, False), ("random", rnd, False), ("score_partial_selector", idx_score, True)):
         mask = torch.full((units, N), 2, dtype=torch.int8, device=dev)
         mask.scatter_(1, sel.view(units, K_total).long(), 1)
         rs = []
         for s in range(nsteps):
-            sg.sg_decode_select(qs[s], pre["k"], cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha, ws_sel)
+            if partial:
+                sg.sg_decode_select(qp[s], k_part, cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha, ws_sel,
+                                    scale=d ** -0.5)
+            else:
+                sg.sg_decode_select(qs[s], pre["k"], cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha, ws_sel)
             sg.sg_split(row_off, idx_dec.view(-1), mask.view(-1), mask_off, mask_len, 0, loc, rem, nl, nr, n_kept=nk)
             rs.append(nr.sum().item() / max(1, nk.sum().item()))
             if name == "score":
@@ -606,6 +620,10 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
                               "k_read_gbs": round(k_bytes / (t_sel * 1e-3) / 1e9, 1),
                               "frac_hbm_peak": round(k_bytes / (t_sel * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                               "selected_fraction": round(float(np.mean(sel_frac)), 4)},
+            "decode_select_partial_40_of_128": {"ms": round(t_sel_p, 4),
+                                                "k_read_gbs": round(kp_bytes / (t_sel_p * 1e-3) / 1e9, 1),
+                                                "frac_hbm_peak": round(kp_bytes / (t_sel_p * 1e-3) / 1e9
+                                                                       / HBM_PEAK_GBS, 4)},
             "on_demand_ratio_by_proactive_choice": ratios, "budget_k": K_total, "steps": nsteps}
 
 

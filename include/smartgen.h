@@ -333,11 +333,12 @@ int sg_pack_blocks(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, 
 
 /* ---------------------------------------------------------------- sg_decode_select
  * Decode-time dynamic KV selection (Section 2.3: each decode step's selector
- * picks KV entries from the step's query; Section 5.1: InfiniGen's alpha = 5
- * and a maximum KV selection ratio of 20%).  For request b, layer l and KV
- * head h, with the G q heads of its group and the request's N = N_b keys:
+ * picks KV entries from the step's query; Section 5.1: InfiniGen's alpha = 5,
+ * partial ratio 0.3 and a maximum KV selection ratio of 20%).  For request b,
+ * layer l and KV head h, with the G q heads of its group and the request's
+ * N = N_b keys:
  *
- *   z[g][j] = q[b][l][g] . K[l][h][j] / sqrt(d),   m_g = max_j z[g][j]
+ *   z[g][j] = scale * q[b][l][g] . K[l][h][j],     m_g = max_j z[g][j]
  *   r_j     = max over g of (z[g][j] - m_g)        (<= 0; 0 at each maximum)
  *   S       = { j : r_j >= -alpha }                (some head of the group picks j)
  *
@@ -347,6 +348,10 @@ int sg_pack_blocks(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, 
  * segment is -1 (which sg_split drops as a pad).  r and the rule are computed
  * in fp32.
  *
+ *   d       row width: the whole head (64, 128) or a partial set of its
+ *           channels (32, 40, 48; InfiniGen speculates with 30% of them); q and
+ *           k hold the same d channels.
+ *   scale   logit scale, 1/sqrt(full head dimension); 0 means 1/sqrt(d).
  *   q       device, dtype, [B][L][Hq][d] (the step's queries).
  *   k       device, dtype, rows of d; unit (b, l, h) token j is row
  *           l * k_layer_rows + h * T + cu_seqlens[b] + j.
@@ -354,13 +359,14 @@ int sg_pack_blocks(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, 
  *   n_sel   device int32 [B][L][Hkv] (output).
  *   ws      device workspace of sg_decode_select_workspace_size(...) bytes
  *           (the logits of every q head).
- * Requirements: G in {1, 2, 4, 8}, max_seqlen <= 32768, alpha finite and >= 0.
+ * Requirements: G in {1, 2, 4, 8}, max_seqlen <= 32768, alpha and scale
+ * finite and >= 0.
  */
 size_t sg_decode_select_workspace_size(int B, int L, int Hq, int max_seqlen);
 int sg_decode_select(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, const void *q,
                      const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *k, int64_t k_layer_rows,
-                     float alpha, const int32_t *cu_cap, int64_t K_cap, int32_t *idx, int32_t *n_sel,
-                     void *ws, size_t ws_bytes);
+                     float scale, float alpha, const int32_t *cu_cap, int64_t K_cap, int32_t *idx,
+                     int32_t *n_sel, void *ws, size_t ws_bytes);
 
 /* ---------------------------------------------------------------- speculative transfer
  * Speculative transfer (Section 4.3): while the decode side computes

@@ -1,6 +1,7 @@
 // sg_decode_select: decode-time dynamic KV selection (Section 2.3: each step
 // the selector picks KV entries from the decode query; Section 5.1: InfiniGen's
-// alpha = 5 and a maximum KV selection ratio of 20%).
+// alpha = 5, a partial ratio of 0.3 and a maximum KV selection ratio of 20%).
+// Rows are whole heads or a partial set of their channels (32 to 128 wide).
 //
 // select_logits: z[u][g][j] = scale * q[b][l][g] . k_j for the G q heads of
 //   unit u = (b, l, h) and every key j < N_b.  One pass over the unit's keys:
@@ -22,12 +23,17 @@ constexpr int SEL_CHUNK = 512;    // keys per workgroup of the logits pass (many
 constexpr int SEL_UNROLL = 4;     // key rows in flight per lane group
 constexpr int SEL_MAX_G = 8;
 
+constexpr int gcd_c(int a, int b) { return b == 0 ? a : gcd_c(b, a % b); }
+
+// Rows of D elements (a whole head, or a partial set of its channels): VPR
+// 16-byte slices, LPR lanes per row (a power of two dividing VPR, at most 4,
+// 8 for rows of 32 slices), VPL slices per lane.
 template <typename T, int D>
 struct SelShape {
-    static constexpr int VPR = D * (int)sizeof(T) / 16;            // 16-byte slices per row
-    static constexpr int LPR = VPR / 4 >= 4 ? VPR / 4 : 4;          // lanes per row
-    static constexpr int VPL = VPR / LPR;                           // slices per lane
-    static constexpr int RPB = SEL_THREADS / LPR;                   // rows per workgroup step
+    static constexpr int VPR = D * (int)sizeof(T) / 16;
+    static constexpr int LPR = gcd_c(VPR, VPR >= 32 ? 8 : 4);
+    static constexpr int VPL = VPR / LPR;
+    static_assert(D * (int)sizeof(T) % 16 == 0, "rows must be whole 16-byte slices");
 };
 
 struct SelUnit {
@@ -113,18 +119,30 @@ __global__ __launch_bounds__(SEL_THREADS) void select_logits_kernel(int B, int L
                 if (live) mx[hh] = fmaxf(mx[hh], zs[r][hh]);
             }
         }
-        // lane L stores row w0 + L of every head (whole 256-byte pieces): that
-        // value sits in lane group L % GPW, unroll slot L / GPW
-        const int jw = w0 + lane;
+        if constexpr (WROWS <= 64) {
+            // lane L stores row w0 + L of every head (whole pieces of 4 * WROWS
+            // bytes): that value sits in lane group L % GPW, unroll slot L / GPW
+            const int jw = w0 + lane;
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-            float v = 0.f;
+            for (int hh = 0; hh < G; ++hh) {
+                float v = 0.f;
+#pragma unroll
+                for (int r = 0; r < SEL_UNROLL; ++r) {
+                    const float t = __shfl(zs[r][hh], (lane % GPW) * S::LPR, 64);
+                    v = lane / GPW == r ? t : v;
+                }
+                if (lane < WROWS && jw < j1) zu[(int64_t)hh * ldz + jw] = v;
+            }
+        } else {
+            // one or two lanes per row: the lane groups of a step already hold
+            // consecutive rows
 #pragma unroll
             for (int r = 0; r < SEL_UNROLL; ++r) {
-                const float t = __shfl(zs[r][hh], (lane % GPW) * S::LPR, 64);
-                v = lane / GPW == r ? t : v;
+                const int j = w0 + r * GPW + grp;
+#pragma unroll
+                for (int hh = 0; hh < G; ++hh)
+                    if (hh % S::LPR == lv && j < j1) zu[(int64_t)hh * ldz + j] = zs[r][hh];
             }
-            if (lane < WROWS && jw < j1) zu[(int64_t)hh * ldz + jw] = v;
         }
     }
     // the chunk's maximum of every head (exact: a maximum of the stored values)
@@ -210,25 +228,44 @@ __global__ __launch_bounds__(TOPK_THREADS) void select_thresh_kernel(int B, int 
     if (tid == 0) *ns = kk;
 }
 
+struct LogitsArgs {
+    int B, L, Hq, Hkv;
+    const int32_t *cu_seqlens;
+    int64_t T;
+    int max_seqlen;
+    const void *q, *k;
+    int64_t k_layer_rows;
+    float scale;
+    float *z, *zmax;
+};
+
 template <typename E, int D, int G>
-static void launch_logits(hipStream_t s, int B, int L, int Hq, int Hkv, const int32_t *cu_seqlens, int64_t T,
-                          int max_seqlen, const void *q, const void *k, int64_t k_layer_rows, float *z, float *zmax) {
-    const int nchunk = (int)ceil_div(max_seqlen, SEL_CHUNK);
-    const int64_t grid = (int64_t)B * L * Hkv * nchunk;
+static void launch_logits(hipStream_t s, const LogitsArgs &a) {
+    const int nchunk = (int)ceil_div(a.max_seqlen, SEL_CHUNK);
+    const int64_t grid = (int64_t)a.B * a.L * a.Hkv * nchunk;
     select_logits_kernel<E, D, G><<<(unsigned)grid, SEL_THREADS, 0, s>>>(
-        B, L, Hq, Hkv, cu_seqlens, T, reinterpret_cast<const E *>(q), reinterpret_cast<const E *>(k), k_layer_rows,
-        1.0f / sqrtf((float)D), nchunk, max_seqlen, z, zmax);
+        a.B, a.L, a.Hq, a.Hkv, a.cu_seqlens, a.T, reinterpret_cast<const E *>(a.q), reinterpret_cast<const E *>(a.k),
+        a.k_layer_rows, a.scale, nchunk, a.max_seqlen, a.z, a.zmax);
 }
 
 template <typename E, int D>
-static void launch_logits_g(hipStream_t s, int G, int B, int L, int Hq, int Hkv, const int32_t *cu_seqlens,
-                            int64_t T, int max_seqlen, const void *q, const void *k, int64_t k_layer_rows, float *z,
-                            float *zmax) {
+static void launch_logits_g(hipStream_t s, int G, const LogitsArgs &a) {
     switch (G) {
-        case 1: launch_logits<E, D, 1>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zmax); break;
-        case 2: launch_logits<E, D, 2>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zmax); break;
-        case 4: launch_logits<E, D, 4>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zmax); break;
-        default: launch_logits<E, D, 8>(s, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zmax); break;
+        case 1: launch_logits<E, D, 1>(s, a); break;
+        case 2: launch_logits<E, D, 2>(s, a); break;
+        case 4: launch_logits<E, D, 4>(s, a); break;
+        default: launch_logits<E, D, 8>(s, a); break;
+    }
+}
+
+template <typename E>
+static void launch_logits_d(hipStream_t s, int d, int G, const LogitsArgs &a) {
+    switch (d) {
+        case 32: launch_logits_g<E, 32>(s, G, a); break;
+        case 40: launch_logits_g<E, 40>(s, G, a); break;
+        case 48: launch_logits_g<E, 48>(s, G, a); break;
+        case 64: launch_logits_g<E, 64>(s, G, a); break;
+        default: launch_logits_g<E, 128>(s, G, a); break;
     }
 }
 
@@ -245,15 +282,18 @@ extern "C" size_t sg_decode_select_workspace_size(int B, int L, int Hq, int max_
 
 extern "C" int sg_decode_select(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, const void *q,
                                 const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *k,
-                                int64_t k_layer_rows, float alpha, const int32_t *cu_cap, int64_t K_cap,
-                                int32_t *idx, int32_t *n_sel, void *ws, size_t ws_bytes) {
+                                int64_t k_layer_rows, float scale, float alpha, const int32_t *cu_cap,
+                                int64_t K_cap, int32_t *idx, int32_t *n_sel, void *ws, size_t ws_bytes) {
     SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "sg_decode_select: unknown dtype %d", (int)dt);
     SG_REQUIRE(B >= 1 && L >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0, SG_EINVAL,
                "sg_decode_select: need B, L, Hq, Hkv >= 1 and Hq %% Hkv == 0");
     const int G = Hq / Hkv;
     SG_REQUIRE(G == 1 || G == 2 || G == 4 || G == 8, SG_EUNSUPPORTED, "sg_decode_select: group size %d (1, 2, 4, 8)",
                G);
-    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "sg_decode_select: head dimension %d not supported", d);
+    SG_REQUIRE(d == 32 || d == 40 || d == 48 || d == 64 || d == 128, SG_EUNSUPPORTED,
+               "sg_decode_select: row width %d not supported (32, 40, 48, 64, 128)", d);
+    SG_REQUIRE(scale >= 0.f && scale < INFINITY, SG_EINVAL, "sg_decode_select: scale must be finite and >= 0");
+    if (scale == 0.f) scale = 1.0f / sqrtf((float)d);
     SG_REQUIRE(alpha >= 0.f && alpha < INFINITY, SG_EINVAL, "sg_decode_select: alpha must be finite and >= 0");
     SG_REQUIRE(T >= 0 && max_seqlen >= 0 && k_layer_rows >= 0 && K_cap >= 0, SG_EINVAL,
                "sg_decode_select: negative size");
@@ -272,13 +312,9 @@ extern "C" int sg_decode_select(void *stream, sg_dtype dt, int B, int L, int Hq,
         SG_REQUIRE(ws && ws_bytes >= need, SG_EWORKSPACE, "sg_decode_select: workspace %zu < %zu", ws_bytes, need);
         float *z = reinterpret_cast<float *>(ws);
         float *zm = z + (int64_t)B * L * Hq * max_seqlen;
-        if (dt == SG_BF16) {
-            if (d == 128) launch_logits_g<uint16_t, 128>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zm);
-            else launch_logits_g<uint16_t, 64>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zm);
-        } else {
-            if (d == 128) launch_logits_g<float, 128>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zm);
-            else launch_logits_g<float, 64>(s, G, B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, z, zm);
-        }
+        const LogitsArgs a{B, L, Hq, Hkv, cu_seqlens, T, max_seqlen, q, k, k_layer_rows, scale, z, zm};
+        if (dt == SG_BF16) launch_logits_d<uint16_t>(s, d, G, a);
+        else launch_logits_d<float>(s, d, G, a);
     }
     const float *z = reinterpret_cast<const float *>(ws);
     const float *zm = z + (int64_t)B * L * Hq * std::max(max_seqlen, 0);

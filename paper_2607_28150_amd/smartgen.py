@@ -78,8 +78,8 @@ def load() -> ctypes.CDLL:
     lib.sg_score_count.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _l, _i, _vp, _vp, _l, _f, _vp, _vp, _sz]
     lib.sg_decode_select_workspace_size.argtypes = [_i, _i, _i, _i]
     lib.sg_decode_select_workspace_size.restype = _sz
-    lib.sg_decode_select.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _l, _i, _vp, _l, _f, _vp, _l, _vp, _vp,
-                                     _vp, _sz]
+    lib.sg_decode_select.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _l, _i, _vp, _l, _f, _f, _vp, _l, _vp,
+                                     _vp, _vp, _sz]
     lib.sg_spec_quota.argtypes = [_l, _i]
     lib.sg_spec_quota.restype = _l
     lib.sg_spec_push.argtypes = [_vp, _i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _vp, _vp, _l, _i, _vp, _vp, _vp]
@@ -195,9 +195,10 @@ def decode_select_workspace_size(B, L, Hq, max_seqlen) -> int:
 
 
 def sg_decode_select(q, k, cu_seqlens, T, max_seqlen, Hkv, cu_cap, K_cap, idx, n_sel, alpha, ws,
-                     k_layer_rows=None, stream=None):
+                     k_layer_rows=None, scale=None, stream=None):
     """Decode-time selection: idx [L][Hkv][K_cap] (ids ascending, then -1) and
-    n_sel [B][L][Hkv] from the step's queries q [B][L][Hq][d] and the keys."""
+    n_sel [B][L][Hkv] from the step's queries q [B][L][Hq][d] and the keys (whole
+    heads or a partial set of channels; scale defaults to 1/sqrt(d))."""
     B, L, Hq, d = q.shape
     _need(k.dtype == q.dtype, "q and k must share a dtype")
     _need(cu_seqlens.dtype == torch.int32 and cu_seqlens.numel() == B + 1, "cu_seqlens must be int32 [B+1]")
@@ -208,7 +209,8 @@ def sg_decode_select(q, k, cu_seqlens, T, max_seqlen, Hkv, cu_cap, K_cap, idx, n
         k_layer_rows = 0 if (k.dim() == 4 and k.shape[0] == 1 and L > 1) else Hkv * T
     _need(k.numel() >= ((L - 1) * k_layer_rows + Hkv * T) * d, "k is smaller than its layout needs")
     rc = load().sg_decode_select(_stream(stream), _dtype_code(q), B, L, Hq, Hkv, d, _ptr(q), _ptr(cu_seqlens), int(T),
-                                 int(max_seqlen), _ptr(k), int(k_layer_rows), float(alpha), _ptr(cu_cap),
+                                 int(max_seqlen), _ptr(k), int(k_layer_rows), float(scale or 0.0), float(alpha),
+                                 _ptr(cu_cap),
                                  int(K_cap), _ptr(idx), _ptr(n_sel), _ptr(ws),
                                  0 if ws is None else ws.numel() * ws.element_size())
     _check("sg_decode_select", rc)

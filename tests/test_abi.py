@@ -162,11 +162,15 @@ def test_selector_host_checks(lib):
     rc = lib.sg_score_count(None, 1, 1, 1, 8, 8, 64, 32, P, 4096, 4096, P, P, 0, 5.0, P, P, 16)
     assert rc == smartgen.SG_EWORKSPACE
     assert smartgen.decode_select_workspace_size(1, 32, 32, 8192) == 32 * 32 * (8192 + 16) * 4   # logits, chunk maxima
-    rc = lib.sg_decode_select(None, 1, 1, 1, 24, 8, 128, P, P, 100, 100, P, 0, 5.0, P, 10, P, P, P, 1 << 30)
+    rc = lib.sg_decode_select(None, 1, 1, 1, 24, 8, 128, P, P, 100, 100, P, 0, 0.0, 5.0, P, 10, P, P, P, 1 << 30)
     assert rc == smartgen.SG_EUNSUPPORTED and "group" in _err(lib)          # G = 3
-    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 40000, 40000, P, 0, 5.0, P, 10, P, P, P, 1 << 30)
+    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 40000, 40000, P, 0, 0.0, 5.0, P, 10, P, P, P, 1 << 30)
     assert rc == smartgen.SG_EUNSUPPORTED                                   # rows above 32 x 1024
-    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 100, 100, P, 0, float("nan"), P, 10, P, P, P, 1 << 30)
+    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 100, 100, P, 0, 0.0, float("nan"), P, 10, P, P, P, 1 << 30)
     assert rc == smartgen.SG_EINVAL
-    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 100, 100, P, 0, 5.0, P, 10, P, P, P, 64)
+    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 56, P, P, 100, 100, P, 0, 0.0, 5.0, P, 10, P, P, P, 1 << 30)
+    assert rc == smartgen.SG_EUNSUPPORTED and "width" in _err(lib)         # 56 channels
+    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 100, 100, P, 0, -1.0, 5.0, P, 10, P, P, P, 1 << 30)
+    assert rc == smartgen.SG_EINVAL and "scale" in _err(lib)
+    rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 100, 100, P, 0, 0.0, 5.0, P, 10, P, P, P, 64)
     assert rc == smartgen.SG_EWORKSPACE

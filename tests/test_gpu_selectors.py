@@ -90,7 +90,7 @@ def test_score_count_llama8b_8k_sampled(gpu_lib):
         assert got[l, h, heavy].mean() > 2 * got[l, h].mean()     # the planted heavy hitters are picked often
 
 
-def _select(gpu_lib, q, k, lens, Hkv, caps, alpha):
+def _select(gpu_lib, q, k, lens, Hkv, caps, alpha, scale=None):
     B, L, Hq, d = q.shape
     cus = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
     cc = np.concatenate([[0], np.cumsum(caps)]).astype(np.int32)
@@ -98,26 +98,31 @@ def _select(gpu_lib, q, k, lens, Hkv, caps, alpha):
     ws = torch.empty(gpu_lib.decode_select_workspace_size(B, L, Hq, max(lens)), dtype=torch.uint8, device="cuda")
     idx = torch.full((L, Hkv, Kc), -7, dtype=torch.int32, device="cuda")
     n_sel = torch.full((B, L, Hkv), -7, dtype=torch.int32, device="cuda")
-    gpu_lib.sg_decode_select(q.cuda(), k.cuda(), cu(cus), T, max(lens), Hkv, cu(cc), Kc, idx, n_sel, alpha, ws)
+    gpu_lib.sg_decode_select(q.cuda(), k.cuda(), cu(cus), T, max(lens), Hkv, cu(cc), Kc, idx, n_sel, alpha, ws,
+                             scale=scale)
     torch.cuda.synchronize()
     return idx.cpu().numpy(), n_sel.cpu().numpy(), cus, cc
 
 
-@pytest.mark.parametrize("dtype,G,lens,cap_bp,alpha", [
-    ("bf16", 4, (3000, 1234), 2000, ALPHA_EXACT),     # the 20% cap
-    ("f32", 2, (5000,), 50, ALPHA_EXACT),             # the cap binds hard
-    ("bf16", 8, (700, 64, 2100), 10000, ALPHA_EXACT),
-    ("bf16", 1, (2049,), 2000, 0.0),                   # alpha 0: each head's maxima only
+@pytest.mark.parametrize("dtype,G,d,lens,cap_bp,alpha", [
+    ("bf16", 4, 64, (3000, 1234), 2000, ALPHA_EXACT),     # the 20% cap
+    ("f32", 2, 64, (5000,), 50, ALPHA_EXACT),             # the cap binds hard
+    ("bf16", 8, 64, (700, 64, 2100), 10000, ALPHA_EXACT),
+    ("bf16", 1, 64, (2049,), 2000, 0.0),                   # alpha 0: each head's maxima only
+    ("bf16", 4, 40, (3000, 900), 2000, ALPHA_EXACT),      # a partial set of 40 channels
+    ("f32", 8, 48, (1500,), 2000, ALPHA_EXACT),
+    ("bf16", 2, 32, (2500,), 500, ALPHA_EXACT),
 ])
-def test_decode_select_exact(gpu_lib, dtype, G, lens, cap_bp, alpha):
-    say("decode select exact", dtype, G, lens, cap_bp, alpha)
-    L, Hkv, d = 2, 2, 64
+def test_decode_select_exact(gpu_lib, dtype, G, d, lens, cap_bp, alpha):
+    say("decode select exact", dtype, G, d, lens, cap_bp, alpha)
+    L, Hkv = 2, 2
     T = sum(lens)
     q = _ints((len(lens), L, Hkv * G, d), -2, 2, G + T, dtype)
     k = _ints((L, Hkv, T, d), -2, 2, G * T + 3, dtype)
     caps = [max(1, n * cap_bp // 10000) for n in lens]
-    idx, n_sel, cus, cc = _select(gpu_lib, q, k, lens, Hkv, caps, alpha)
-    r_idx, r_n, _ = oracle.decode_select(q.float().numpy(), k.float().numpy(), cus, Hkv, cc, alpha)
+    # scale 1/8 keeps every logit exact at every width (that of a 64-wide head)
+    idx, n_sel, cus, cc = _select(gpu_lib, q, k, lens, Hkv, caps, alpha, scale=0.125)
+    r_idx, r_n, _ = oracle.decode_select(q.float().numpy(), k.float().numpy(), cus, Hkv, cc, alpha, scale=0.125)
     np.testing.assert_array_equal(n_sel, r_n)
     np.testing.assert_array_equal(idx, r_idx)
 
@@ -143,17 +148,18 @@ def _check_band(idx, n_sel, r_idx, r_n, r, cus, cc, alpha, eps=1e-3):
                 assert not inside[rr < edge - eps].any(), "a clearly rejected entry is selected"
 
 
-@pytest.mark.parametrize("G,lens", [(4, (4000, 900)), (8, (2500,))])
-def test_decode_select_band(gpu_lib, G, lens):
-    say("decode select band", G, lens)
-    L, Hkv, d, alpha = 2, 2, 128, 5.0
+@pytest.mark.parametrize("G,d,lens", [(4, 128, (4000, 900)), (8, 128, (2500,)), (4, 40, (3000, 1000))])
+def test_decode_select_band(gpu_lib, G, d, lens):
+    say("decode select band", G, d, lens)
+    L, Hkv, alpha = 2, 2, 5.0
     T = sum(lens)
-    g = np.random.default_rng(G + T)
+    scale = 128 ** -0.5                   # the full head's scale, also for a partial set of channels
+    g = np.random.default_rng(G + T + d)
     q = torch.from_numpy(g.standard_normal((len(lens), L, Hkv * G, d), dtype=np.float32) * 2).to(torch.bfloat16)
     k = torch.from_numpy(g.standard_normal((L, Hkv, T, d), dtype=np.float32)).to(torch.bfloat16)
     caps = [n // 5 for n in lens]
-    idx, n_sel, cus, cc = _select(gpu_lib, q, k, lens, Hkv, caps, alpha)
-    r_idx, r_n, r = oracle.decode_select(q.float().numpy(), k.float().numpy(), cus, Hkv, cc, alpha)
+    idx, n_sel, cus, cc = _select(gpu_lib, q, k, lens, Hkv, caps, alpha, scale=scale)
+    r_idx, r_n, r = oracle.decode_select(q.float().numpy(), k.float().numpy(), cus, Hkv, cc, alpha, scale=scale)
     _check_band(idx, n_sel, r_idx, r_n, r, cus, cc, alpha)
 
 
