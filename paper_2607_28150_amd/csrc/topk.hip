@@ -14,6 +14,13 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(int B, const int32_t
                                                             int64_t K_total, const float *__restrict__ scores,
                                                             int32_t *__restrict__ idx) {
     __shared__ SelectSmem sm;
+    // long rows pass through LDS in chunks: coalesced loads, then each thread
+    // reads its consecutive keys (one pad word per 32 keeps the reads free of
+    // bank conflicts); reading them straight from memory would touch a new
+    // cache line per lane and instruction
+    constexpr bool STAGE = ITEMS >= 16 && ITEMS <= 32;   // wider rows: no registers to spare
+    constexpr int CH = 16384;
+    __shared__ float stage[STAGE ? CH + CH / 32 : 1];
 
     const int b = blockIdx.x % B;
     const int64_t lh = blockIdx.x / B;
@@ -37,8 +44,25 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(int B, const int32_t
     const int first = tid * ITEMS;
     const int nv = (int)max<int64_t>(0, min<int64_t>(ITEMS, N - first));
     uint32_t key[ITEMS];
+    if constexpr (STAGE) {
 #pragma unroll
-    for (int i = 0; i < ITEMS; ++i) key[i] = i < nv ? order_key(row[first + i]) : 0u;
+        for (int i = 0; i < ITEMS; ++i) key[i] = 0u;
+        for (int c0 = 0; c0 < (int)N; c0 += CH) {       // uniform
+            const int cn = min<int64_t>(CH, N - c0);
+#pragma unroll 4
+            for (int j = tid; j < cn; j += TOPK_THREADS) stage[j + (j >> 5)] = row[c0 + j];
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < ITEMS; ++i) {
+                const int x = first + i - c0;
+                if (i < nv && x >= 0 && x < cn) key[i] = order_key(stage[x + (x >> 5)]);
+            }
+            __syncthreads();
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < ITEMS; ++i) key[i] = i < nv ? order_key(row[first + i]) : 0u;
+    }
 
     select_top<ITEMS>(key, nv, first, (int)kk, out, sm);
 }
