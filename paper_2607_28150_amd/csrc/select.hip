@@ -208,17 +208,35 @@ __global__ __launch_bounds__(TOPK_THREADS) void select_thresh_kernel(int B, int 
     for (int hh = 0; hh < SEL_MAX_G; ++hh) mg[hh] = hh < G ? gmax[0][hh] : -INFINITY;
     // r_j = the best margin over the group's heads; the rule's count
     uint32_t key[ITEMS];
+    float rr[ITEMS];
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) rr[i] = -INFINITY;
+    const bool vec = ITEMS % 4 == 0 && nv == ITEMS && ldz % 4 == 0;    // whole, 16-byte aligned pieces
+#pragma unroll
+    for (int hh = 0; hh < SEL_MAX_G; ++hh) {
+        if (hh < G) {
+            const float *zr = zu + (int64_t)hh * ldz + first;
+            if (vec) {
+#pragma unroll
+                for (int i = 0; i < ITEMS; i += 4) {
+                    const float4 x = *reinterpret_cast<const float4 *>(zr + i);
+                    rr[i] = fmaxf(rr[i], x.x - mg[hh]);
+                    rr[i + 1] = fmaxf(rr[i + 1], x.y - mg[hh]);
+                    rr[i + 2] = fmaxf(rr[i + 2], x.z - mg[hh]);
+                    rr[i + 3] = fmaxf(rr[i + 3], x.w - mg[hh]);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < ITEMS; ++i)
+                    if (i < nv) rr[i] = fmaxf(rr[i], zr[i] - mg[hh]);
+            }
+        }
+    }
     int cnt = 0;
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i) {
-        float r = -INFINITY;
-        if (i < nv) {
-#pragma unroll
-            for (int hh = 0; hh < SEL_MAX_G; ++hh)
-                if (hh < G) r = fmaxf(r, zu[(int64_t)hh * ldz + first + i] - mg[hh]);
-        }
-        key[i] = i < nv ? order_key(r) : 0u;
-        cnt += (i < nv && r >= -alpha) ? 1 : 0;
+        key[i] = i < nv ? order_key(rr[i]) : 0u;
+        cnt += (i < nv && rr[i] >= -alpha) ? 1 : 0;
     }
     int total;
     block_scan_incl(cnt, sm.wsum, total);

@@ -59,6 +59,16 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(int B, const int32_t
             }
             __syncthreads();
         }
+    } else if (ITEMS % 4 == 0 && nv == ITEMS && (reinterpret_cast<uintptr_t>(row + first) & 15u) == 0) {
+        // a thread's keys whole and 16-byte aligned: vector loads
+#pragma unroll
+        for (int i = 0; i < ITEMS; i += 4) {
+            const float4 x = *reinterpret_cast<const float4 *>(row + first + i);
+            key[i] = order_key(x.x);
+            key[i + 1] = order_key(x.y);
+            key[i + 2] = order_key(x.z);
+            key[i + 3] = order_key(x.w);
+        }
     } else {
 #pragma unroll
         for (int i = 0; i < ITEMS; ++i) key[i] = i < nv ? order_key(row[first + i]) : 0u;
