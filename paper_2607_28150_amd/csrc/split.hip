@@ -7,18 +7,13 @@
 // the stable descending sort by mask value (operators 4, 5) are all prefix
 // popcounts plus a running per-value count.  A first pass counts the remote
 // entries, which fixes where the local entries start in the reordered row.
+// Each pass takes four chunks at a time, issuing all their loads together.
 #include "sg_internal.h"
 
 namespace sg {
 
 constexpr int SPLIT_WAVES = 4;
-
-__device__ __forceinline__ int gather_mask(const int8_t *__restrict__ mask, int64_t moff, int32_t mlen,
-                                           int64_t mask_bytes, int32_t t) {
-    int m = 0;
-    if (t >= 0 && t < mlen && moff + t < mask_bytes) m = mask[moff + t];
-    return (m == 1 || m == 2) ? m : 0;
-}
+constexpr int SPLIT_GROUP = 4;     // 64-entry chunks whose loads are issued together
 
 __global__ __launch_bounds__(64 * SPLIT_WAVES) void split_kernel(
     int rows, const int32_t *__restrict__ row_off, int64_t total, const int32_t *__restrict__ kv_index,
@@ -43,43 +38,64 @@ __global__ __launch_bounds__(64 * SPLIT_WAVES) void split_kernel(
     const int32_t mlen = moff >= 0 ? mask_len[r] : 0;   // a negative offset makes every entry a pad
     const uint64_t lt = lanemask_lt();
 
+    // The loads of SPLIT_GROUP chunks are issued together (indices, then mask
+    // values at clamped addresses), so a group costs two memory round trips.
+    const bool has_mask = mask_bytes > 0;
+    auto load_group = [&](int64_t c, int32_t (&t)[SPLIT_GROUP], int (&m)[SPLIT_GROUP]) {
+#pragma unroll
+        for (int u = 0; u < SPLIT_GROUP; ++u) t[u] = kv_index[o + min<int64_t>(c + u * 64 + lane, n - 1)];
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < SPLIT_GROUP; ++u) {
+            const bool ok = has_mask && t[u] >= 0 && t[u] < mlen && moff + t[u] < mask_bytes;
+            const int x = has_mask ? mask[ok ? moff + t[u] : 0] : 0;
+            m[u] = ok && (x == 1 || x == 2) ? x : 0;
+        }
+    };
     // pass 1: count remote entries (the start of the local block in the reordered row)
     int64_t n2 = 0, n1 = 0;
-    for (int64_t c = 0; c < n; c += 64) {
-        const int64_t i = c + lane;
-        const int m = i < n ? gather_mask(mask, moff, mlen, mask_bytes, kv_index[o + i]) : 0;
-        n2 += __popcll(__ballot(m == 2));
-        n1 += __popcll(__ballot(m == 1));
+    for (int64_t c = 0; c < n; c += 64 * SPLIT_GROUP) {
+        int32_t t[SPLIT_GROUP];
+        int m[SPLIT_GROUP];
+        load_group(c, t, m);
+#pragma unroll
+        for (int u = 0; u < SPLIT_GROUP; ++u) {
+            const bool in = c + u * 64 + lane < n;
+            n2 += __popcll(__ballot(in && m[u] == 2));
+            n1 += __popcll(__ballot(in && m[u] == 1));
+        }
     }
     // pass 2: write the partitions
     int64_t c2 = 0, c1 = 0, c0 = 0;
-    for (int64_t c = 0; c < n; c += 64) {
-        const int64_t i = c + lane;
-        int32_t t = -1;
-        int m = 0;
-        if (i < n) {
-            t = kv_index[o + i];
-            m = gather_mask(mask, moff, mlen, mask_bytes, t);
-        }
-        const uint64_t b2 = __ballot(i < n && m == 2);
-        const uint64_t b1 = __ballot(i < n && m == 1);
-        const uint64_t b0 = __ballot(i < n && m == 0);
-        if (i < n) {
-            if (m == 2) {
-                const int64_t p = c2 + __popcll(b2 & lt);
-                remote[o + p] = t;
-                if (reorder) out_index[o + p] = t;
-            } else if (m == 1) {
-                const int64_t p = c1 + __popcll(b1 & lt);
-                local[o + p] = t;
-                if (reorder) out_index[o + n2 + p] = t;
-            } else if (reorder) {
-                out_index[o + n2 + n1 + c0 + __popcll(b0 & lt)] = t;
+    for (int64_t c = 0; c < n; c += 64 * SPLIT_GROUP) {
+        int32_t tt[SPLIT_GROUP];
+        int mm[SPLIT_GROUP];
+        load_group(c, tt, mm);
+#pragma unroll
+        for (int u = 0; u < SPLIT_GROUP; ++u) {
+            const int64_t i = c + u * 64 + lane;
+            const int32_t t = tt[u];
+            const int m = mm[u];
+            const uint64_t b2 = __ballot(i < n && m == 2);
+            const uint64_t b1 = __ballot(i < n && m == 1);
+            const uint64_t b0 = __ballot(i < n && m == 0);
+            if (i < n) {
+                if (m == 2) {
+                    const int64_t p = c2 + __popcll(b2 & lt);
+                    remote[o + p] = t;
+                    if (reorder) out_index[o + p] = t;
+                } else if (m == 1) {
+                    const int64_t p = c1 + __popcll(b1 & lt);
+                    local[o + p] = t;
+                    if (reorder) out_index[o + n2 + p] = t;
+                } else if (reorder) {
+                    out_index[o + n2 + n1 + c0 + __popcll(b0 & lt)] = t;
+                }
             }
+            c2 += __popcll(b2);
+            c1 += __popcll(b1);
+            c0 += __popcll(b0);
         }
-        c2 += __popcll(b2);
-        c1 += __popcll(b1);
-        c0 += __popcll(b0);
     }
     // unused tails of the compacted outputs
     for (int64_t i = n1 + lane; i < n; i += 64) local[o + i] = -1;
