@@ -159,15 +159,15 @@ def main():
     # decode steps, each one attention launch over all layers.  The decode
     # launches run back to back between two events (an event between every
     # launch would add its own marker to each measured interval).
+    # (events mark only the ends of the select region, the split and the
+    # decode launches; each op's own time is measured apart, below)
     def step(r, e):
         if e is None:
             e = [None] * 6
         rec = lambda i: e[i].record() if e[i] is not None else None  # noqa: E731
         rec(0)
         sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score)
-        rec(1)
         sg.sg_topk(scores, cus, T, N, cuk, K_total, idx)
-        rec(2)
         sg.sg_pack(pre["k"], pre["v"], idx, cus, T, cuk, K_total, K_total, bufs[r % reps])
         rec(3)
         sg.sg_split(row_off, idx.view(-1), mask.view(-1), mask_off, mask_len, 1, sp_local, sp_remote, sp_nl,
@@ -192,17 +192,27 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
 
-    # the one-pass score (row normalisers supplied), timed on its own
+    # each op of the select region on its own (back-to-back launches), and the
+    # one-pass score (row normalisers supplied)
     nrep = 10
-    ev_l = [ev() for _ in range(2)]
-    sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score, lse_in=lse_win)
-    torch.cuda.synchronize()
-    ev_l[0].record()
-    for _ in range(nrep):
-        sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score, lse_in=lse_win)
-    ev_l[1].record()
-    torch.cuda.synchronize()
-    t_score_lse = ev_l[0].elapsed_time(ev_l[1]) / nrep
+
+    def per_launch(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record()
+        for i in range(nrep):
+            fn(i)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / nrep
+
+    t_score = per_launch(lambda i=0: sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score))
+    t_topk = per_launch(lambda i=0: sg.sg_topk(scores, cus, T, N, cuk, K_total, idx))
+    t_pack = per_launch(lambda i=0: sg.sg_pack(pre["k"], pre["v"], idx, cus, T, cuk, K_total, K_total,
+                                               bufs[i % reps]))
+    t_score_lse = per_launch(lambda i=0: sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score,
+                                                     lse_in=lse_win))
 
     # block-granular proactive selection (eq. 1, eq. 2; M = 1024 blocks per
     # layer, transfer time 6.5x the prefill time), timed on its own
@@ -217,15 +227,13 @@ def main():
     # ------------------------------------------------------------- per-op times (HIP events on the launch stream)
     def ms(a, b):
         return a.elapsed_time(b)
-    t_score = np.mean([ms(e[0], e[1]) for e in ev_pool])
-    t_topk = np.mean([ms(e[1], e[2]) for e in ev_pool])
-    t_pack = np.mean([ms(e[2], e[3]) for e in ev_pool])
+    t_select = np.mean([ms(e[0], e[3]) for e in ev_pool])        # score + top-k + pack, back to back
     t_split = np.mean([ms(e[3], e[4]) for e in ev_pool])
     t_dec = np.mean([ms(e[4], e[5]) for e in ev_pool]) / nsteps_dec
     ms_per_step = wall * 1e3 / args.steps
 
     kv_bytes = 2 * L * Hkv * T * d * esize                       # the whole KV cache
-    sel_ms = t_score + t_topk + t_pack
+    sel_ms = t_select
     value = kv_bytes / (sel_ms * 1e-3) / 1e9
     score_flops = 2.0 * d * G * (W * N - W * (W - 1) / 2) * units
     pack_bytes_alg = 2 * S * d * esize * 2 + S * 4 * 2          # rows read + written, index read + written
@@ -271,7 +279,8 @@ def main():
         "config": {"workload": cfg.name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
                    "prompt": N, "score_window": W, "budget_bp": cfg.budget_bp, "k": K_total,
                    "decode_steps": nsteps_dec, "page_size": P, "transfer_replicas": reps},
-        "value_lse_in": round(kv_bytes / ((t_score_lse + t_topk + t_pack) * 1e-3) / 1e9, 2),
+        "select_ms": round(t_select, 4),
+        "value_lse_in": round(kv_bytes / ((t_select - t_score + t_score_lse) * 1e-3) / 1e9, 2),
         "decode_tokens_per_s": round(tokens_per_s, 1),
         "roofline": {"kernel": "sg_decode_attn", "bound": "hbm", "achieved": round(dec_gbs, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
