@@ -115,3 +115,89 @@ def test_two_lane_steps_llama8b_32k(gpu_lib, reuse):
         assert ratios[-1] <= ratios[0]
     else:
         assert ratios == pytest.approx([ratios[0]] * steps)
+
+
+def test_dynamic_decode_steps_exact(gpu_lib):
+    """The decode step of Sections 4.2 and 5.1 end to end: decode-time selection
+    from the step's queries (alpha rule, 20% cap), Algorithm 1 against the
+    decode side's mask, the two lanes with reuse, attention over the assembled
+    set.  Integer-valued inputs at d = 64 (scale 1/8) make every selection exact
+    on both sides, so the oracle replays the same steps and every array matches."""
+    say("dynamic decode steps")
+    B, L, Hq, Hkv, d, N, P, steps = 1, 2, 8, 2, 64, 3000, 16, 3
+    G, T, cap = Hq // Hkv, N, N // 5
+    alpha, scale = 5.0625, 0.125
+    g = np.random.default_rng(41)
+    ints = lambda shape: torch.from_numpy(g.integers(-2, 3, shape).astype(np.float32)).to(torch.bfloat16)
+    k, v = ints((L, Hkv, T, d)), ints((L, Hkv, T, d))
+    qs = [ints((B, L, Hq, d)) for _ in range(steps)]
+    units = L * Hkv
+    base = np.arange(units, dtype=np.int64) * T
+    base_d, mlen = cu(base, dtype=torch.int64), cu(np.full(units, N, np.int32))
+    src_k, src_v = k.contiguous().pin_memory(), v.contiguous().pin_memory()
+    kd = k.cuda()
+    # proactive set: the first 10% of every unit's tokens, delivered with their mask entries
+    kb = N // 10
+    sel = np.tile(np.arange(kb, dtype=np.int32), units)
+    store_k = torch.zeros((L, Hkv, T, d), dtype=torch.bfloat16, device="cuda")
+    store_v = torch.zeros_like(store_k)
+    mask = torch.full((L, Hkv, T), 2, dtype=torch.int8, device="cuda")
+    sel_off = cu(np.arange(units + 1) * kb)
+    gpu_lib.sg_fetch_keep(sel_off, units * kb, cu(sel), None, base_d, src_k, src_v, None, 1, None, None, None,
+                          base_d, store_k, store_v, mask.view(-1), base_d, mlen)
+    hk, hv = raw(src_k).reshape(-1, d), raw(src_v).reshape(-1, d)
+    o_sk, o_sv = np.zeros_like(hk), np.zeros_like(hv)
+    o_mask = np.full(units * T, 2, np.int8)
+    oracle.fetch_keep(np.arange(units + 1) * kb, sel, None, base, hk, hv, None, 1, np.zeros(units, np.int32), None,
+                      None, base, o_sk, o_sv, o_mask, base, np.full(units, N, np.int32))
+    max_pages = -(-cap // P)
+    pt = (g.permutation(units * max_pages).reshape(units, max_pages) * P).astype(np.int32)
+    pool_rows = units * max_pages * P
+    pt_d = cu(pt)
+    cus, cc = cu([0, N]), cu([0, cap])
+    ws_sel = torch.empty(gpu_lib.decode_select_workspace_size(B, L, Hq, N), dtype=torch.uint8, device="cuda")
+    ws_dec = torch.empty(max(16, gpu_lib.decode_workspace_size(L, Hq, Hkv, d, max_pages, P)), dtype=torch.uint8,
+                         device="cuda")
+    row_off = np.arange(units + 1, dtype=np.int32) * cap
+    lanes = TwoLane()
+    ratios = []
+    for step in range(steps):
+        say("dynamic decode step", step)
+        idx = torch.empty((L, Hkv, cap), dtype=torch.int32, device="cuda")
+        n_sel = torch.empty((B, L, Hkv), dtype=torch.int32, device="cuda")
+        gpu_lib.sg_decode_select(qs[step].cuda(), kd, cus, T, N, Hkv, cc, cap, idx, n_sel, alpha, ws_sel, scale=scale)
+        kp = torch.zeros((pool_rows, d), dtype=torch.bfloat16, device="cuda")
+        vp = torch.zeros_like(kp)
+        buf = StepBuffers.alloc(units, units * cap)
+        n_kept = lanes.gather(row_off=cu(row_off), kv_index=idx.view(-1), mask=mask.view(-1), mask_off=base_d,
+                              mask_len=mlen, store_k=store_k, store_v=store_v, store_base=base_d, src_k=src_k,
+                              src_v=src_v, src_base=base_d, page_table=pt_d, page_size=P, k_pool=kp, v_pool=vp,
+                              buf=buf)
+        q_dec = qs[step][0].cuda()                                             # the step's queries, [L][Hq][d]
+        out = torch.empty((L, Hq, d), dtype=torch.float32, device="cuda")
+        gpu_lib.sg_decode_attn(q_dec, kp, vp, pt_d.view(L, Hkv, max_pages), n_kept, P, out, ws=ws_dec, scale=scale)
+        torch.cuda.synchronize()
+        # the oracle's own step
+        r_idx, r_n, _ = oracle.decode_select(qs[step].float().numpy(), k.float().numpy(), [0, N], Hkv, [0, cap],
+                                             alpha, scale=scale)
+        np.testing.assert_array_equal(idx.cpu().numpy(), r_idx)
+        np.testing.assert_array_equal(n_sel.cpu().numpy(), r_n)
+        r_out, r_loc, r_rem, r_nl, r_nr = oracle.split(row_off, r_idx.reshape(-1), o_mask, base,
+                                                       np.full(units, N), 1)
+        np.testing.assert_array_equal(buf.order[:units * cap].cpu().numpy(), r_out)
+        np.testing.assert_array_equal(n_kept.cpu().numpy(), r_nl + r_nr)
+        assert (r_nl + r_nr == r_n.reshape(-1)).all()                         # pads dropped, nothing else
+        okp, ovp = np.zeros((pool_rows, d), np.uint16), np.zeros((pool_rows, d), np.uint16)
+        oracle.fetch(row_off, r_loc, r_nl, base, o_sk, o_sv, pt, P, r_nr, okp, ovp)
+        oracle.fetch_keep(row_off, r_rem, r_nr, base, hk, hv, pt, P, np.zeros(units, np.int32), okp, ovp,
+                          base, o_sk, o_sv, o_mask, base, np.full(units, N, np.int32))
+        np.testing.assert_array_equal(raw(kp), okp)
+        np.testing.assert_array_equal(raw(vp), ovp)
+        np.testing.assert_array_equal(mask.view(-1).cpu().numpy(), o_mask)
+        ref = oracle.decode_attn(q_dec.float().cpu().numpy(), _f32_rows(okp, torch.bfloat16),
+                                 _f32_rows(ovp, torch.bfloat16), pt.reshape(L, Hkv, max_pages),
+                                 (r_nl + r_nr).reshape(L, Hkv), P, scale=scale)
+        np.testing.assert_allclose(out.cpu().numpy(), ref, atol=2e-2, rtol=0)
+        ratios.append(r_nr.sum() / (r_nl + r_nr).sum())
+    np.testing.assert_array_equal(raw(store_k).reshape(-1, d), o_sk)
+    assert ratios[0] > 0 and ratios[-1] <= ratios[0]      # reuse: fetched rows turn local
