@@ -327,17 +327,40 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
             for (int e = 0; e < PER16; ++e) o[g][j][e] = row_groups_sum<LPR>(o[g][j][e]);
     }
     __syncthreads();    // every wavefront is done with its ring
-    float *o_s = reinterpret_cast<float *>(ring);       // [NPART][HG][D]
+
+    // The partial state of every DPP row (4 per wavefront) goes to LDS.  After
+    // the row-group sums the COP lanes of a row that hold the same slice hold
+    // the same values, so each writes a different EPC-element piece of it, and
+    // piece (j, cp, c) is stored at ((j * COP + cp) * LPR + c) * EPC of the
+    // head's D floats: the 16 lanes of a row store one contiguous run (no bank
+    // conflicts).
+    constexpr int COP = 16 / LPR, EPC = PER16 / COP;
+    float *o_s = reinterpret_cast<float *>(ring);       // [NPART][HG][D], pieces permuted as above
     const int part = wave * 4 + lane / 16;
-    if (lane % 16 < LPR) {
+    {
+        const int cp = (lane % 16) / LPR;
 #pragma unroll
         for (int g = 0; g < HG; ++g)
 #pragma unroll
-            for (int j = 0; j < VPL; ++j)
+            for (int j = 0; j < VPL; ++j) {
+                float v[EPC];
 #pragma unroll
-                for (int e = 0; e < PER16; e += 4)
-                    *reinterpret_cast<float4 *>(o_s + (part * HG + g) * D + (j * LPR + c) * PER16 + e) =
-                        make_float4(o[g][j][e], o[g][j][e + 1], o[g][j][e + 2], o[g][j][e + 3]);
+                for (int e = 0; e < EPC; ++e) {
+                    v[e] = o[g][j][e];
+#pragma unroll
+                    for (int x = 1; x < COP; ++x) v[e] = cp == x ? o[g][j][x * EPC + e] : v[e];
+                }
+                float *dst = o_s + (part * HG + g) * D + ((j * COP + cp) * LPR + c) * EPC;
+                if constexpr (EPC >= 4) {
+#pragma unroll
+                    for (int e = 0; e < EPC; e += 4)
+                        *reinterpret_cast<float4 *>(dst + e) = make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
+                } else if constexpr (EPC == 2) {
+                    *reinterpret_cast<float2 *>(dst) = make_float2(v[0], v[1]);
+                } else {
+                    dst[0] = v[0];
+                }
+            }
     }
     if (lane % 16 == 0) {
 #pragma unroll
@@ -347,43 +370,75 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
 #pragma unroll
         for (int g = 0; g < HG; ++g) m_s[wave][g] = m[g];
     }
-    __syncthreads();
+    __syncthreads();    // partial states written
 
-    // combine the partial states; thread t handles four consecutive columns
-    // (g, cc .. cc + 3)
-    for (int i = tid; i < HG * D / 4; i += 64 * WAVES) {
-        const int g = 4 * i / D, cc = 4 * i % D;
+    // Combine.  An item is a run of RW stored floats of one head (inside one
+    // piece, so RW consecutive output columns); SUB adjacent threads share an
+    // item, each rescaling and adding NPART / SUB of the partial states, and
+    // DPP adds combine them.
+    constexpr int RW = EPC < 4 ? EPC : 4;
+    constexpr int ITEMS = HG * D / RW, THREADS = 64 * WAVES;
+    constexpr int SUB = THREADS / ITEMS >= 4 ? 4 : (THREADS / ITEMS >= 2 ? 2 : 1);
+    constexpr int PPS = NPART / SUB;
+    const int sub = tid % SUB;
+    for (int it = tid / SUB; it < ITEMS; it += THREADS / SUB) {     // uniform within a SUB group
+        const int g = it * RW / D, s0 = it * RW % D;
         float M = -INFINITY;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) M = fmaxf(M, m_s[w][g]);
-        float Lsum = 0.f;
-        float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+        float Lsum = 0.f, O[RW];
+#pragma unroll
+        for (int k = 0; k < RW; ++k) O[k] = 0.f;
         if (M > -INFINITY) {
 #pragma unroll
-            for (int w = 0; w < WAVES; ++w) {
+            for (int pp = 0; pp < PPS; ++pp) {
+                const int p = sub * PPS + pp, w = p / 4;
                 const float a = m_s[w][g] > -INFINITY ? __builtin_amdgcn_exp2f(m_s[w][g] - M) : 0.f;
+                const float *src = o_s + (p * HG + g) * D + s0;
+                float x[RW];
+                if constexpr (RW == 4) {
+                    const float4 y = *reinterpret_cast<const float4 *>(src);
+                    x[0] = y.x; x[1] = y.y; x[2] = y.z; x[3] = y.w;
+                } else {
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    const float4 x = *reinterpret_cast<const float4 *>(o_s + ((w * 4 + rr) * HG + g) * D + cc);
-                    Lsum = fmaf(a, l_s[w * 4 + rr][g], Lsum);
-                    O.x = fmaf(a, x.x, O.x);
-                    O.y = fmaf(a, x.y, O.y);
-                    O.z = fmaf(a, x.z, O.z);
-                    O.w = fmaf(a, x.w, O.w);
+                    for (int k = 0; k < RW; ++k) x[k] = src[k];
                 }
+                Lsum = fmaf(a, l_s[p][g], Lsum);
+#pragma unroll
+                for (int k = 0; k < RW; ++k) O[k] = fmaf(a, x[k], O[k]);
             }
         }
-        const float ov[4] = {O.x, O.y, O.z, O.w};
+        if constexpr (SUB >= 2) {
+            Lsum += dpp<DPP_XOR1>(Lsum);
+#pragma unroll
+            for (int k = 0; k < RW; ++k) O[k] += dpp<DPP_XOR1>(O[k]);
+        }
+        if constexpr (SUB == 4) {
+            Lsum += dpp<DPP_XOR2>(Lsum);
+#pragma unroll
+            for (int k = 0; k < RW; ++k) O[k] += dpp<DPP_XOR2>(O[k]);
+        }
+        // output column of stored float s0: piece (j, cp, c), element e
+        const int piece = s0 / EPC, e = s0 % EPC;
+        const int cc = ((piece / (LPR * COP)) * LPR + piece % LPR) * PER16 + ((piece / LPR) % COP) * EPC + e;
         const int gl = (int)blockIdx.z * HG + g;       // head within the KV group
-        if (nsplit == 1) {
-            float *po = out + ((int64_t)b * Hq + gq0 + g) * D + cc;
+        if (sub == 0) {
+            if (nsplit == 1) {
+                float *po = out + ((int64_t)b * Hq + gq0 + g) * D + cc;
+                const float inv = Lsum > 0.f ? 1.f / Lsum : 0.f;
+                if (RW == 4 && (reinterpret_cast<uintptr_t>(po) & 15u) == 0) {
+                    *reinterpret_cast<float4 *>(po) = make_float4(O[0] * inv, O[RW > 1 ? 1 : 0] * inv,
+                                                                  O[RW > 2 ? 2 : 0] * inv, O[RW > 3 ? 3 : 0] * inv);
+                } else {
 #pragma unroll
-            for (int k = 0; k < 4; ++k) po[k] = Lsum > 0.f ? ov[k] / Lsum : 0.f;
-        } else {
-            float *pp = part_ptr(ws, unit, nsplit, split, G, D) + (int64_t)gl * (D + 2);
-            if (cc == 0) { pp[0] = M; pp[1] = Lsum; }
+                    for (int k = 0; k < RW; ++k) po[k] = O[k] * inv;
+                }
+            } else {
+                float *pp = part_ptr(ws, unit, nsplit, split, G, D) + (int64_t)gl * (D + 2);
+                if (cc == 0) { pp[0] = M; pp[1] = Lsum; }
 #pragma unroll
-            for (int k = 0; k < 4; ++k) pp[2 + cc + k] = ov[k];
+                for (int k = 0; k < RW; ++k) pp[2 + cc + k] = O[k];
+            }
         }
     }
 }
