@@ -25,9 +25,11 @@
 //            only on those rare steps;
 //   values : each lane accumulates its V slices weighted by the row's
 //            probability for every head in fp32.
-// At the end the row groups are summed with DPP adds, and the partial states
-// of the DPP rows of all wavefronts are merged through LDS with (max, sum,
-// output) rescaling.  With one split the normalised output is written
+// At the end each wavefront sums its row groups with DPP adds and its four
+// DPP rows with lane swaps (permlane32 / permlane16, in transposed form, so
+// every swap and add halves the registers to reduce), then as soon as its own
+// rows are done stores its state in LDS; the wavefronts' states are merged
+// with (max, sum, output) rescaling.  With one split the normalised output is written
 // directly; otherwise the split's state goes to the workspace and a merge
 // kernel combines the splits in a fixed order.  All reductions have a fixed
 // order, so results are deterministic.
@@ -139,9 +141,11 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     constexpr int STEPB = S::STEPB, SLOTB = S::SLOTB;
     constexpr int CPR = D / PER16;         // 16-byte vectors per row
     constexpr int NPART = WAVES * 4;       // partial states: the 4 DPP rows of every wavefront
-    constexpr int RINGB = WAVES * NS * SLOTB, MERGEB = NPART * HG * D * 4;
+    constexpr int RINGB = WAVES * NS * SLOTB;
     static_assert((NS - 1) * 2 * VPL <= 63, "loads in flight per wavefront");
-    __shared__ __attribute__((aligned(16))) char ring[RINGB > MERGEB ? RINGB : MERGEB];   // the merge reuses it
+    __shared__ __attribute__((aligned(16))) char ring[RINGB];
+    // a wavefront's partial outputs [HG][D] go to its own ring once its loads have drained
+    static_assert(NS * SLOTB >= HG * D * 4, "partial state fits a wavefront's ring");
     __shared__ int32_t pte[DEC_PT_CAP];
     __shared__ float m_s[WAVES][HG], l_s[NPART][HG];
 
@@ -317,7 +321,8 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
         wait_vmem<0>();     // the ring is reused below
     }
 
-    // sum the row groups within each 16-lane DPP row (m is wavefront-uniform)
+    // The wavefront's partial state.  First the row groups within each 16-lane
+    // DPP row are summed (m is wavefront-uniform) ...
 #pragma unroll
     for (int g = 0; g < HG; ++g) {
         l[g] = row_groups_sum<LPR>(l[g]);
@@ -326,42 +331,50 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
 #pragma unroll
             for (int e = 0; e < PER16; ++e) o[g][j][e] = row_groups_sum<LPR>(o[g][j][e]);
     }
-    __syncthreads();    // every wavefront is done with its ring
-
-    // The partial state of every DPP row (4 per wavefront) goes to LDS.  After
-    // the row-group sums the COP lanes of a row that hold the same slice hold
-    // the same values, so each writes a different EPC-element piece of it, and
-    // piece (j, cp, c) is stored at ((j * COP + cp) * LPR + c) * EPC of the
-    // head's D floats: the 16 lanes of a row store one contiguous run (no bank
-    // conflicts).
-    constexpr int COP = 16 / LPR, EPC = PER16 / COP;
-    float *o_s = reinterpret_cast<float *>(ring);       // [NPART][HG][D], pieces permuted as above
-    const int part = wave * 4 + lane / 16;
+    // ... then the four DPP rows, in transposed form: a swap of the wave halves
+    // (permlane32) and an add turn two values into one register holding one
+    // value's half-sums in lanes 0-31 and the other's in lanes 32-63; a swap of
+    // neighbouring rows (permlane16) and an add do the same again.  Afterwards
+    // register k of DPP row rho holds the wavefront's total of value
+    // 4 k + {0, 2, 1, 3}[rho] (value n = (g * VPL + j) * PER16 + e) for the
+    // row's slices.
+    constexpr int NV = HG * VPL * PER16, COP = 16 / LPR;
+    static_assert(NV % (4 * COP) == 0, "transposed reduction shape");
+    float s2[NV / 4];
     {
-        const int cp = (lane % 16) / LPR;
+        float s1[NV / 2];
 #pragma unroll
-        for (int g = 0; g < HG; ++g)
+        for (int i = 0; i < NV / 2; ++i) {
+            const int n0 = 2 * i, n1 = 2 * i + 1;
+            const float a0 = o[n0 / (VPL * PER16)][(n0 / PER16) % VPL][n0 % PER16];
+            const float a1 = o[n1 / (VPL * PER16)][(n1 / PER16) % VPL][n1 % PER16];
+            const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a0), __float_as_uint(a1), false, false);
+            s1[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+        }
 #pragma unroll
-            for (int j = 0; j < VPL; ++j) {
-                float v[EPC];
-#pragma unroll
-                for (int e = 0; e < EPC; ++e) {
-                    v[e] = o[g][j][e];
-#pragma unroll
-                    for (int x = 1; x < COP; ++x) v[e] = cp == x ? o[g][j][x * EPC + e] : v[e];
-                }
-                float *dst = o_s + (part * HG + g) * D + ((j * COP + cp) * LPR + c) * EPC;
-                if constexpr (EPC >= 4) {
-#pragma unroll
-                    for (int e = 0; e < EPC; e += 4)
-                        *reinterpret_cast<float4 *>(dst + e) = make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
-                } else if constexpr (EPC == 2) {
-                    *reinterpret_cast<float2 *>(dst) = make_float2(v[0], v[1]);
-                } else {
-                    dst[0] = v[0];
-                }
-            }
+        for (int k = 0; k < NV / 4; ++k) {
+            const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s1[2 * k]), __float_as_uint(s1[2 * k + 1]),
+                                                            false, false);
+            s2[k] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+        }
     }
+    // The COP lanes of a row holding the same slice split the registers; each
+    // store instruction then covers 64 consecutive floats of one head.  The
+    // state goes to the wavefront's own ring, whose loads have all landed.
+    {
+        const int rho = lane / 16, cp = (lane % 16) / LPR;
+        const int pr = rho == 1 ? 2 : (rho == 2 ? 1 : rho);
+#pragma unroll
+        for (int i = 0; i < NV / (4 * COP); ++i) {
+            float x = s2[i * COP];
+#pragma unroll
+            for (int q = 1; q < COP; ++q) x = cp == q ? s2[i * COP + q] : x;
+            const int n = 4 * (i * COP + cp) + pr;
+            const int g = n / (VPL * PER16), j = (n / PER16) % VPL, e = n % PER16;
+            reinterpret_cast<float *>(ring + wave * (NS * SLOTB))[g * D + (j * LPR + c) * PER16 + e] = x;
+        }
+    }
+    const int part = wave * 4 + lane / 16;
     if (lane % 16 == 0) {
 #pragma unroll
         for (int g = 0; g < HG; ++g) l_s[part][g] = l[g];
@@ -372,72 +385,70 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     }
     __syncthreads();    // partial states written
 
-    // Combine.  An item is a run of RW stored floats of one head (inside one
-    // piece, so RW consecutive output columns); SUB adjacent threads share an
-    // item, each rescaling and adding NPART / SUB of the partial states, and
-    // DPP adds combine them.
-    constexpr int RW = EPC < 4 ? EPC : 4;
-    constexpr int ITEMS = HG * D / RW, THREADS = 64 * WAVES;
-    constexpr int SUB = THREADS / ITEMS >= 4 ? 4 : (THREADS / ITEMS >= 2 ? 2 : 1);
-    constexpr int PPS = NPART / SUB;
+    // Combine.  An item is 4 consecutive output columns of one head; SUB
+    // adjacent threads share an item, each rescaling and adding WAVES / SUB of
+    // the wavefronts' states, and DPP adds combine them.
+    constexpr int ITEMS = HG * D / 4, THREADS = 64 * WAVES;
+    constexpr int SUB_T = THREADS / ITEMS >= 4 ? 4 : (THREADS / ITEMS >= 2 ? 2 : 1);
+    constexpr int SUB = SUB_T < WAVES ? SUB_T : WAVES;
+    constexpr int PW = WAVES / SUB;
+    static_assert(WAVES % SUB == 0, "combine split");
     const int sub = tid % SUB;
     for (int it = tid / SUB; it < ITEMS; it += THREADS / SUB) {     // uniform within a SUB group
-        const int g = it * RW / D, s0 = it * RW % D;
+        const int g = it * 4 / D, cc = it * 4 % D;
         float M = -INFINITY;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) M = fmaxf(M, m_s[w][g]);
-        float Lsum = 0.f, O[RW];
-#pragma unroll
-        for (int k = 0; k < RW; ++k) O[k] = 0.f;
+        float Lsum = 0.f;
+        float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
         if (M > -INFINITY) {
 #pragma unroll
-            for (int pp = 0; pp < PPS; ++pp) {
-                const int p = sub * PPS + pp, w = p / 4;
+            for (int wp = 0; wp < PW; ++wp) {
+                const int w = sub * PW + wp;
                 const float a = m_s[w][g] > -INFINITY ? __builtin_amdgcn_exp2f(m_s[w][g] - M) : 0.f;
-                const float *src = o_s + (p * HG + g) * D + s0;
-                float x[RW];
-                if constexpr (RW == 4) {
-                    const float4 y = *reinterpret_cast<const float4 *>(src);
-                    x[0] = y.x; x[1] = y.y; x[2] = y.z; x[3] = y.w;
-                } else {
-#pragma unroll
-                    for (int k = 0; k < RW; ++k) x[k] = src[k];
-                }
-                Lsum = fmaf(a, l_s[p][g], Lsum);
-#pragma unroll
-                for (int k = 0; k < RW; ++k) O[k] = fmaf(a, x[k], O[k]);
+                const float lw = (l_s[4 * w][g] + l_s[4 * w + 1][g]) + (l_s[4 * w + 2][g] + l_s[4 * w + 3][g]);
+                const float4 x = *reinterpret_cast<const float4 *>(ring + w * (NS * SLOTB) + (g * D + cc) * 4);
+                Lsum = fmaf(a, lw, Lsum);
+                O.x = fmaf(a, x.x, O.x);
+                O.y = fmaf(a, x.y, O.y);
+                O.z = fmaf(a, x.z, O.z);
+                O.w = fmaf(a, x.w, O.w);
             }
         }
         if constexpr (SUB >= 2) {
             Lsum += dpp<DPP_XOR1>(Lsum);
-#pragma unroll
-            for (int k = 0; k < RW; ++k) O[k] += dpp<DPP_XOR1>(O[k]);
+            O.x += dpp<DPP_XOR1>(O.x);
+            O.y += dpp<DPP_XOR1>(O.y);
+            O.z += dpp<DPP_XOR1>(O.z);
+            O.w += dpp<DPP_XOR1>(O.w);
         }
         if constexpr (SUB == 4) {
             Lsum += dpp<DPP_XOR2>(Lsum);
-#pragma unroll
-            for (int k = 0; k < RW; ++k) O[k] += dpp<DPP_XOR2>(O[k]);
+            O.x += dpp<DPP_XOR2>(O.x);
+            O.y += dpp<DPP_XOR2>(O.y);
+            O.z += dpp<DPP_XOR2>(O.z);
+            O.w += dpp<DPP_XOR2>(O.w);
         }
-        // output column of stored float s0: piece (j, cp, c), element e
-        const int piece = s0 / EPC, e = s0 % EPC;
-        const int cc = ((piece / (LPR * COP)) * LPR + piece % LPR) * PER16 + ((piece / LPR) % COP) * EPC + e;
         const int gl = (int)blockIdx.z * HG + g;       // head within the KV group
         if (sub == 0) {
             if (nsplit == 1) {
                 float *po = out + ((int64_t)b * Hq + gq0 + g) * D + cc;
                 const float inv = Lsum > 0.f ? 1.f / Lsum : 0.f;
-                if (RW == 4 && (reinterpret_cast<uintptr_t>(po) & 15u) == 0) {
-                    *reinterpret_cast<float4 *>(po) = make_float4(O[0] * inv, O[RW > 1 ? 1 : 0] * inv,
-                                                                  O[RW > 2 ? 2 : 0] * inv, O[RW > 3 ? 3 : 0] * inv);
+                if ((reinterpret_cast<uintptr_t>(po) & 15u) == 0) {
+                    *reinterpret_cast<float4 *>(po) = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
                 } else {
-#pragma unroll
-                    for (int k = 0; k < RW; ++k) po[k] = O[k] * inv;
+                    po[0] = O.x * inv;
+                    po[1] = O.y * inv;
+                    po[2] = O.z * inv;
+                    po[3] = O.w * inv;
                 }
             } else {
                 float *pp = part_ptr(ws, unit, nsplit, split, G, D) + (int64_t)gl * (D + 2);
                 if (cc == 0) { pp[0] = M; pp[1] = Lsum; }
-#pragma unroll
-                for (int k = 0; k < RW; ++k) pp[2 + cc + k] = O[k];
+                pp[2 + cc] = O.x;
+                pp[3 + cc] = O.y;
+                pp[4 + cc] = O.z;
+                pp[5 + cc] = O.w;
             }
         }
     }
