@@ -222,6 +222,13 @@ def _paged_set(g, B, Hkv, d, nmax, P, td, empty_some=True):
     ("bf16", 128, 4, 256, 16, 4),              # exactly one split
     ("bf16", 128, 4, 819, 16, 128),            # >= 256 units: one split, several tiles per wavefront
     ("bf16", 128, 8, 1700, 16, 128),
+    # every lane layout of the end-of-kernel reduction (lanes per row 4, 8, 16)
+    ("bf16", 64, 2, 700, 16, 3),
+    ("bf16", 64, 4, 333, 8, 2),
+    ("bf16", 128, 2, 900, 16, 130),
+    ("f32", 128, 8, 500, 16, 2),
+    ("f32", 64, 4, 611, 2, 3),
+    ("f32", 128, 4, 410, 16, 140),
 ])
 def test_decode_parity(gpu_lib, dtype, d, G, nmax, P, B):
     g = np.random.default_rng(nmax + G + d + P)
