@@ -214,6 +214,15 @@ def main():
     t_score_lse = per_launch(lambda i=0: sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score,
                                                      lse_in=lse_win))
 
+    # the on-box reference: a plain device-to-device copy of the decode step's
+    # byte count, over rotating buffers so that the last-level cache cannot serve it
+    copy_bytes = 2 * S * d * esize
+    copy_src = [torch.empty(copy_bytes, dtype=torch.uint8, device=dev).fill_(1) for _ in range(6)]
+    copy_dst = [torch.empty(copy_bytes, dtype=torch.uint8, device=dev) for _ in range(6)]
+    t_copy = min(per_launch(lambda i=0: copy_dst[i % 6].copy_(copy_src[(i + 3) % 6])) for _ in range(3))
+    copy_gbs = 2 * copy_bytes / (t_copy * 1e-3) / 1e9             # bytes read + written
+    del copy_src, copy_dst
+
     # block-granular proactive selection (eq. 1, eq. 2; M = 1024 blocks per
     # layer, transfer time 6.5x the prefill time), timed on its own
     blk = block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize)
@@ -257,11 +266,16 @@ def main():
                  "gbs": round((scores.numel() * 4 + idx.numel() * 4) / (t_topk * 1e-3) / 1e9, 1)},
         "pack": {"ms": round(t_pack, 4), "gbs": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9, 1),
                  "frac_hbm_peak": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                 "frac_measured_copy": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9 / copy_gbs, 4),
                  "mb_algorithmic": round(pack_bytes_alg / 1e6, 2)},
         "split": {"ms": round(t_split, 4)},
         "decode_attn": {"ms": round(t_dec, 4), "gbs": round(dec_gbs, 1),
                         "frac_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4),
+                        "frac_measured_copy": round(dec_gbs / copy_gbs, 4),
                         "mb_algorithmic": round(dec_bytes / 1e6, 2)},
+        "measured_copy": {"gbs": round(copy_gbs, 1), "ms": round(t_copy, 4), "mb": round(copy_bytes / 1e6, 2),
+                          "note": "device-to-device copy (bytes read + written) over six rotating buffer pairs; "
+                                  "the fractions named frac_measured_copy are against it"},
     }
     line = {
         "metric": "select+pack GB/s and sparse decode-attn tokens/s; % of MI355X HBM/MFMA peak",
@@ -285,7 +299,7 @@ def main():
         "roofline": {"kernel": "sg_decode_attn", "bound": "hbm", "achieved": round(dec_gbs, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(), "bytes_per_launch": dec_bytes,
-                     "avg_launch_ms": round(t_dec, 5)},
+                     "avg_launch_ms": round(t_dec, 5), "frac_measured_copy": round(dec_gbs / copy_gbs, 4)},
         "ops": ops,
         "setup_s": round(setup_s, 2),
     }
@@ -710,6 +724,17 @@ def cpu_baseline(cfg, pre, bud, layers, min_seconds):
     dt = (time.perf_counter() - t0) / reps
     esize = 2 if cfg.dtype == "bf16" else 4
     kv_bytes = 2 * units * pre["T"] * cfg.d * esize
+    # one thread on the first layer alone
+    oracle.set_threads(1)
+    try:
+        t1 = time.perf_counter()
+        s1 = oracle.score(q[:, :1], k[:1], pre["cu_seqlens"], cfg.Hkv)
+        i1 = oracle.topk(s1.astype(np.float32), pre["cu_seqlens"], bud["cu_k"])
+        oracle.pack(kraw[:1], vraw[:1], i1, pre["cu_seqlens"], bud["cu_k"])
+        dt1 = time.perf_counter() - t1
+    finally:
+        oracle.set_threads(threads)
+    kv1 = 2 * cfg.Hkv * pre["T"] * cfg.d * esize
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -723,7 +748,9 @@ def cpu_baseline(cfg, pre, bud, layers, min_seconds):
             "kind": "oracle", "seconds_per_pass": round(dt, 3), "passes": reps,
             "sample": f"score+topk+pack of layers 0..{layers - 1} ({units} of {cfg.L * cfg.Hkv} units), "
                       f"same request, fp64 C oracle with OpenMP over units, repeated {reps}x",
-            "cpu_model": cpu, "host": platform.node()}
+            "cpu_model": cpu, "host": platform.node(),
+            "single_thread": {"value": round(kv1 / dt1 / 1e9, 4), "unit": "GB/s", "seconds": round(dt1, 3),
+                              "sample": f"score+topk+pack of layer 0 ({cfg.Hkv} units), one thread"}}
 
 
 if __name__ == "__main__":
