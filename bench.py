@@ -223,6 +223,9 @@ def main():
     copy_gbs = 2 * copy_bytes / (t_copy * 1e-3) / 1e9             # bytes read + written
     del copy_src, copy_dst
 
+    # the decode step as a model runs it: one launch per layer, in a HIP graph
+    dec_layers = per_layer_mode(sg, qdec[0], pools[0][0], pools[0][1], page_table, n_rows, P)
+
     # block-granular proactive selection (eq. 1, eq. 2; M = 1024 blocks per
     # layer, transfer time 6.5x the prefill time), timed on its own
     blk = block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize)
@@ -273,6 +276,7 @@ def main():
                         "frac_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4),
                         "frac_measured_copy": round(dec_gbs / copy_gbs, 4),
                         "mb_algorithmic": round(dec_bytes / 1e6, 2)},
+        "decode_attn_per_layer": dec_layers,
         "measured_copy": {"gbs": round(copy_gbs, 1), "ms": round(t_copy, 4), "mb": round(copy_bytes / 1e6, 2),
                           "note": "device-to-device copy (bytes read + written) over six rotating buffer pairs; "
                                   "the fractions named frac_measured_copy are against it"},
@@ -693,6 +697,64 @@ def measured_traffic():
     if not h or not t or h.group(1) != sources_sha256(TRAFFIC_SOURCES):
         return None
     return int(t.group(1))
+
+
+def per_layer_mode(sg, q, k_pool, v_pool, page_table, n_rows, P, nrep=20):
+    """One decode step as a model runs it: one sg_decode_attn launch per layer
+    (B = 1, the layer's KV heads), the layers in order, captured once in a HIP
+    graph and replayed.  Every replay is checked bit for bit against the same
+    launches made eagerly (with eager work between the replays) before it is
+    timed."""
+    import torch
+    L, Hkv, npg = page_table.shape
+    Hq, d = q.shape[1], q.shape[2]
+    dev = q.device
+    ws = torch.zeros(max(sg.decode_workspace_size(1, Hq, Hkv, d, npg, P), 16), dtype=torch.uint8, device=dev)
+    out = torch.empty((L, Hq, d), device=dev)
+
+    def layers():
+        for l in range(L):
+            sg.sg_decode_attn(q[l:l + 1], k_pool, v_pool, page_table[l:l + 1], n_rows[l:l + 1], P, out[l:l + 1],
+                              ws=ws)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(nrep):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / nrep
+
+    layers()
+    torch.cuda.synchronize()
+    ref = out.clone()
+    t_eager = timed(layers)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        layers()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        layers()
+    for _ in range(3):
+        out.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), "graph replay differs from the eager launches"
+        layers()
+        torch.cuda.synchronize()
+    t_graph = timed(graph.replay)
+    graph.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref), "graph replay differs from the eager launches"
+    return {"launches": f"{L} sg_decode_attn calls per step, one per layer ({Hkv} KV heads, {Hq} q heads each)",
+            "graph_ms": round(t_graph, 4), "eager_ms": round(t_eager, 4),
+            "tokens_per_s_graph": round(1.0 / (t_graph * 1e-3), 1),
+            "note": "graph replays checked bit for bit against eager launches"}
 
 
 def cpu_baseline(cfg, pre, bud, layers, min_seconds):
