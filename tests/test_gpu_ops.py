@@ -250,6 +250,27 @@ def test_decode_parity(gpu_lib, dtype, d, G, nmax, P, B):
     np.testing.assert_allclose(o, ref, atol=tol, rtol=0)
 
 
+def test_decode_split_workspace_reused(gpu_lib):
+    """Few units split their rows over several workgroups and a merge combines
+    them through the workspace; one workspace serves call after call."""
+    say("decode split workspace reuse")
+    g = np.random.default_rng(77)
+    B, Hkv, G, d, nmax, P = 2, 2, 4, 128, 1500, 16
+    Hq = G * Hkv
+    n, pages, kp, vp = _paged_set(g, B, Hkv, d, nmax, P, torch.bfloat16, empty_some=False)
+    wsz = gpu_lib.decode_workspace_size(B, Hq, Hkv, d, pages.shape[-1], P)
+    assert wsz > 0                         # this shape splits
+    ws = torch.empty((wsz,), dtype=torch.uint8, device="cuda")
+    kd, vd, pd, nd = kp.cuda(), vp.cuda(), cu(pages), cu(n)
+    for call in range(3):
+        q = (torch.randn((B, Hq, d), generator=torch.Generator().manual_seed(100 + call)) * 2).to(torch.bfloat16)
+        out = torch.full((B, Hq, d), float("nan"), device="cuda")
+        gpu_lib.sg_decode_attn(q.cuda(), kd, vd, pd, nd, P, out, ws=ws)
+        torch.cuda.synchronize()
+        ref = oracle.decode_attn(f32(q), f32(kp), f32(vp), pages, n, P)
+        np.testing.assert_allclose(out.cpu().numpy(), ref, atol=2e-2, rtol=0)
+
+
 def test_decode_invalid_pages_are_skipped(gpu_lib):
     say("decode invalid pages")
     d, P = 128, 16
