@@ -25,7 +25,7 @@
  *                   (Section 2.3, Section 5.1)
  *   sg_fetch_keep   on-demand fetch that keeps fetched rows in the decode
  *                   side's store and marks them local (reuse, Section 4.2)
- *   sg_spec_quota, sg_spec_push
+ *   sg_spec_quota, sg_spec_push, sg_spec_commit
  *                   speculative transfer of the remaining KV blocks in
  *                   importance order (Section 4.3)
  *
@@ -394,7 +394,8 @@ int sg_decode_select(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, i
  *   (L - 1) * src_layer_rows + Hkv * T rows (a stride of 0 shares one source
  *   across layers); k_dst, v_dst: device (the decode side's store), at least
  *   (L - 1) * dst_layer_rows + Hkv * T rows; ids device int32 [nblk]; mask
- *   device int8 [L][Hkv][T]; rem device float [L M] or NULL.  Requires
+ *   device int8 [L][Hkv][T] or NULL (rows only: no mask or rem update; see
+ *   sg_spec_commit); rem device float [L M] or NULL.  Requires
  *   s0 + N <= T and N > 0 when nblk > 0.  Store rows, mask and rem become
  *   visible to work ordered after the call (stream order or an event).
  */
@@ -402,6 +403,22 @@ int64_t sg_spec_quota(int64_t blocks, int ratio_bp);
 int sg_spec_push(void *stream, sg_dtype dt, int L, int Hkv, int d, int64_t T, int64_t s0, int64_t N, int M,
                  const void *k_src, const void *v_src, int64_t src_layer_rows, void *k_dst, void *v_dst,
                  int64_t dst_layer_rows, int nblk, const int32_t *ids, int8_t *mask, float *rem);
+
+/* sg_spec_commit: the marking half of sg_spec_push on its own.  For every
+ *   delivered block id c = l * M + m in ids[0 .. nblk), every KV head h and
+ *   block token t = m * Nb + r < N: mask[(l * Hkv + h) * T + s0 + t] = 1, and
+ *   rem[c] = NaN when rem is not NULL; other ids are skipped.
+ *   The paper's transfer puts a block's rows before its mask update with
+ *   in-order delivery (Section 4.3).  Here a push without a mask
+ *   (sg_spec_push with mask = NULL moves the rows only, on a side stream)
+ *   lets the decode steps go on; once the push has completed, the consumer
+ *   enqueues sg_spec_commit on its own stream, ordered after the push (an
+ *   event), so no step reads a local entry whose row has not landed.
+ *   ids device int32 [nblk]; mask device int8 [L][Hkv][T]; rem device float
+ *   [L M] or NULL.  Requires s0 + N <= T and N > 0 when nblk > 0.
+ */
+int sg_spec_commit(void *stream, int L, int Hkv, int64_t T, int64_t s0, int64_t N, int M, int nblk,
+                   const int32_t *ids, int8_t *mask, float *rem);
 
 #ifdef __cplusplus
 }

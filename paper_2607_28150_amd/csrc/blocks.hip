@@ -13,7 +13,9 @@
 //   the copy runs like a plain strided memcpy.
 // sg_spec_push (speculative transfer, Section 4.3): the same flat copy, with
 //   each row stored at its own position in the decode side's store, its mask
-//   entry turned local and the block marked in the remaining importances.
+//   entry turned local and the block marked in the remaining importances
+//   (or, without a mask, the rows alone; sg_spec_commit then does the marking
+//   on the consumer's stream once the rows have landed).
 #include <math.h>
 
 #include "sg_internal.h"
@@ -118,10 +120,10 @@ __global__ __launch_bounds__(BLK_THREADS) void pack_blocks_kernel(int L, int Hkv
 
 // Speculative push: the grid is flat over 16-byte vectors of the pushed rows
 // like the block pack, but every row goes back to its own position in the
-// decode side's store; the lane holding vector 0 of a row turns its mask entry
-// local, and the first lane of a block takes the block out of the remaining
-// importances.
-template <int CPR>
+// decode side's store; with MARK the lane holding vector 0 of a row turns its
+// mask entry local, and the first lane of a block takes the block out of the
+// remaining importances.
+template <int CPR, bool MARK>
 __global__ __launch_bounds__(BLK_THREADS) void spec_push_kernel(int L, int Hkv, int64_t T, int64_t s0, int64_t N,
                                                                   int M, int64_t Nb, const v4u *__restrict__ k,
                                                                   const v4u *__restrict__ v, int64_t src_layer_rows,
@@ -163,9 +165,33 @@ __global__ __launch_bounds__(BLK_THREADS) void spec_push_kernel(int L, int Hkv, 
                 __builtin_nontemporal_store(kr[u], kd + row_dst[u]);
                 __builtin_nontemporal_store(vr[u], vd + row_dst[u]);
             }
-            if (mpos[u] >= 0) mask[mpos[u]] = 1;
-            if (rem && lead[u] >= 0) rem[lead[u]] = __builtin_nanf("");
+            if constexpr (MARK) {
+                if (mpos[u] >= 0) mask[mpos[u]] = 1;
+                if (rem && lead[u] >= 0) rem[lead[u]] = __builtin_nanf("");
+            }
         }
+    }
+}
+
+// Commit of delivered blocks: one thread per (block, KV head, block token)
+// turns the mask entry local; the block's first thread takes it out of the
+// remaining importances.
+__global__ __launch_bounds__(BLK_THREADS) void spec_commit_kernel(int L, int Hkv, int64_t T, int64_t s0, int64_t N,
+                                                                    int M, int64_t Nb, int nblk,
+                                                                    const int32_t *__restrict__ ids,
+                                                                    int8_t *__restrict__ mask,
+                                                                    float *__restrict__ rem) {
+    const int64_t total = (int64_t)nblk * Hkv * Nb;
+    for (int64_t i = (int64_t)blockIdx.x * BLK_THREADS + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * BLK_THREADS) {
+        const int64_t r = i % Nb, sh = i / Nb;
+        const int h = (int)(sh % Hkv), s = (int)(sh / Hkv);
+        const int32_t id = ids[s];
+        if (id < 0 || (int64_t)id >= (int64_t)L * M) continue;
+        const int l = id / M, m = id % M;
+        const int64_t t = (int64_t)m * Nb + r;
+        if (t < N) mask[((int64_t)l * Hkv + h) * T + s0 + t] = 1;
+        if (rem && h == 0 && r == 0) rem[id] = __builtin_nanf("");
     }
 }
 
@@ -258,7 +284,7 @@ extern "C" int sg_spec_push(void *stream, sg_dtype dt, int L, int Hkv, int d, in
                "sg_spec_push: the request's tokens [s0, s0 + N) must lie in [0, T)");
     SG_REQUIRE(src_layer_rows >= 0 && dst_layer_rows >= 0, SG_EINVAL, "sg_spec_push: negative layer stride");
     if (nblk == 0) return SG_OK;
-    SG_REQUIRE(k_src && v_src && k_dst && v_dst && ids && mask, SG_EINVAL, "sg_spec_push: null pointer");
+    SG_REQUIRE(k_src && v_src && k_dst && v_dst && ids, SG_EINVAL, "sg_spec_push: null pointer");
     SG_REQUIRE(aligned16(k_src) && aligned16(v_src) && aligned16(k_dst) && aligned16(v_dst), SG_EINVAL,
                "sg_spec_push: row arrays must be 16-byte aligned");
     SG_REQUIRE(N > 0, SG_EINVAL, "sg_spec_push: blocks of an empty request");
@@ -273,10 +299,35 @@ extern "C" int sg_spec_push(void *stream, sg_dtype dt, int L, int Hkv, int d, in
     auto kd = reinterpret_cast<v4u *>(k_dst);
     auto vd = reinterpret_cast<v4u *>(v_dst);
     switch (cpr) {
-        case 8: spec_push_kernel<8><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem); break;
-        case 16: spec_push_kernel<16><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem); break;
-        case 32: spec_push_kernel<32><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem); break;
+        case 8:
+            if (mask) spec_push_kernel<8, true><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem);
+            else spec_push_kernel<8, false><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, nullptr, nullptr);
+            break;
+        case 16:
+            if (mask) spec_push_kernel<16, true><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem);
+            else spec_push_kernel<16, false><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, nullptr, nullptr);
+            break;
+        case 32:
+            if (mask) spec_push_kernel<32, true><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, mask, rem);
+            else spec_push_kernel<32, false><<<(unsigned)grid, BLK_THREADS, 0, s>>>(L, Hkv, T, s0, N, M, Nb, ks, vs, src_layer_rows, kd, vd, dst_layer_rows, nblk, ids, nullptr, nullptr);
+            break;
         default: set_error("sg_spec_push: internal row size"); return SG_EINTERNAL;
     }
     return launch_status("sg_spec_push");
+}
+
+extern "C" int sg_spec_commit(void *stream, int L, int Hkv, int64_t T, int64_t s0, int64_t N, int M, int nblk,
+                              const int32_t *ids, int8_t *mask, float *rem) {
+    SG_REQUIRE(L >= 1 && Hkv >= 1 && M >= 1, SG_EINVAL, "sg_spec_commit: L, Hkv, M must be >= 1");
+    SG_REQUIRE(T >= 0 && s0 >= 0 && N >= 0 && s0 + N <= T && nblk >= 0, SG_EINVAL,
+               "sg_spec_commit: the request's tokens [s0, s0 + N) must lie in [0, T)");
+    if (nblk == 0) return SG_OK;
+    SG_REQUIRE(ids && mask, SG_EINVAL, "sg_spec_commit: null pointer");
+    SG_REQUIRE(N > 0, SG_EINVAL, "sg_spec_commit: blocks of an empty request");
+    const int64_t Nb = (N + M - 1) / M;
+    const int64_t total = (int64_t)nblk * Hkv * Nb;
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, BLK_THREADS), 65536));
+    spec_commit_kernel<<<(unsigned)grid, BLK_THREADS, 0, as_stream(stream)>>>(L, Hkv, T, s0, N, M, Nb, nblk, ids, mask,
+                                                                               rem);
+    return launch_status("sg_spec_commit");
 }

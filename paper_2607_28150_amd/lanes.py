@@ -1,4 +1,5 @@
-"""Parallel on-demand transfer on one GPU (Section 4.2): stream plumbing only.
+"""Parallel on-demand transfer (Section 4.2) and speculative transfer (Section
+4.3) on one GPU: stream plumbing only.
 
 After Algorithm 1 splits a step's KV index (sg_split, remote entries first), two
 lanes fill the decode pool at once:
@@ -8,8 +9,14 @@ lanes fill the decode pool at once:
     remote entries from the prefill side's copy into pool rows [0, n_remote),
     and with reuse keeps them in the store and marks them local.
 Each lane runs on its own stream; the caller's stream waits for both, so the
-attention that follows on it sees the whole pool.  Every copy runs in the
-library's kernels; this module only orders them.
+attention that follows on it sees the whole pool.
+
+SpecPusher sends the blocks that the proactive transfer left behind, a quota at
+a time in importance order, on a side stream, without holding up any decode
+step: a push moves rows only (sg_spec_push without a mask), and once its
+completion event has fired, the next step boundary enqueues the marking
+(sg_spec_commit) on the caller's stream, ordered after the rows.  Every copy
+runs in the library's kernels; this module only orders them.
 """
 from __future__ import annotations
 
@@ -76,3 +83,68 @@ class TwoLane:
         main.wait_event(done_l)
         main.wait_event(done_r)
         return buf.n_kept
+
+
+class SpecPusher:
+    """Speculative transfer of one request's remaining blocks (Section 4.3).
+
+    ``imp`` is the request's L * M block importances (eq. 1).  At most one
+    push is in flight; each step calls ``commit_if_landed`` before its split
+    and ``launch_if_idle`` after its lanes.  Neither waits: a push that has
+    not landed is committed at a later step."""
+
+    def __init__(self, src_k, src_v, imp, s0, N, M, store_k, store_v, mask, quota, L=None, device=None):
+        self.src_k, self.src_v = src_k, src_v
+        self.store_k, self.store_v, self.mask = store_k, store_v, mask
+        self.s0, self.N, self.M = int(s0), int(N), int(M)
+        self.L = store_k.shape[0] if L is None else L
+        self.Hkv, self.T = store_k.shape[1], store_k.shape[2]
+        self.LM = self.L * self.M
+        self.rem = imp.reshape(-1)[: self.LM].clone()
+        self.quota = int(quota)
+        self.left = self.LM
+        self.pushes = 0
+        dev = imp.device
+        self.ids = torch.empty(max(1, self.quota), dtype=torch.int32, device=dev)
+        self.cu_row = torch.tensor([0, self.LM], dtype=torch.int32, device=dev)
+        self.cu_q = {q: torch.tensor([0, q], dtype=torch.int32, device=dev)
+                     for q in {self.quota, self.LM % self.quota or self.quota}}
+        self.stream = torch.cuda.Stream(device=device)
+        self.inflight = None        # (block count, completion event)
+
+    def commit_if_landed(self, stream):
+        """Marks the in-flight push's blocks on `stream` if its rows have landed."""
+        if self.inflight is None or not self.inflight[1].query():
+            return False
+        q, done = self.inflight
+        stream.wait_event(done)
+        sg.sg_spec_commit(self.ids[:q], self.L, self.Hkv, self.T, self.s0, self.N, self.M, self.mask, self.rem,
+                          stream=stream)
+        self.inflight = None
+        return True
+
+    def launch_if_idle(self, stream):
+        """Chooses the next quota of blocks on `stream` and pushes their rows on
+        the side stream, if no push is in flight and blocks are left."""
+        if self.inflight is not None or self.left == 0:
+            return False
+        q = min(self.quota, self.left)
+        sg.sg_topk(self.rem.view(1, 1, self.LM), self.cu_row, self.LM, self.LM, self.cu_q[q], q,
+                   self.ids[:q].view(1, 1, q), stream=stream)
+        chosen = torch.cuda.Event()
+        chosen.record(stream)
+        self.stream.wait_event(chosen)
+        sg.sg_spec_push(self.src_k, self.src_v, self.ids[:q], self.s0, self.N, self.M, self.store_k, self.store_v,
+                        None, None, L=self.L, stream=self.stream)
+        done = torch.cuda.Event()
+        done.record(self.stream)
+        self.inflight = (q, done)
+        self.left -= q
+        self.pushes += 1
+        return True
+
+    def drain(self, stream):
+        """Waits on `stream` for the in-flight push and commits it."""
+        if self.inflight is not None:
+            self.inflight[1].synchronize()
+            self.commit_if_landed(stream)

@@ -28,7 +28,7 @@ EXPORTS = [
     "sg_fetch",
     "sg_decode_attn_workspace_size", "sg_decode_attn",
     "sg_block_importance", "sg_block_budget", "sg_pack_blocks_bytes", "sg_pack_blocks",
-    "sg_fetch_keep", "sg_spec_quota", "sg_spec_push", "sg_score_count",
+    "sg_fetch_keep", "sg_spec_quota", "sg_spec_push", "sg_spec_commit", "sg_score_count",
     "sg_decode_select_workspace_size", "sg_decode_select",
 ]
 
@@ -83,8 +83,10 @@ def load() -> ctypes.CDLL:
     lib.sg_spec_quota.argtypes = [_l, _i]
     lib.sg_spec_quota.restype = _l
     lib.sg_spec_push.argtypes = [_vp, _i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _vp, _vp, _l, _i, _vp, _vp, _vp]
+    lib.sg_spec_commit.argtypes = [_vp, _i, _i, _l, _l, _l, _i, _i, _vp, _vp, _vp]
     for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn", "sg_block_importance",
-              "sg_pack_blocks", "sg_fetch_keep", "sg_spec_push", "sg_score_count", "sg_decode_select"):
+              "sg_pack_blocks", "sg_fetch_keep", "sg_spec_push", "sg_spec_commit", "sg_score_count",
+              "sg_decode_select"):
         getattr(lib, f).restype = _i
     _lib = lib
     return lib
@@ -380,7 +382,9 @@ class DecodeCall:
         self._geom = (int(page_size), int(page_table.shape[2]))
         self._ws = _ptr(ws)
         self._wsb = 0 if ws is None else ws.numel() * ws.element_size()
-        self._stream = _stream(stream)
+        # a stream given here is kept; otherwise each call launches on torch's
+        # current stream at the time of the call (graph capture, stream contexts)
+        self._stream = None if stream is None else _stream(stream)
         self._pool_rows = k_pool.numel() // d
         self._numel = (q.numel(), k_pool.numel(), out.numel())
 
@@ -388,7 +392,8 @@ class DecodeCall:
         _need(q.numel() == self._numel[0] and k_pool.numel() == self._numel[1] and out.numel() == self._numel[2]
               and v_pool.numel() == self._numel[1], "prepared decode call used with other shapes")
         B, Hq, Hkv, d = self._shape
-        rc = self._lib.sg_decode_attn(self._stream, self._dt, B, Hq, Hkv, d, self._scale, q.data_ptr(),
+        st = self._stream if self._stream is not None else _stream(None)
+        rc = self._lib.sg_decode_attn(st, self._dt, B, Hq, Hkv, d, self._scale, q.data_ptr(),
                                       k_pool.data_ptr(), v_pool.data_ptr(), self._pool_rows, self._pt, self._nr,
                                       self._geom[0], self._geom[1], out.data_ptr(), self._ws, self._wsb)
         _check("sg_decode_attn", rc)
@@ -453,15 +458,16 @@ def sg_spec_push(k_src, v_src, ids, s0, N, M, k_dst, v_dst, mask, rem=None, L=No
                  dst_layer_rows=None, stream=None):
     """Delivers the blocks `ids` of one request from k_src / v_src [Lkv][Hkv][T][d]
     (device or pinned host) into the store k_dst / v_dst [L][Hkv][T][d] at the same
-    rows, turns their mask [L][Hkv][T] entries local and their rem [L*M] entries NaN."""
+    rows, turns their mask [L][Hkv][T] entries local and their rem [L*M] entries NaN
+    (mask=None: the rows only; sg_spec_commit marks them later)."""
     _need(k_src.dtype == v_src.dtype == k_dst.dtype == v_dst.dtype, "k/v source and store dtypes differ")
-    _need(ids.dtype == torch.int32 and mask.dtype == torch.int8, "ids must be int32 and mask int8")
+    _need(ids.dtype == torch.int32, "ids must be int32")
     Lkv, Hkv, T, d = k_src.shape
     Ld = k_dst.shape[0]
     if L is None:
         L = Ld
     _need(tuple(k_dst.shape[1:]) == (Hkv, T, d) and v_dst.shape == k_dst.shape, "store must be [L][Hkv][T][d]")
-    _need(mask.numel() >= L * Hkv * T, "mask must be int8 [L][Hkv][T]")
+    _need(mask is None or (mask.dtype == torch.int8 and mask.numel() >= L * Hkv * T), "mask must be int8 [L][Hkv][T]")
     _need(rem is None or (rem.dtype == torch.float32), "rem must be float32 [L*M]")
     if src_layer_rows is None:
         src_layer_rows = 0 if (Lkv == 1 and L > 1) else Hkv * T
@@ -471,3 +477,14 @@ def sg_spec_push(k_src, v_src, ids, s0, N, M, k_dst, v_dst, mask, rem=None, L=No
                              _ptr(k_src), _ptr(v_src), int(src_layer_rows), _ptr(k_dst), _ptr(v_dst),
                              int(dst_layer_rows), ids.numel(), _ptr(ids), _ptr(mask), _ptr(rem))
     _check("sg_spec_push", rc)
+
+
+def sg_spec_commit(ids, L, Hkv, T, s0, N, M, mask, rem=None, stream=None):
+    """Marks the delivered blocks `ids` of one request: mask [L][Hkv][T] entries
+    local, rem [L*M] entries NaN (the marking half of sg_spec_push)."""
+    _need(ids.dtype == torch.int32 and mask.dtype == torch.int8, "ids must be int32 and mask int8")
+    _need(mask.numel() >= L * Hkv * T, "mask must be int8 [L][Hkv][T]")
+    _need(rem is None or (rem.dtype == torch.float32 and rem.numel() >= L * M), "rem must be float32 [L*M]")
+    rc = load().sg_spec_commit(_stream(stream), int(L), int(Hkv), int(T), int(s0), int(N), int(M), ids.numel(),
+                               _ptr(ids), _ptr(mask), _ptr(rem))
+    _check("sg_spec_commit", rc)

@@ -180,3 +180,95 @@ def test_split_reports_kept_rows(gpu_lib):
     np.testing.assert_array_equal(cnt[0].cpu().numpy(), nl)
     np.testing.assert_array_equal(cnt[1].cpu().numpy(), nr)
     np.testing.assert_array_equal(cnt[2].cpu().numpy(), nl + nr)
+
+
+@pytest.mark.parametrize("dtype,d,lens,M,b,pinned", [
+    ("bf16", 128, (8192,), 1024, 0, True),
+    ("f32", 64, (1000, 37), 7, 1, False),
+])
+def test_spec_push_rows_then_commit(gpu_lib, dtype, d, lens, M, b, pinned):
+    """A push without a mask moves the rows only (mask and remaining row
+    untouched); sg_spec_commit afterwards leaves the same state as the
+    oracle's push of rows and marks together."""
+    L, Hkv = 3, 2
+    say("spec push rows then commit", dtype, d, lens, M, b, pinned)
+    g = np.random.default_rng(3 * d + M)
+    cus = np.concatenate([[0], np.cumsum(lens)])
+    T, s0, N = int(cus[-1]), int(cus[b]), lens[b]
+    k = _rows((L, Hkv, T, d), dtype, g)
+    v = _rows((L, Hkv, T, d), dtype, g)
+    kd0 = _rows((L, Hkv, T, d), dtype, g)
+    vd0 = _rows((L, Hkv, T, d), dtype, g)
+    mask0 = g.integers(0, 3, (L, Hkv, T)).astype(np.int8)
+    rem0 = g.standard_normal(L * M).astype(np.float32)
+    ids = g.choice(L * M, size=min(L * M, 29), replace=False).astype(np.int32)
+    ids[3] = -1                                                  # invalid: skipped
+    src_k = k.pin_memory() if pinned else k.cuda()
+    src_v = v.pin_memory() if pinned else v.cuda()
+    kd, vd = kd0.cuda(), vd0.cuda()
+    mask = torch.from_numpy(mask0).cuda()
+    rem = torch.from_numpy(rem0).cuda()
+    ids_d = cu(ids)
+    gpu_lib.sg_spec_push(src_k, src_v, ids_d, s0, N, M, kd, vd, None, None, L=L)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(mask.cpu().numpy(), mask0)
+    np.testing.assert_array_equal(rem.cpu().numpy(), rem0)
+    gpu_lib.sg_spec_commit(ids_d, L, Hkv, T, s0, N, M, mask, rem)
+    torch.cuda.synchronize()
+    okd, ovd, omask, orem = raw(kd0), raw(vd0), mask0.copy(), rem0.copy()
+    oracle.spec_push(raw(k), raw(v), ids, s0, N, M, okd, ovd, omask, orem, L=L)
+    np.testing.assert_array_equal(raw(kd), okd)
+    np.testing.assert_array_equal(raw(vd), ovd)
+    np.testing.assert_array_equal(mask.cpu().numpy(), omask)
+    got = rem.cpu().numpy()
+    np.testing.assert_array_equal(np.isnan(got), np.isnan(orem))
+    np.testing.assert_array_equal(got[~np.isnan(orem)], orem[~np.isnan(orem)])
+
+
+def test_spec_pusher_schedule(gpu_lib):
+    """The pusher (one push in flight, committed at a later step boundary)
+    delivers every block in importance order: after each commit the remaining
+    row and the mask equal the oracle's after the same number of transfers,
+    and the store ends equal to the source."""
+    from paper_2607_28150_amd.lanes import SpecPusher
+    L, Hkv, d, N, M = 4, 2, 64, 1000, 50
+    LM = L * M
+    say("spec pusher schedule", L, Hkv, d, N, M)
+    g = np.random.default_rng(5)
+    imp = (g.standard_normal(LM) ** 2).astype(np.float32)
+    imp[:M] = np.inf
+    imp[100:140] = np.float32(0.25)                              # ties
+    k = _rows((L, Hkv, N, d), "bf16", g)
+    v = _rows((L, Hkv, N, d), "bf16", g)
+    src_k, src_v = k.pin_memory(), v.pin_memory()
+    kd = torch.zeros((L, Hkv, N, d), dtype=torch.bfloat16, device="cuda")
+    vd = torch.zeros_like(kd)
+    mask = torch.full((L, Hkv, N), 2, dtype=torch.int8, device="cuda")
+    quota = oracle.spec_quota(LM, 1500)
+    main = torch.cuda.current_stream()
+    p = SpecPusher(src_k, src_v, torch.from_numpy(imp).cuda(), 0, N, M, kd, vd, mask, quota)
+    okd = np.zeros(raw(kd).shape, np.uint16)
+    ovd = np.zeros_like(okd)
+    omask = np.full((L, Hkv, N), 2, np.int8)
+    orem = imp.copy()
+    commits = 0
+    for _ in range(4 * LM):
+        if p.commit_if_landed(main):
+            commits += 1
+            q = min(quota, LM - quota * (commits - 1))
+            ids = oracle.topk(np.where(np.isnan(orem), np.float32(np.nan), orem)[None, None], [0, LM], [0, q])[0, 0]
+            oracle.spec_push(raw(k), raw(v), ids, 0, N, M, okd, ovd, omask, orem, L=L)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(mask.cpu().numpy(), omask)
+            got = p.rem.cpu().numpy()
+            np.testing.assert_array_equal(np.isnan(got), np.isnan(orem))
+        p.launch_if_idle(main)
+        if p.left == 0 and p.inflight is None:
+            break
+        torch.cuda.synchronize()
+    p.drain(main)
+    torch.cuda.synchronize()
+    assert p.pushes == -(-LM // quota)
+    np.testing.assert_array_equal(raw(kd), raw(k))
+    np.testing.assert_array_equal(raw(vd), raw(v))
+    assert (mask.cpu().numpy() == 1).all()
