@@ -118,7 +118,7 @@ extern "C" int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,
     SG_REQUIRE(kv_layer_rows >= 0, SG_EINVAL, "sg_pack: negative layer stride");
     const size_t need = sg_pack_bytes(dt, L, Hkv, d, K_total);
     SG_REQUIRE(dst_bytes >= need, SG_EWORKSPACE, "sg_pack: destination holds %zu bytes, needs %zu", dst_bytes, need);
-    if (K_total == 0 || max_k == 0) return SG_OK;
+    if (K_total == 0) return SG_OK;
     SG_REQUIRE(cu_seqlens && cu_k && k && v && idx && dst, SG_EINVAL, "sg_pack: null pointer");
     SG_REQUIRE(aligned16(k) && aligned16(v) && aligned16(dst), SG_EINVAL, "sg_pack: k, v and dst must be 16-byte aligned");
     const int rowb = d * esize_of(dt);
@@ -129,7 +129,8 @@ extern "C" int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,
     int32_t *di = reinterpret_cast<int32_t *>(dv + S * cpr);
     const int rows_per_block = (PACK_THREADS / cpr) * PACK_UNROLL;
     const int64_t units = (int64_t)L * Hkv * B;
-    const int64_t nchunk = std::min<int64_t>(ceil_div(max_k, rows_per_block), 65535);
+    // the kernel's chunks stride over every k_b, so a bound of 0 still covers them
+    const int64_t nchunk = std::min<int64_t>(std::max<int64_t>(1, ceil_div(max_k, rows_per_block)), 65535);
     SG_REQUIRE(units * nchunk <= 0x7fffffff, SG_EINVAL, "sg_pack: too many units");
     const dim3 grid((unsigned)(units * nchunk));
     hipStream_t s = as_stream(stream);

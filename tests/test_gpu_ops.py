@@ -42,6 +42,23 @@ def test_pack_bit_exact(gpu_lib, dtype, d, lens, ks):
     assert np.array_equal(dst.cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("max_k", [0, 1])
+def test_pack_small_launch_bound_covers_every_row(gpu_lib, max_k):
+    """max_k only sizes the launch: a bound of 0 or 1 still packs every k_b."""
+    cfg = _cfg(dtype="bf16", d=128, seqlens=(900, 300), B=2, W=4)
+    say("pack launch bound", max_k)
+    pre = inputs.make_prefill(cfg, device="cuda")
+    ks = (300, 40)
+    cuk = inputs.cu_from_lengths(ks)
+    idx = inputs.random_selection(cfg, [900, 300], list(ks), device="cuda")
+    nbytes = gpu_lib.pack_bytes(pre["k"].dtype, cfg.L, cfg.Hkv, 128, cuk[-1])
+    dst = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device="cuda")
+    gpu_lib.sg_pack(pre["k"], pre["v"], idx, cu(pre["cu_seqlens"]), pre["T"], cu(cuk), cuk[-1], max_k, dst)
+    torch.cuda.synchronize()
+    ref = oracle.pack(raw(pre["k"]), raw(pre["v"]), raw(idx), pre["cu_seqlens"], cuk)
+    assert np.array_equal(dst.cpu().numpy(), ref)
+
+
 def test_pack_to_pinned_host_and_full_selection(gpu_lib):
     cfg = _cfg(seqlens=(333,), L=1, W=4)
     say("pack pinned host full selection")
