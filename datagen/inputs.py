@@ -182,3 +182,53 @@ def extras_for_step(cfg: Config, step: int, lens, sel_layer: torch.Tensor, cu_k,
             pick = torch.argsort(r, stable=True)[:e]
             out.append(torch.sort(pick).values)
     return out
+
+
+def extras_layer(cfg: Config, step: int, lens, sel_layer: torch.Tensor, cu_k, layer: int):
+    """The same draws as ``extras_for_step`` for one layer, for every (KV head,
+    request) at once (one sort per layer instead of one per unit).
+
+    Returns (ids, cu_e): ids int32 [Hkv][E_total] with request b's ascending
+    ids at columns cu_e[b] .. cu_e[b + 1] of every head row, E_total = sum of
+    floor(N_b * extra_bp / 10000).
+    """
+    ids, cu_e = extras_layers(cfg, step, lens, sel_layer[None], cu_k, [layer])
+    return ids[0], cu_e
+
+
+def extras_layers(cfg: Config, step: int, lens, sel: torch.Tensor, cu_k, layers):
+    """``extras_layer`` for several layers at once: sel [len(layers)][Hkv][K_total]
+    holds each listed layer's selection; returns ids int32
+    [len(layers)][Hkv][E_total] and cu_e."""
+    device = sel.device
+    B, H, nl = len(lens), cfg.Hkv, len(layers)
+    R = nl * H                                                    # rows (layer, head)
+    cu = cu_from_lengths(lens)
+    T = cu[-1]
+    ecount = [extras_count(n, cfg.extra_bp) for n in lens]
+    cu_e = cu_from_lengths(ecount)
+    big = torch.iinfo(torch.int64).max
+    lens_t = torch.tensor(lens, dtype=torch.int64, device=device)
+    cu_t = torch.tensor(cu[:-1], dtype=torch.int64, device=device)
+    keys = torch.tensor([[rng._s64(rng.stream_key(cfg.seed, TAG_EXTRA, step, b, layer, h)) for b in range(B)]
+                         for layer in layers for h in range(H)], dtype=torch.int64, device=device)   # [R][B]
+    seg_b = torch.repeat_interleave(torch.arange(B, device=device), lens_t)             # token -> request
+    local = torch.arange(T, dtype=torch.int64, device=device) - cu_t[seg_b]
+    # element i of stream `key` is mix64(i * gamma + key), as in rng.raw64
+    r = rng.mix64(local[None, :] * rng._s64(rng._GAMMA) + keys[:, seg_b]) & big          # [R][T]
+    ks = torch.tensor([cu_k[b + 1] - cu_k[b] for b in range(B)], dtype=torch.int64, device=device)
+    sel_tok = sel.reshape(R, -1).to(torch.int64) + cu_t[torch.repeat_interleave(torch.arange(B, device=device), ks)]
+    r.scatter_(1, sel_tok, big)
+    flat = r.reshape(-1)
+    seg = (torch.arange(R, device=device)[:, None] * B + seg_b[None, :]).reshape(-1)
+    o1 = torch.argsort(flat, stable=True)                     # by key, ties by position
+    o2 = torch.argsort(seg[o1], stable=True)                  # grouped by (row, request), key order kept
+    order = o1[o2]                                            # segment (row i, request b) starts at i * T + cu[b]
+    es = torch.tensor(ecount, dtype=torch.int64, device=device)
+    e_seg = torch.repeat_interleave(torch.arange(B, device=device), es)                 # pick -> request
+    j = torch.arange(int(cu_e[-1]), dtype=torch.int64, device=device) - torch.tensor(cu_e[:-1], dtype=torch.int64,
+                                                                                      device=device)[e_seg]
+    start = torch.arange(R, device=device)[:, None] * T + cu_t[e_seg][None, :]             # [R][E_total]
+    picks = order[start + j[None, :]]
+    picks = torch.sort(picks.reshape(-1)).values.view(R, -1)  # segments are disjoint increasing ranges
+    return (picks - start).to(torch.int32).view(nl, H, -1), cu_e

@@ -81,3 +81,32 @@ def test_extras_avoid_selection():
         s = set(sel[0, h].tolist())
         e = ex[h].tolist()
         assert len(e) == 50 and len(set(e)) == 50 and not (s & set(e))
+
+
+def test_extras_layer_matches_per_unit_draws():
+    cfg = datagen.get("batched64").with_(B=4, L=2, varlen_lo=300, varlen_hi=900, extra_bp=700)
+    lens = inputs.seqlens(cfg)
+    b = inputs.make_budget(cfg, lens)
+    sel = inputs.random_selection(cfg, lens, b["k"])
+    for layer in range(cfg.L):
+        for step in (0, 5):
+            ids, cu_e = inputs.extras_layer(cfg, step, lens, sel[layer], b["cu_k"], layer)
+            ref = inputs.extras_for_step(cfg, step, lens, sel[layer], b["cu_k"], layer)
+            for h in range(cfg.Hkv):
+                for r in range(cfg.B):
+                    got = ids[h, cu_e[r]:cu_e[r + 1]]
+                    assert torch.equal(got.to(torch.int64), ref[h * cfg.B + r])
+
+
+def test_extras_layers_matches_single_layer_calls():
+    cfg = datagen.get("llama8b_32k").with_(L=3, seqlens=(700,), extra_bp=300)
+    lens = [700]
+    b = inputs.make_budget(cfg, lens)
+    sel = inputs.random_selection(cfg, lens, b["k"])
+    ids, cu_e = inputs.extras_layers(cfg, 2, lens, sel, b["cu_k"], [0, 1, 2])
+    for layer in range(3):
+        one, _ = inputs.extras_layer(cfg, 2, lens, sel[layer], b["cu_k"], layer)
+        assert torch.equal(ids[layer], one)
+        ref = inputs.extras_for_step(cfg, 2, lens, sel[layer], b["cu_k"], layer)
+        for h in range(cfg.Hkv):
+            assert torch.equal(ids[layer, h].to(torch.int64), ref[h])
