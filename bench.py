@@ -1,23 +1,36 @@
 """Benchmark of the selective KV-transfer hot path on one MI355X.
 
-One step = one pass of the whole path over one request of the Llama-3-8B-shaped
-workload (32 layers, 32 q heads / 8 KV heads, d = 128, bf16, 8192-token prompt,
-64-query score window, 10% budget, 128 decode steps):
+Headline workload (``--workload batched64``, the default): 64 requests with
+prompt lengths uniform in [2048, 32768] (1.21 M tokens in all), Llama-3-8B
+attention shape (32 layers, 32 q heads / 8 KV heads, d = 128, bf16), one K/V
+source read by every layer, 64-query score window, 10% of each request's
+tokens selected per (layer, KV head), 2% more fetched on demand per decode
+step, 16-row pages.
 
-  prefill side   sg_score -> sg_topk -> sg_pack (transfer buffer in HBM)
-  decode side    128 x [ sg_split (Algorithm 1 on the step's KV index)
-                         -> sg_decode_attn over the selected rows of all 32
-                            layers, batched as 32 sequences ]
+One step is one pass of the whole path over that batch:
 
-Inputs are generated on the GPU before timing.  The decode reads rotate over
-several replicas of the transfer buffer so the working set exceeds the 256 MB
-last-level cache (a real decode step streams the model weights between layers).
+  prefill side   sg_score -> sg_topk -> sg_pack  (transfer buffer in HBM)
+  receive        sg_fetch: the transfer buffer's rows into the decode side's
+                 paged pool (logical rows 0 .. k-1 of every unit)
+  D decode steps sg_split (Algorithm 1 on [extras ++ selected], per-head mask)
+                 -> sg_fetch of the remote entries from the pinned-host copy
+                    of the prompt K/V (the prefill node) into logical rows
+                    k .. k+e-1
+                 -> sg_decode_attn, one launch per layer in model order
+                    (a HIP graph of L launches)
 
-Prints one JSON line.  ``value`` is select+pack throughput: bytes of the KV
-cache (K and V of every layer and head) turned into a transfer buffer per
-second of score + top-k + pack time.  The decode rate is reported as
-``decode_tokens_per_s``; the roofline object covers the dominant kernel
-(sparse decode attention).
+Inputs are generated on the GPU before timing.  Prints one JSON line:
+  value               select+pack rate: bytes of the KV cache (K and V of every
+                      layer and head, 146 GB here) turned into a transfer
+                      buffer per second of score + top-k + pack time
+  decode_tokens_per_s the other half of the metric: requests x decode steps per
+                      second of attention time (per-layer launches, model order)
+  roofline            sg_decode_attn, the HBM-bound kernel of the decode steps
+  cpu_baseline        the oracle on a bounded sample, in the same run
+  ops                 every op's median time (>= 20 repetitions after >= 3
+                      warm-ups, HIP events on the launch stream), rates and
+                      fractions of peak; ops.workloads holds the 8B 8K, 8B 32K
+                      and 70B 16K workloads (including pinned-host staging)
 """
 from __future__ import annotations
 
@@ -26,6 +39,7 @@ import json
 import math
 import os
 import platform
+import statistics
 import sys
 import time
 
@@ -34,12 +48,14 @@ if _ROOT not in sys.path:
     sys.path.insert(0, _ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# the counter summary that gives the decode kernel's measured HBM traffic, and
-# the sources whose hash it records (a changed kernel makes the figure stale)
-TRAFFIC_SUMMARY = os.path.join(_ROOT, "profiles", "all_kernels.llama8b_8k.hbm_traffic.md")
-TRAFFIC_SOURCES = ("paper_2607_28150_amd/csrc/decode_attn.hip", "paper_2607_28150_amd/csrc/sg_internal.h")
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
+# the counter summary that gives the decode kernel's measured HBM traffic at
+# the headline workload, and the sources whose hash it records (a changed
+# kernel makes the figure stale)
+TRAFFIC_SUMMARY = os.path.join(_ROOT, "profiles", "decode_attn.batched64.hbm_traffic.md")
+TRAFFIC_SOURCES = ("paper_2607_28150_amd/csrc/decode_attn.hip", "paper_2607_28150_amd/csrc/sg_internal.h")
+REPS, WARM = 20, 3
 
 
 def parse():
@@ -47,18 +63,428 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=5)
     p.add_argument("--warmup", type=int, default=2)
-    p.add_argument("--workload", default="llama8b_8k")
-    p.add_argument("--decode-steps", type=int, default=None, help="decode steps per step (default: workload's)")
+    p.add_argument("--workload", default="batched64")
+    p.add_argument("--decode-steps", type=int, default=16, help="decode steps per step")
+    p.add_argument("--seed", type=int, default=None, help="override the workload's seed")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--no-decode-side", action="store_true", help="skip the 32K-token decode-side section")
-    p.add_argument("--only", choices=["decode_side"], default=None,
+    p.add_argument("--no-ops", action="store_true", help="time the steps only (profiling runs)")
+    p.add_argument("--no-workloads", action="store_true", help="skip the other workloads' ops")
+    p.add_argument("--only", choices=["decode_side", "workload"], default=None,
                    help="run one section on its own and print its JSON line (profiling one workload)")
-    p.add_argument("--cpu-layers", type=int, default=0, help="layers the oracle is timed on (0 = all)")
-    p.add_argument("--cpu-seconds", type=float, default=10.0, help="repeat the oracle sample to at least this long")
+    p.add_argument("--cpu-seconds", type=float, default=8.0, help="repeat each oracle sample to at least this long")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of MIB MiB three times (counter calibration) and exit")
     return p.parse_args()
 
+
+# --------------------------------------------------------------------------- timing
+
+def _ev():
+    import torch
+    return torch.cuda.Event(enable_timing=True)
+
+
+def median_ms(fn, reps=REPS, warm=WARM):
+    """Median over `reps` calls of fn(i) after `warm` untimed calls; each call is
+    bracketed by its own pair of HIP events on the current stream."""
+    import torch
+    for i in range(warm):
+        fn(i)
+    torch.cuda.synchronize()
+    evs = [(_ev(), _ev()) for _ in range(reps)]
+    for i, (a, b) in enumerate(evs):
+        a.record()
+        fn(i)
+        b.record()
+    torch.cuda.synchronize()
+    return statistics.median(a.elapsed_time(b) for a, b in evs)
+
+
+def gbs(nbytes, ms):
+    return nbytes / (ms * 1e-3) / 1e9
+
+
+def r4(x):
+    return round(float(x), 4)
+
+
+# --------------------------------------------------------------------------- the path of one workload
+
+class Path:
+    """Every buffer of the hot path of one workload, resident before timing,
+    and the library calls of one step.
+
+    Units are ordered u = (l * B + b) * Hkv + h, so a layer's units are the
+    [B][Hkv] block that one per-layer sg_decode_attn call takes, and the whole
+    table is the [L * B][Hkv] block of the batched-layer call.  Every unit owns
+    ceil((k_b + e_b) / P) pages of the pool, placed at seeded random pool pages.
+    """
+
+    def __init__(self, sg, cfg, decode_steps, device="cuda", staged=None):
+        import torch
+        from datagen import inputs, rng
+
+        self.sg, self.cfg, self.D = sg, cfg, decode_steps
+        L, Hq, Hkv, d, W, P = cfg.L, cfg.Hq, cfg.Hkv, cfg.d, cfg.W, cfg.page_size
+        dev = device
+        self.staged = cfg.stage_host if staged is None else staged
+        pre = inputs.make_prefill(cfg, device=dev)
+        self.pre = pre
+        lens, T, B = pre["seqlens"], pre["T"], cfg.B
+        self.lens, self.T, self.B, self.N_max = lens, T, B, max(lens)
+        bud = inputs.make_budget(cfg, lens)
+        self.kb, self.cu_k, self.K_total = bud["k"], bud["cu_k"], bud["K_total"]
+        self.eb = [inputs.extras_count(n, cfg.extra_bp) for n in lens]
+        self.E_total = sum(self.eb)
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.cus = torch.tensor(pre["cu_seqlens"], **i32)
+        self.cuk = torch.tensor(self.cu_k, **i32)
+        self.esize = pre["k"].element_size()
+        self.scores = torch.empty((L, Hkv, T), device=dev)
+        self.idx = torch.empty((L, Hkv, self.K_total), **i32)
+        self.ws_score = torch.empty(sg.score_workspace_size(B, L, Hq, Hkv, d, W, self.N_max), dtype=torch.uint8,
+                                    device=dev)
+        S = L * Hkv * self.K_total
+        self.S = S
+        nbytes = sg.pack_bytes(pre["k"].dtype, L, Hkv, d, self.K_total)
+        self.tbuf = (torch.empty(nbytes, dtype=torch.uint8, pin_memory=True) if self.staged
+                     else torch.empty(nbytes, dtype=torch.uint8, device=dev))
+        rb = d * self.esize
+        self.tk = self.tbuf[: S * rb].view(pre["k"].dtype).view(S, d)
+        self.tv = self.tbuf[S * rb: 2 * S * rb].view(pre["k"].dtype).view(S, d)
+
+        # ---- decode-side pool and page tables
+        units = L * B * Hkv
+        self.units = units
+        rows_b = [k + e for k, e in zip(self.kb, self.eb)]
+        pages_b = [-(-r // P) for r in rows_b]
+        self.max_pages = max(pages_b)
+        lbh = lambda v: torch.tensor(v, dtype=torch.int64, device=dev)[None, :, None].expand(L, B, Hkv).reshape(-1)  # noqa: E731
+        pages_u = lbh(pages_b)
+        total_pages = int(pages_u.sum())
+        place = torch.argsort(rng.raw64(rng.stream_key(cfg.seed, 99, 1), total_pages, dev), stable=True)
+        first = torch.cumsum(pages_u, 0) - pages_u
+        j = torch.arange(self.max_pages, device=dev)[None, :]
+        ok = j < pages_u[:, None]
+        flat = (first[:, None] + j).clamp(max=total_pages - 1)
+        self.page_table = torch.where(ok, place[flat] * P, torch.full_like(flat, -1)).to(torch.int32)
+        self.page_table = self.page_table.view(L * B, Hkv, self.max_pages).contiguous()
+        pool_rows = total_pages * P
+        self.pool_bytes = 2 * pool_rows * rb
+        # enough pool replicas that a decode step's reads do not hit in the 256 MB last-level cache
+        self.reps = max(1, math.ceil(600e6 / self.pool_bytes))
+        self.pools = [(torch.empty((pool_rows, d), dtype=pre["k"].dtype, device=dev),
+                       torch.empty((pool_rows, d), dtype=pre["k"].dtype, device=dev)) for _ in range(self.reps)]
+        self.pages_read_per_layer = int(pages_u[: B * Hkv].sum())
+        self.rows_per_layer = Hkv * sum(rows_b)
+
+        # receive: unit u's k_b rows from transfer-buffer slot (l * Hkv + h) * K_total + cu_k[b]
+        l_u = torch.arange(L, device=dev)[:, None, None].expand(L, B, Hkv).reshape(-1)
+        b_u = torch.arange(B, device=dev)[None, :, None].expand(L, B, Hkv).reshape(-1)
+        h_u = torch.arange(Hkv, device=dev)[None, None, :].expand(L, B, Hkv).reshape(-1)
+        k_u = lbh(self.kb)
+        e_u = lbh(self.eb)
+        cuk_t = torch.tensor(self.cu_k[:-1], dtype=torch.int64, device=dev)
+        cus_t = torch.tensor(pre["cu_seqlens"][:-1], dtype=torch.int64, device=dev)
+        self.recv_off = torch.cat([torch.zeros(1, dtype=torch.int64, device=dev), torch.cumsum(k_u, 0)]).to(torch.int32)
+        self.recv_src = (l_u * Hkv + h_u) * self.K_total + cuk_t[b_u]
+        self.zeros = torch.zeros(units, **i32)
+
+        # decode steps: index row of unit u = [e_b extras ++ k_b selected], mask per (l, h, token)
+        rows_u = k_u + e_u
+        self.row_off = torch.cat([torch.zeros(1, dtype=torch.int64, device=dev), torch.cumsum(rows_u, 0)])
+        self.total = int(self.row_off[-1])
+        self.row_off = self.row_off.to(torch.int32)
+        self.mask = torch.full((L, Hkv, T), 2, dtype=torch.int8, device=dev)
+        self.mask_off = (l_u * Hkv + h_u) * T + cus_t[b_u]
+        self.mask_len = lbh(lens).to(torch.int32)
+        lk = torch.zeros_like(l_u) if cfg.kv_shared_layers else l_u
+        self.src_base = (lk * Hkv + h_u) * T + cus_t[b_u]
+        self.dst_start = k_u.to(torch.int32)
+        self.host_k = pre["k"].cpu().pin_memory() if self.E_total else None
+        self.host_v = pre["v"].cpu().pin_memory() if self.E_total else None
+        self.local = torch.empty(max(1, self.total), **i32)
+        self.remote = torch.empty(max(1, self.total), **i32)
+        self.n_local = torch.empty(units, **i32)
+        self.n_remote = torch.empty(units, **i32)
+        self.n_kept = torch.empty(units, **i32)
+        # position of every index entry in cat([extras of all layers, selection of all layers])
+        u_of = torch.repeat_interleave(torch.arange(units, device=dev), rows_u)
+        jj = torch.arange(self.total, device=dev) - self.row_off[:-1].to(torch.int64)[u_of]
+        lu, bu, hu = l_u[u_of], b_u[u_of], h_u[u_of]
+        eu = e_u[u_of]
+        cue_t = torch.tensor(inputs.cu_from_lengths(self.eb)[:-1], dtype=torch.int64, device=dev)
+        ext_pos = (lu * Hkv + hu) * self.E_total + cue_t[bu] + jj
+        sel_pos = L * Hkv * self.E_total + (lu * Hkv + hu) * self.K_total + cuk_t[bu] + (jj - eu)
+        self._entry_src = torch.where(jj < eu, ext_pos, sel_pos)
+        del u_of, jj, lu, bu, hu, eu, ext_pos, sel_pos
+        self.qdec = [inputs.decode_queries(cfg, s, device=dev, mu=pre["mu"]).permute(1, 0, 2, 3).contiguous()
+                     for s in range(decode_steps)]                    # [L][B][Hq][d]
+        self.out = torch.empty((L, B, Hq, d), device=dev)
+        self.ws_layer = torch.zeros(max(16, sg.decode_workspace_size(B, Hq, Hkv, d, self.max_pages, P)),
+                                    dtype=torch.uint8, device=dev)
+        self.ws_all = torch.zeros(max(16, sg.decode_workspace_size(L * B, Hq, Hkv, d, self.max_pages, P)),
+                                  dtype=torch.uint8, device=dev)
+        self.kv_index = []
+        self.graphs = []
+
+    # ---- the calls of a step
+    def score(self, lse_in=None):
+        c = self.cfg
+        self.sg.sg_score(self.pre["q_win"], self.pre["k"], self.cus, self.T, self.N_max, c.Hkv, self.scores,
+                         ws=self.ws_score, lse_in=lse_in)
+
+    def topk(self):
+        self.sg.sg_topk(self.scores, self.cus, self.T, self.N_max, self.cuk, self.K_total, self.idx)
+
+    def pack(self):
+        self.sg.sg_pack(self.pre["k"], self.pre["v"], self.idx, self.cus, self.T, self.cuk, self.K_total,
+                        max(self.kb), self.tbuf, L=self.cfg.L, Hkv=self.cfg.Hkv)
+
+    def receive(self, rep=0):
+        kp, vp = self.pools[rep]
+        self.sg.sg_fetch(self.recv_off, self.S, None, None, self.recv_src, self.tk, self.tv,
+                         self.page_table.view(self.units, -1), self.cfg.page_size, self.zeros, kp, vp)
+
+    def split(self, s):
+        self.sg.sg_split(self.row_off, self.kv_index[s], self.mask.view(-1), self.mask_off, self.mask_len, 0,
+                         self.local, self.remote, self.n_local, self.n_remote, n_kept=self.n_kept)
+
+    def fetch(self, s):
+        if not self.E_total:
+            return
+        kp, vp = self.pools[s % self.reps]
+        self.sg.sg_fetch(self.row_off, self.total, self.remote, self.n_remote, self.src_base, self.host_k,
+                         self.host_v, self.page_table.view(self.units, -1), self.cfg.page_size, self.dst_start,
+                         kp, vp)
+
+    def attn_layers(self, s):
+        c = self.cfg
+        B, Hkv = self.B, c.Hkv
+        kp, vp = self.pools[s % self.reps]
+        q = self.qdec[s]
+        nk = self.n_kept.view(c.L * B, Hkv)
+        for l in range(c.L):
+            self.sg.sg_decode_attn(q[l], kp, vp, self.page_table[l * B:(l + 1) * B], nk[l * B:(l + 1) * B],
+                                   c.page_size, self.out[l], ws=self.ws_layer)
+
+    def attn_batched(self, s):
+        c = self.cfg
+        kp, vp = self.pools[s % self.reps]
+        self.sg.sg_decode_attn(self.qdec[s].view(c.L * self.B, c.Hq, c.d), kp, vp, self.page_table,
+                               self.n_kept.view(c.L * self.B, c.Hkv), c.page_size,
+                               self.out.view(c.L * self.B, c.Hq, c.d), ws=self.ws_all)
+
+    def attn_graph(self, s):
+        self.graphs[s].replay()
+
+    # ---- set-up that needs the selection
+    def prepare(self, capture=True, selection=None):
+        """Runs the select region once (or takes `selection`, an index table
+        [L][Hkv][K_total], in place of score and top-k), then builds what the
+        decode side holds after the transfer (the per-head mask from the
+        selection, every pool replica with the received rows) and each decode
+        step's KV index (extras drawn from the complement of the selection).
+        Captures one graph per decode step of the per-layer attention launches
+        and checks every replay bit for bit against eager launches."""
+        import torch
+        from datagen import inputs
+        c = self.cfg
+        L, Hkv, B, dev = c.L, c.Hkv, self.B, self.idx.device
+        if selection is None:
+            self.score()
+            self.topk()
+        else:
+            self.idx.copy_(selection)
+        self.pack()
+        for r in range(self.reps):
+            self.receive(r)
+        ks = torch.tensor(self.kb, dtype=torch.int64, device=dev)
+        col_off = torch.tensor(self.pre["cu_seqlens"][:-1], dtype=torch.int64, device=dev)
+        col_off = torch.repeat_interleave(col_off, ks)
+        self.mask.view(L * Hkv, self.T).scatter_(1, self.idx.view(L * Hkv, -1).to(torch.int64) + col_off[None, :], 1)
+        for s in range(self.D):
+            if self.E_total:
+                ex = torch.stack([inputs.extras_layer(c, s, self.lens, self.idx[l], self.cu_k, l)[0]
+                                  for l in range(L)])                    # [L][Hkv][E_total]
+                src = torch.cat([ex.reshape(-1), self.idx.reshape(-1)])
+            else:
+                src = self.idx.reshape(-1)
+            self.kv_index.append(src[self._entry_src].contiguous())
+        del self._entry_src
+        torch.cuda.synchronize()
+        if not capture:
+            return
+        for s in range(self.D):
+            self.split(s)
+            self.fetch(s)
+            self.attn_layers(s)
+            torch.cuda.synchronize()
+            ref = self.out.clone()
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                self.attn_layers(s)
+            torch.cuda.current_stream().wait_stream(side)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self.attn_layers(s)
+            for _ in range(3):
+                self.out.fill_(float("nan"))
+                g.replay()
+                torch.cuda.synchronize()
+                assert torch.equal(self.out, ref), "graph replay differs from the eager launches"
+                self.attn_layers(s)
+                torch.cuda.synchronize()
+            self.graphs.append(g)
+
+    # ---- algorithmic work
+    def score_flops(self):
+        c = self.cfg
+        W = c.W
+        return sum(2.0 * c.d * c.G * (W * n - W * (W - 1) / 2) for n in self.lens) * c.L * c.Hkv
+
+    def kv_cache_bytes(self):
+        c = self.cfg
+        return 2 * c.L * c.Hkv * self.T * c.d * self.esize
+
+    def pack_bytes(self):
+        return 2 * self.S * self.cfg.d * self.esize * 2 + self.S * 4 * 2      # rows read + written, ids read + written
+
+    def receive_bytes(self):
+        return 2 * self.S * self.cfg.d * self.esize * 2                         # rows read + written
+
+    def fetch_bytes(self):
+        return self.cfg.L * self.cfg.Hkv * self.E_total * 2 * self.cfg.d * self.esize
+
+    def decode_layer_bytes(self):
+        c = self.cfg
+        return (self.rows_per_layer * 2 * c.d * self.esize + self.B * c.Hq * c.d * (self.esize + 4)
+                + self.pages_read_per_layer * 4 + self.B * c.Hkv * 4)
+
+    def free(self):
+        import torch
+        for k in list(self.__dict__):
+            setattr(self, k, None)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
+# --------------------------------------------------------------------------- ops of a path
+
+def path_ops(p: Path, lse=False):
+    """Median time of every op of the path, with rates and fractions of peak."""
+    import torch
+    c = p.cfg
+    peak_mfma = BF16_MFMA_PEAK_TFLOPS if c.dtype == "bf16" else FP32_MFMA_PEAK_TFLOPS
+    fl = p.score_flops()
+    ops = {}
+    t = median_ms(lambda i: p.score())
+    ops["score"] = {"ms": r4(t), "tflops": round(fl / (t * 1e-3) / 1e12, 1),
+                    "frac_mfma_peak": r4(fl / (t * 1e-3) / 1e12 / peak_mfma), "gflop_algorithmic": round(fl / 1e9, 1),
+                    "note": "self-contained: row statistics pass + column-sum pass (the contraction runs twice)"}
+    if lse:
+        lse_win = window_lse(p.pre["q_win"], p.pre["k"], p.lens, c.Hkv, c.W, c.d, c.kv_shared_layers)
+        t = median_ms(lambda i: p.score(lse_in=lse_win))
+        ops["score_lse_in"] = {"ms": r4(t), "tflops": round(fl / (t * 1e-3) / 1e12, 1),
+                               "frac_mfma_peak": r4(fl / (t * 1e-3) / 1e12 / peak_mfma),
+                               "note": "one pass: window-row log-sum-exp supplied by the prefill attention"}
+        del lse_win
+        p.score()
+    t = median_ms(lambda i: p.topk())
+    ops["topk"] = {"ms": r4(t), "rows": c.L * c.Hkv * p.B, "k_total": p.K_total}
+    t = median_ms(lambda i: p.pack())
+    pb = p.pack_bytes()
+    if p.staged:
+        ops["stage_host"] = {"ms": r4(t), "host_link_mb": round((pb / 2) / 1e6, 1),
+                             "host_link_gbs": round(gbs(pb / 2, t), 1),
+                             "note": "sg_pack with a pinned-host destination: rows + ids read from HBM, written "
+                                     "over the host link"}
+    else:
+        ops["pack"] = {"ms": r4(t), "gbs": round(gbs(pb, t), 1), "frac_hbm_peak": r4(gbs(pb, t) / HBM_PEAK_GBS),
+                       "mb_algorithmic": round(pb / 1e6, 1)}
+    t = median_ms(lambda i: p.receive(i % p.reps))
+    rb = p.receive_bytes()
+    ops["receive"] = {"ms": r4(t), "mb_algorithmic": round(rb / 1e6, 1)}
+    if p.staged:
+        ops["receive"].update({"host_link_gbs": round(gbs(rb / 2, t), 1),
+                               "note": "sg_fetch from the pinned-host transfer buffer into the pool pages"})
+    else:
+        ops["receive"].update({"gbs": round(gbs(rb, t), 1), "frac_hbm_peak": r4(gbs(rb, t) / HBM_PEAK_GBS)})
+    t = median_ms(lambda i: p.split(i % p.D))
+    ops["split"] = {"ms": r4(t), "entries": p.total}
+    if p.E_total:
+        p.split(0)
+        t = median_ms(lambda i: p.fetch(0))
+        fb = p.fetch_bytes()
+        ops["fetch"] = {"ms": r4(t), "host_link_mb": round(fb / 1e6, 1), "host_link_gbs": round(gbs(fb, t), 1),
+                        "rows": c.L * c.Hkv * p.E_total}
+    p.split(0)
+    p.fetch(0)
+    lb = p.decode_layer_bytes()
+    t = median_ms(lambda i: p.attn_graph(0)) if p.graphs else median_ms(lambda i: p.attn_layers(0))
+    ops["decode_attn_per_layer"] = {
+        "ms_per_step": r4(t), "launches_per_step": c.L, "mb_per_launch": round(lb / 1e6, 1),
+        "gbs": round(gbs(lb * c.L, t), 1), "frac_hbm_peak": r4(gbs(lb * c.L, t) / HBM_PEAK_GBS),
+        "tokens_per_s": round(p.B / (t * 1e-3), 1),
+        "note": "one sg_decode_attn per layer in model order, replayed from a HIP graph (bit-identical to eager)"}
+    t = median_ms(lambda i: p.attn_batched(0))
+    ops["decode_attn_batched_layers"] = {
+        "ms_per_step": r4(t), "gbs": round(gbs(lb * c.L, t), 1), "frac_hbm_peak": r4(gbs(lb * c.L, t) / HBM_PEAK_GBS),
+        "tokens_per_s": round(p.B / (t * 1e-3), 1),
+        "note": "all layers in one launch as L x B sequences: a kernel-bandwidth ceiling, not a model order"}
+    return ops
+
+
+def window_lse(q_win, k, lens, Hkv, W, d, shared):
+    """[B][L][Hq][W] natural-log LSE of the scaled causal logits of every
+    request's window rows (row w sits at position N - W + w), in fp32 with
+    torch: what a prefill attention kernel leaves behind."""
+    import torch
+    B, L, Hq, _, _ = q_win.shape
+    G = Hq // Hkv
+    out = torch.empty((B, L, Hq, W), dtype=torch.float32, device=q_win.device)
+    off = 0
+    for b, N in enumerate(lens):
+        pos = torch.arange(N - W, N, device=q_win.device)[:, None]
+        late = torch.arange(N, device=q_win.device)[None, :] > pos
+        for l in range(L):
+            lk = 0 if shared else l
+            for h in range(Hkv):
+                q = q_win[b, l, h * G:(h + 1) * G].float().reshape(G * W, d)
+                kt = k[lk, h, off:off + N].float().t().contiguous()
+                z = ((q @ kt) * (d ** -0.5)).view(G, W, N).masked_fill(late, float("-inf"))
+                out[b, l, h * G:(h + 1) * G] = torch.logsumexp(z, dim=-1)
+        off += N
+    return out
+
+
+# --------------------------------------------------------------------------- host link and device copy
+
+def host_link(nbytes=1 << 30):
+    """Pinned-host <-> device hipMemcpyAsync rates (the host link's measured peak)."""
+    import torch
+    h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    g = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    t_h2d = median_ms(lambda i: g.copy_(h, non_blocking=True), reps=10, warm=2)
+    t_d2h = median_ms(lambda i: h.copy_(g, non_blocking=True), reps=10, warm=2)
+    del h, g
+    return {"h2d_gbs": round(gbs(nbytes, t_h2d), 1), "d2h_gbs": round(gbs(nbytes, t_d2h), 1),
+            "mb": round(nbytes / 1e6, 1), "note": "hipMemcpyAsync between pinned host memory and HBM, median of 10"}
+
+
+def device_copy(nbytes):
+    """A plain device-to-device copy (bytes read + written) over rotating
+    buffers: the on-box ceiling for the gathers."""
+    import torch
+    src = [torch.ones(nbytes, dtype=torch.uint8, device="cuda") for _ in range(3)]
+    dst = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(3)]
+    t = median_ms(lambda i: dst[i % 3].copy_(src[(i + 1) % 3]))
+    del src, dst
+    return {"gbs": round(gbs(2 * nbytes, t), 1), "ms": r4(t), "mb": round(nbytes / 1e6, 1)}
+
+
+# --------------------------------------------------------------------------- main
 
 def main():
     args = parse()
@@ -81,7 +507,6 @@ def main():
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}), flush=True)
         return
 
-    from datagen import inputs
     from datagen.configs import get
     from paper_2607_28150_amd import smartgen as sg
 
@@ -93,194 +518,76 @@ def main():
     if args.only == "decode_side":
         print(json.dumps({"section": "decode_side", "n_gpus": 1, "decode_side": decode_side(sg)}), flush=True)
         return
-    dev = "cuda"
     cfg = get(args.workload)
-    assert cfg.B == 1 and cfg.extra_bp == 0, "the bench step covers single-request workloads without extras"
-    nsteps_dec = cfg.steps if args.decode_steps is None else args.decode_steps
-    L, Hq, Hkv, d, W, G = cfg.L, cfg.Hq, cfg.Hkv, cfg.d, cfg.W, cfg.G
+    if args.seed is not None:
+        cfg = cfg.with_(seed=args.seed)
+    if args.only == "workload":
+        print(json.dumps({"section": "workload", "workload": cfg.name, "ops": workload_ops(sg, cfg.name)}),
+              flush=True)
+        return
+    D = args.decode_steps
+    L, Hkv = cfg.L, cfg.Hkv
 
     # ------------------------------------------------------------- inputs (resident in HBM)
     t0 = time.time()
-    pre = inputs.make_prefill(cfg, device=dev)
-    lens, T = pre["seqlens"], pre["T"]
-    N = lens[0]
-    bud = inputs.make_budget(cfg, lens)
-    K_total = bud["K_total"]
-    cus = torch.tensor(pre["cu_seqlens"], dtype=torch.int32, device=dev)
-    cuk = torch.tensor(bud["cu_k"], dtype=torch.int32, device=dev)
-    qdec = torch.stack([inputs.decode_queries(cfg, s, device=dev, mu=pre["mu"])[0] for s in range(nsteps_dec)])
-    qdec = qdec.contiguous()                                           # [steps][L][Hq][d]
-    esize = 2 if cfg.dtype == "bf16" else 4
-    S = L * Hkv * K_total
-    nbytes = sg.pack_bytes(pre["k"].dtype, L, Hkv, d, K_total)
-    reps = max(2, math.ceil(640e6 / nbytes))
-    bufs = [torch.empty(nbytes, dtype=torch.uint8, device=dev) for _ in range(reps)]
-    scores = torch.empty((L, Hkv, T), device=dev)
-    idx = torch.empty((L, Hkv, K_total), dtype=torch.int32, device=dev)
-    ws_score = torch.empty(sg.score_workspace_size(1, L, Hq, Hkv, d, W, N), dtype=torch.uint8, device=dev)
-    P = cfg.page_size
-    npg = (K_total + P - 1) // P
-    units = L * Hkv
-    # decode: sequence = layer; unit (l, h) rows are slots (l*Hkv + h)*K_total + i of the K / V regions
-    page_table = (torch.arange(units, device=dev)[:, None] * K_total
-                  + torch.arange(npg, device=dev)[None, :] * P).to(torch.int32).view(L, Hkv, npg).contiguous()
-    n_rows = torch.full((L, Hkv), K_total, dtype=torch.int32, device=dev)
-    ws_dec = torch.zeros(max(sg.decode_workspace_size(L, Hq, Hkv, d, npg, P), 16), dtype=torch.uint8, device=dev)
-    out = torch.empty((L, Hq, d), device=dev)
-    pools = []
-    for b in bufs:
-        kp = b[: S * d * esize].view(pre["k"].dtype).view(S, d)
-        vp = b[S * d * esize: 2 * S * d * esize].view(pre["k"].dtype).view(S, d)
-        pools.append((kp, vp))
-    # Algorithm 1 inputs: every selected row is local (mask 1) in this workload
-    split_rows = units
-    row_off = (torch.arange(split_rows + 1, device=dev) * K_total).to(torch.int32)
-    mask = torch.ones((units, N), dtype=torch.int8, device=dev)
-    mask_off = (torch.arange(units, device=dev, dtype=torch.int64) * N)
-    mask_len = torch.full((units,), N, dtype=torch.int32, device=dev)
-    sp_local = torch.empty(S, dtype=torch.int32, device=dev)
-    sp_remote = torch.empty(S, dtype=torch.int32, device=dev)
-    sp_order = torch.empty(S, dtype=torch.int32, device=dev)
-    sp_nl = torch.empty(split_rows, dtype=torch.int32, device=dev)
-    sp_nr = torch.empty(split_rows, dtype=torch.int32, device=dev)
-    # row log-sum-exp of the window queries, as a prefill attention kernel
-    # leaves it behind (here: plain fp32 torch on the GPU, before timing); it
-    # feeds the one-pass score measured beside the self-contained one
-    lse_win = window_lse(pre["q_win"], pre["k"], N, Hkv, W, d)
-    torch.cuda.synchronize()
+    p = Path(sg, cfg, D)
+    print(f"[bench] {cfg.name}: inputs made in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    p.prepare()
     setup_s = time.time() - t0
+    print(f"[bench] {cfg.name}: set-up done in {setup_s:.1f} s", file=sys.stderr, flush=True)
 
-    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    decode = sg.DecodeCall(qdec[0], pools[0][0], pools[0][1], page_table, n_rows, P, out, ws=ws_dec)
-    ev_pool = [[ev() for _ in range(6)] for _ in range(args.steps)]
+    NE = 5 + 3 * D
 
-    # one step: score, top-k, pack; Algorithm 1 on the step's KV index (the
-    # selected set, all local in this workload, so once per request); then the
-    # decode steps, each one attention launch over all layers.  The decode
-    # launches run back to back between two events (an event between every
-    # launch would add its own marker to each measured interval).
-    # (events mark only the ends of the select region, the split and the
-    # decode launches; each op's own time is measured apart, below)
-    def step(r, e):
-        if e is None:
-            e = [None] * 6
-        rec = lambda i: e[i].record() if e[i] is not None else None  # noqa: E731
+    def step(e):
+        rec = (lambda i: e[i].record()) if e is not None else (lambda i: None)
         rec(0)
-        sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score)
-        sg.sg_topk(scores, cus, T, N, cuk, K_total, idx)
-        sg.sg_pack(pre["k"], pre["v"], idx, cus, T, cuk, K_total, K_total, bufs[r % reps])
+        p.score()
+        rec(1)
+        p.topk()
+        rec(2)
+        p.pack()
         rec(3)
-        sg.sg_split(row_off, idx.view(-1), mask.view(-1), mask_off, mask_len, 1, sp_local, sp_remote, sp_nl,
-                    sp_nr, out_index=sp_order)
+        p.receive()
         rec(4)
-        for s in range(nsteps_dec):
-            kp, vp = pools[(r + s) % reps]
-            decode(qdec[s], kp, vp, out)
-        rec(5)
+        for s in range(D):
+            p.split(s)
+            rec(5 + 3 * s)
+            p.fetch(s)
+            rec(6 + 3 * s)
+            p.attn_graph(s)
+            rec(7 + 3 * s)
 
-    # every replica holds a packed buffer before timing
-    for r in range(reps):
-        step(r, None)
-    for w in range(args.warmup):
-        step(w, None)
+    for _ in range(args.warmup):
+        step(None)
     torch.cuda.synchronize()
-
+    evs = [[_ev() for _ in range(NE)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k in range(args.steps):
-        step(k, ev_pool[k])
+        step(evs[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
+    print(f"[bench] {cfg.name}: {args.steps} steps in {wall:.2f} s", file=sys.stderr, flush=True)
 
-    # each op of the select region on its own (back-to-back launches), and the
-    # one-pass score (row normalisers supplied)
-    nrep = 10
+    def seg(i, j):
+        return float(np.median([e[i].elapsed_time(e[j]) for e in evs]))
 
-    def per_launch(fn):
-        fn()
-        torch.cuda.synchronize()
-        a, b = ev(), ev()
-        a.record()
-        for i in range(nrep):
-            fn(i)
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / nrep
+    def seg_dec(part):
+        # decode step s: split from the previous mark to 5 + 3s, fetch to 6 + 3s, attention to 7 + 3s
+        def one(e, s):
+            return e[4 + 3 * s + part].elapsed_time(e[5 + 3 * s + part])
+        return float(np.median([np.mean([one(e, s) for s in range(D)]) for e in evs]))
 
-    t_score = per_launch(lambda i=0: sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score))
-    t_topk = per_launch(lambda i=0: sg.sg_topk(scores, cus, T, N, cuk, K_total, idx))
-    t_pack = per_launch(lambda i=0: sg.sg_pack(pre["k"], pre["v"], idx, cus, T, cuk, K_total, K_total,
-                                               bufs[i % reps]))
-    t_score_lse = per_launch(lambda i=0: sg.sg_score(pre["q_win"], pre["k"], cus, T, N, Hkv, scores, ws=ws_score,
-                                                     lse_in=lse_win))
-
-    # the on-box reference: a plain device-to-device copy of the decode step's
-    # byte count, over rotating buffers so that the last-level cache cannot serve it
-    copy_bytes = 2 * S * d * esize
-    copy_src = [torch.empty(copy_bytes, dtype=torch.uint8, device=dev).fill_(1) for _ in range(6)]
-    copy_dst = [torch.empty(copy_bytes, dtype=torch.uint8, device=dev) for _ in range(6)]
-    t_copy = min(per_launch(lambda i=0: copy_dst[i % 6].copy_(copy_src[(i + 3) % 6])) for _ in range(3))
-    copy_gbs = 2 * copy_bytes / (t_copy * 1e-3) / 1e9             # bytes read + written
-    del copy_src, copy_dst
-
-    # the decode step as a model runs it: one launch per layer, in a HIP graph
-    dec_layers = per_layer_mode(sg, qdec[0], pools[0][0], pools[0][1], page_table, n_rows, P)
-
-    # block-granular proactive selection (eq. 1, eq. 2; M = 1024 blocks per
-    # layer, transfer time 6.5x the prefill time), timed on its own
-    blk = block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize)
-
-    # selector variants: alpha-rule counts, decode-time selection, on-demand ratio
-    sel_ops = selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx)
-
-    # the decode side of the 32K-token workload: two lanes, reuse, speculative transfer
-    dside = None if args.no_decode_side else decode_side(sg)
-
-    # ------------------------------------------------------------- per-op times (HIP events on the launch stream)
-    def ms(a, b):
-        return a.elapsed_time(b)
-    t_select = np.mean([ms(e[0], e[3]) for e in ev_pool])        # score + top-k + pack, back to back
-    t_split = np.mean([ms(e[3], e[4]) for e in ev_pool])
-    t_dec = np.mean([ms(e[4], e[5]) for e in ev_pool]) / nsteps_dec
+    t_select = seg(0, 3)
+    t_score, t_topk, t_pack, t_recv = seg(0, 1), seg(1, 2), seg(2, 3), seg(3, 4)
+    t_split, t_fetch, t_attn = seg_dec(0), seg_dec(1), seg_dec(2)
     ms_per_step = wall * 1e3 / args.steps
+    value = gbs(p.kv_cache_bytes(), t_select)
+    lb = p.decode_layer_bytes()
+    dec_gbs = gbs(lb, t_attn / L)
+    tokens_per_s = p.B / (t_attn * 1e-3)
+    step_tok_s = p.B / ((t_split + t_fetch + t_attn) * 1e-3)
 
-    kv_bytes = 2 * L * Hkv * T * d * esize                       # the whole KV cache
-    sel_ms = t_select
-    value = kv_bytes / (sel_ms * 1e-3) / 1e9
-    score_flops = 2.0 * d * G * (W * N - W * (W - 1) / 2) * units
-    pack_bytes_alg = 2 * S * d * esize * 2 + S * 4 * 2          # rows read + written, index read + written
-    dec_bytes = (2 * S * d * esize + L * Hq * d * esize + L * Hq * d * 4 + page_table.numel() * 4
-                 + n_rows.numel() * 4)
-    dec_gbs = dec_bytes / (t_dec * 1e-3) / 1e9
-    tokens_per_s = 1.0 / (t_dec * 1e-3)                          # one token of one request per decode step
-    peak_mfma = BF16_MFMA_PEAK_TFLOPS if cfg.dtype == "bf16" else FP32_MFMA_PEAK_TFLOPS
-    ops = {
-        "score": {"ms": round(t_score, 4), "tflops": round(score_flops / (t_score * 1e-3) / 1e12, 2),
-                  "frac_mfma_peak": round(score_flops / (t_score * 1e-3) / 1e12 / peak_mfma, 4),
-                  "gflop_algorithmic": round(score_flops / 1e9, 2)},
-        "score_lse_in": {"ms": round(t_score_lse, 4),
-                         "tflops": round(score_flops / (t_score_lse * 1e-3) / 1e12, 2),
-                         "frac_mfma_peak": round(score_flops / (t_score_lse * 1e-3) / 1e12 / peak_mfma, 4),
-                         "note": "one pass: row normalisers supplied by the prefill attention"},
-        "block_mode": blk,
-        "decode_side": dside,
-        "selectors": sel_ops,
-        "topk": {"ms": round(t_topk, 4),
-                 "gbs": round((scores.numel() * 4 + idx.numel() * 4) / (t_topk * 1e-3) / 1e9, 1)},
-        "pack": {"ms": round(t_pack, 4), "gbs": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9, 1),
-                 "frac_hbm_peak": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                 "frac_measured_copy": round(pack_bytes_alg / (t_pack * 1e-3) / 1e9 / copy_gbs, 4),
-                 "mb_algorithmic": round(pack_bytes_alg / 1e6, 2)},
-        "split": {"ms": round(t_split, 4)},
-        "decode_attn": {"ms": round(t_dec, 4), "gbs": round(dec_gbs, 1),
-                        "frac_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4),
-                        "frac_measured_copy": round(dec_gbs / copy_gbs, 4),
-                        "mb_algorithmic": round(dec_bytes / 1e6, 2)},
-        "decode_attn_per_layer": dec_layers,
-        "measured_copy": {"gbs": round(copy_gbs, 1), "ms": round(t_copy, 4), "mb": round(copy_bytes / 1e6, 2),
-                          "note": "device-to-device copy (bytes read + written) over six rotating buffer pairs; "
-                                  "the fractions named frac_measured_copy are against it"},
-    }
     line = {
         "metric": "select+pack GB/s and sparse decode-attn tokens/s; % of MI355X HBM/MFMA peak",
         "value": round(value, 2),
@@ -294,29 +601,98 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": cfg.name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
-                   "prompt": N, "score_window": W, "budget_bp": cfg.budget_bp, "k": K_total,
-                   "decode_steps": nsteps_dec, "page_size": P, "transfer_replicas": reps},
-        "select_ms": round(t_select, 4),
-        "value_lse_in": round(kv_bytes / ((t_select - t_score + t_score_lse) * 1e-3) / 1e9, 2),
+        "config": {"workload": cfg.name, "requests": p.B, "layers": L, "q_heads": cfg.Hq, "kv_heads": Hkv,
+                   "head_dim": cfg.d, "prompt_tokens": p.T, "prompt_min": min(p.lens), "prompt_max": max(p.lens),
+                   "score_window": cfg.W, "budget_bp": cfg.budget_bp, "extra_bp": cfg.extra_bp,
+                   "selected_rows": p.K_total, "extra_rows": p.E_total, "decode_steps": D,
+                   "page_size": cfg.page_size, "kv_source_shared_by_layers": cfg.kv_shared_layers,
+                   "seed": cfg.seed},
+        "select_ms": r4(t_select),
+        "value_note": "bytes of the KV cache of every layer and head turned into a transfer buffer per second of "
+                      "score + top-k + pack time (medians over the timed steps)",
         "decode_tokens_per_s": round(tokens_per_s, 1),
+        "decode_tokens_per_s_note": "requests per second of decode attention, one launch per layer in model order "
+                                    "(HIP graph); without the on-demand fetch",
+        "decode_step_tokens_per_s": round(step_tok_s, 1),
+        "decode_step_tokens_per_s_note": "requests per second of whole decode steps: Algorithm 1 + on-demand "
+                                         "fetch over the host link + attention",
+        "step_ms": {"score": r4(t_score), "topk": r4(t_topk), "pack": r4(t_pack), "receive": r4(t_recv),
+                    "split_per_decode_step": r4(t_split), "fetch_per_decode_step": r4(t_fetch),
+                    "attention_per_decode_step": r4(t_attn)},
         "roofline": {"kernel": "sg_decode_attn", "bound": "hbm", "achieved": round(dec_gbs, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(), "bytes_per_launch": dec_bytes,
-                     "avg_launch_ms": round(t_dec, 5), "frac_measured_copy": round(dec_gbs / copy_gbs, 4)},
-        "ops": ops,
-        "setup_s": round(setup_s, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": r4(dec_gbs / HBM_PEAK_GBS),
+                     "traffic": measured_traffic(), "bytes_per_launch": lb,
+                     "avg_launch_ms": round(t_attn / L, 5),
+                     "basis": f"HIP events around each decode step's graph of {L} per-layer launches in the timed "
+                              "steps (median), divided by the launches; includes the gaps between launches"},
+        "setup_s": round(setup_s, 1),
     }
+    if not args.no_ops:
+        ops = path_ops(p)
+        ops["host_link"] = host_link()
+        ops["measured_copy"] = device_copy(lb // 2)
+        cp = ops["measured_copy"]["gbs"]
+        for k in ("pack", "receive", "decode_attn_per_layer", "decode_attn_batched_layers"):
+            if k in ops and "gbs" in ops[k]:
+                ops[k]["frac_measured_copy"] = r4(ops[k]["gbs"] / cp)
+        if "fetch" in ops:
+            ops["fetch"]["frac_host_link_peak"] = r4(ops["fetch"]["host_link_gbs"] / ops["host_link"]["h2d_gbs"])
+        line["roofline"]["frac_measured_copy"] = r4(dec_gbs / cp)
+        line["ops"] = ops
+    cpu_in = None
+    if not args.no_cpu_baseline:
+        cpu_in = cpu_inputs(p)
+    p.free()
+    del p
+    if not args.no_ops and not args.no_workloads:
+        wl = {}
+        for name in ("llama8b_8k", "llama8b_32k", "llama70b_16k"):
+            print(f"[bench] workload {name}", file=sys.stderr, flush=True)
+            wl[name] = workload_ops(sg, name)
+        print("[bench] decode side (8B 32K)", file=sys.stderr, flush=True)
+        wl["llama8b_32k"]["decode_side"] = decode_side(sg)
+        for name in ("llama70b_16k", "llama8b_32k"):
+            o = wl[name]
+            for k in ("stage_host", "fetch"):
+                if k in o and "host_link_gbs" in o[k]:
+                    o[k]["frac_host_link_peak"] = r4(o[k]["host_link_gbs"] / line["ops"]["host_link"][
+                        "d2h_gbs" if k == "stage_host" else "h2d_gbs"])
+        line["ops"]["workloads"] = wl
 
     # ------------------------------------------------------------- oracle on the host cores
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, pre, bud, args.cpu_layers or cfg.L, args.cpu_seconds)
-        if line["cpu_baseline"].get("value"):
-            line["gpu_over_cpu"] = round(value / line["cpu_baseline"]["value"], 1)
+    if cpu_in is not None:
+        print("[bench] oracle baseline", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(cfg, cpu_in, args.cpu_seconds)
+        line["gpu_over_cpu"] = round(value / line["cpu_baseline"]["value"], 1)
+        line["decode_gpu_over_cpu"] = round(tokens_per_s / line["cpu_baseline"]["decode"]["tokens_per_s"], 1)
     print(json.dumps(line), flush=True)
 
 
-def block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize, M=1024, ratio=1 / 6.5, nrep=10):
+# --------------------------------------------------------------------------- other workloads
+
+def workload_ops(sg, name, decode_steps=2):
+    """Ops of one of the other workloads through the same path (the 70B slice
+    stages its transfer buffer in pinned host memory and the decode side
+    receives it from there); the 8B 8K workload also times block mode and the
+    selector variants."""
+    import torch
+    from datagen.configs import get
+    cfg = get(name)
+    p = Path(sg, cfg, decode_steps)
+    p.prepare()
+    ops = path_ops(p, lse=True)
+    ops["config"] = {"layers": cfg.L, "q_heads": cfg.Hq, "kv_heads": cfg.Hkv, "prompt": p.lens[0], "k": p.K_total,
+                     "extras": p.E_total, "staged_in_host_memory": p.staged, "pool_replicas": p.reps}
+    if name == "llama8b_8k":
+        esize = p.esize
+        ops["block_mode"] = block_mode(sg, p.scores, p.cus, p.T, p.lens[0], cfg.L, cfg.Hkv, cfg.d, p.pre, esize)
+        ops["selectors"] = selectors(sg, cfg, p.pre, p.cus, p.cuk, p.T, p.lens[0], p.K_total, p.idx)
+    p.free()
+    torch.cuda.empty_cache()
+    return ops
+
+
+def block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize, M=1024, ratio=1 / 6.5):
     """Times eq. 1 (block importance), the top-K_r over the L * M blocks and the
     push of the chosen blocks (device destination, two alternating buffers).
     The default T_p / T_t of 1 / 6.5 is the transfer-to-prefill time ratio
@@ -329,54 +705,37 @@ def block_mode(sg, scores, cus, T, N, L, Hkv, d, pre, esize, M=1024, ratio=1 / 6
     cu_row, cu_kr = (torch.tensor([0, L * M], dtype=torch.int32, device=dev),
                      torch.tensor([0, Kr], dtype=torch.int32, device=dev))
     nbytes = sg.pack_blocks_bytes(pre["k"].dtype, Hkv, d, N, M, Kr)
-    dsts = [torch.empty(nbytes, dtype=torch.uint8, device=dev) for _ in range(2)]
-
-    def run(i, ev=None):
-        if ev:
-            ev[0].record()
-        sg.sg_block_importance(scores, cus, T, M, imp)
-        if ev:
-            ev[1].record()
-        sg.sg_topk(imp.view(1, 1, L * M), cu_row, L * M, L * M, cu_kr, Kr, ids)
-        if ev:
-            ev[2].record()
-        sg.sg_pack_blocks(pre["k"], pre["v"], ids.view(-1), 0, N, M, dsts[i % 2])
-        if ev:
-            ev[3].record()
-    run(0)
-    run(1)
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(nrep)]
-    for i in range(nrep):
-        run(i, evs[i])
-    torch.cuda.synchronize()
-    t = [sum(e[j].elapsed_time(e[j + 1]) for e in evs) / nrep for j in range(3)]
+    dsts = [torch.empty(nbytes, dtype=torch.uint8, device=dev) for _ in range(3)]
+    t_imp = median_ms(lambda i: sg.sg_block_importance(scores, cus, T, M, imp))
+    t_top = median_ms(lambda i: sg.sg_topk(imp.view(1, 1, L * M), cu_row, L * M, L * M, cu_kr, Kr, ids))
+    t_pack = median_ms(lambda i: sg.sg_pack_blocks(pre["k"], pre["v"], ids.view(-1), 0, N, M, dsts[i % 3]))
     Nb = -(-N // M)
     rows = Kr * Hkv * Nb
     pack_bytes = 2 * 2 * rows * d * esize + 2 * Kr * 4                # rows read + written, ids read + written
     imp_bytes = L * Hkv * N * 4 + L * M * 4
     return {"M": M, "transfer_over_prefill": round(1 / ratio, 2), "K_r": Kr, "blocks": L * M,
-            "importance_ms": round(t[0], 4), "importance_gbs": round(imp_bytes / (t[0] * 1e-3) / 1e9, 1),
-            "topk_ms": round(t[1], 4),
-            "pack_ms": round(t[2], 4), "pack_gbs": round(pack_bytes / (t[2] * 1e-3) / 1e9, 1),
-            "pack_frac_hbm_peak": round(pack_bytes / (t[2] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "importance_ms": r4(t_imp), "importance_gbs": round(gbs(imp_bytes, t_imp), 1),
+            "topk_ms": r4(t_top),
+            "pack_ms": r4(t_pack), "pack_gbs": round(gbs(pack_bytes, t_pack), 1),
+            "pack_frac_hbm_peak": r4(gbs(pack_bytes, t_pack) / HBM_PEAK_GBS),
             "pack_mb_algorithmic": round(pack_bytes / 1e6, 2)}
 
 
-def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
+def decode_side(sg, nsteps=12, long_steps=256, ratio_bp=1000, M=1024):
     """Decode side of the 8B-shaped 32K-token workload (5% of the rows sent at
     prefill, 2% more fetched on demand per step, all 32 layers per step):
     Algorithm 1 and the two lanes of Section 4.2 (serial on one stream, or on
     two streams; with and without reuse of fetched rows), and speculative
-    transfer (Section 4.3: the quota of remaining blocks pushed while the
-    attention runs; the next step's split waits for it).  The prefill side's
-    copy of K / V is pinned host memory, so the remote lane and the speculative
-    push cross the host link; the decode side's store is in HBM."""
+    transfer (Section 4.3: the quota of remaining blocks pushed on a side stream
+    while the decode steps go on; a step's split waits only for pushes that
+    have already completed).  The prefill side's copy of K / V is pinned host
+    memory, so the remote lane and the speculative push cross the host link;
+    the decode side's store is in HBM."""
     import numpy as np
     import torch
     from datagen import inputs
     from datagen.configs import get
-    from paper_2607_28150_amd.lanes import StepBuffers, TwoLane
+    from paper_2607_28150_amd.lanes import SpecPusher, StepBuffers, TwoLane
 
     cfg = get("llama8b_32k")
     dev = "cuda"
@@ -405,12 +764,11 @@ def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
 
     # each step's KV index per (layer, head): that step's extras, then the selected rows
     per = kb + e
-    idx = torch.empty((nsteps, rows, per), dtype=torch.int32, device=dev)
-    for s in range(nsteps):
-        for l in range(L):
-            ex = inputs.extras_for_step(cfg, s, lens, sel[l], bud["cu_k"], l)
-            for h in range(Hkv):
-                idx[s, l * Hkv + h, :e] = ex[h].to(torch.int32)
+    nidx = max(nsteps, long_steps)
+    idx = torch.empty((nidx, rows, per), dtype=torch.int32, device=dev)
+    for s in range(nidx):
+        ex, _ = inputs.extras_layers(cfg, s, lens, sel, bud["cu_k"], range(L))
+        idx[s, :, :e] = ex.view(rows, e)
         idx[s, :, e:] = sel.view(rows, kb)
     row_off = (torch.arange(rows + 1, device=dev) * per).to(torch.int32)
     max_pages = -(-per // P)
@@ -434,25 +792,21 @@ def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
     sg.sg_block_importance(scores, cus, T, M, imp)
     LM = L * M
     quota = sg.spec_quota(LM, ratio_bp)
-    rem = torch.empty(LM, device=dev)
-    ids = torch.empty(quota, dtype=torch.int32, device=dev)
-    cu_row = torch.tensor([0, LM], dtype=torch.int32, device=dev)
-    spec_stream = torch.cuda.Stream()
     main = torch.cuda.current_stream()
-    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    counts = torch.empty((nsteps, 2, rows), dtype=torch.int32, device=dev)
-    # top-k offsets of every push size, made before any stream uses them
-    cu_q = {q: torch.tensor([0, q], dtype=torch.int32, device=dev) for q in {quota, LM % quota or quota}}
+    ev = _ev
+    counts = torch.empty((nidx, 2, rows), dtype=torch.int32, device=dev)
 
-    def run(mode):
+    def run(mode, quota_blocks=quota, steps=nsteps):
         reset()
-        rem.copy_(imp.view(-1))
-        left = LM
+        pusher = SpecPusher(src_k, src_v, imp.view(-1), 0, N, M, store_k, store_v, mask, quota_blocks) \
+            if mode.startswith("speculative") else None
         torch.cuda.synchronize()
         t = []
-        for s in range(nsteps):
+        for s in range(steps):
             a, b = ev(), ev()
             a.record(main)
+            if pusher is not None:
+                pusher.commit_if_landed(main)
             if mode == "serial":
                 sg.sg_split(row_off, idx[s].view(-1), mask.view(-1), base, mlen, 1, buf.local, buf.remote,
                             buf.n_local, buf.n_remote, out_index=buf.order, n_kept=buf.n_kept)
@@ -465,31 +819,31 @@ def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
                              mask_len=mlen, store_k=store_k, store_v=store_v, store_base=base, src_k=src_k,
                              src_v=src_v, src_base=base, page_table=page_table, page_size=P, k_pool=kp, v_pool=vp,
                              buf=buf, reuse=mode != "two_lane_no_reuse")
-            if mode == "speculative" and left > 0:
-                # the prefill side pushes the next blocks while the attention runs
-                q = min(quota, left)
-                go = torch.cuda.Event()
-                go.record(main)
-                spec_stream.wait_event(go)
-                sg.sg_topk(rem.view(1, 1, LM), cu_row, LM, LM, cu_q[q], q, ids[:q].view(1, 1, q), stream=spec_stream)
-                sg.sg_spec_push(src_k, src_v, ids[:q], 0, N, M, store_k, store_v, mask, rem, stream=spec_stream)
-                left -= q
-            sg.sg_decode_attn(qdec[s], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P, out, ws=ws)
-            if mode == "speculative":
-                done = torch.cuda.Event()
-                done.record(spec_stream)
-                main.wait_event(done)
+            if pusher is not None:
+                pusher.launch_if_idle(main)
+            sg.sg_decode_attn(qdec[s % nsteps], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P, out,
+                              ws=ws)
             b.record(main)
             counts[s, 0].copy_(buf.n_remote)
             counts[s, 1].copy_(buf.n_kept)
             t.append((a, b))
         torch.cuda.synchronize()
-        c = counts.double().sum(dim=2).cpu().numpy()
-        ratio = [round(float(x), 4) for x in c[:, 0] / c[:, 1]]
+        c = counts[:steps].double().sum(dim=2).cpu().numpy()
+        ratio = c[:, 0] / c[:, 1]
         ms_steps = [a.elapsed_time(b) for a, b in t]
-        return {"ms_per_step": round(float(np.mean(ms_steps[1:])), 3), "ms_first": round(ms_steps[0], 3),
-                "ms_steps": [round(x, 3) for x in ms_steps],
-                "on_demand_ratio": ratio, "remote_rows_per_step": [int(x) for x in c[:, 0]]}
+        res = {"steps": steps, "ms_per_step": round(float(np.median(ms_steps[1:])), 3),
+               "ms_first": round(ms_steps[0], 3), "ms_total": round(float(np.sum(ms_steps)), 2)}
+        if steps <= 16:
+            res.update({"ms_steps": [round(x, 3) for x in ms_steps],
+                        "on_demand_ratio": [r4(x) for x in ratio], "remote_rows_per_step": [int(x) for x in c[:, 0]]})
+        else:
+            marks = sorted({0, 1, 5, 10, 20, 50, 100, steps // 2, steps - 1} & set(range(steps)))
+            res.update({"ms_at_step": {str(i): round(ms_steps[i], 3) for i in marks},
+                        "on_demand_ratio_at_step": {str(i): r4(ratio[i]) for i in marks},
+                        "on_demand_ratio_mean": r4(ratio.mean())})
+        if pusher is not None:
+            res.update({"pushes_done": pusher.pushes, "blocks_left": pusher.left})
+        return res
 
     res = {"workload": cfg.name, "steps": nsteps, "rows_per_unit": per, "selected": kb, "extras": e}
     for mode in ("serial", "two_lane", "two_lane_no_reuse", "speculative"):
@@ -497,6 +851,12 @@ def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
     res["speculative"]["ratio_bp"] = ratio_bp
     res["speculative"]["blocks_per_push"] = quota
     res["speculative"]["pushes_to_complete"] = -(-LM // quota)
+    # the workload's whole decode: two lanes with reuse, without and with
+    # speculative transfer, cumulative time over every step
+    res["over_all_steps"] = {"two_lane": run("two_lane", steps=long_steps),
+                             "speculative": run("speculative", steps=long_steps)}
+    a, b2 = res["over_all_steps"]["two_lane"]["ms_total"], res["over_all_steps"]["speculative"]["ms_total"]
+    res["over_all_steps"]["speculative_speedup"] = round(a / b2, 3)
     # lane rates and interference, each on its own
     reset()
     torch.cuda.synchronize()
@@ -506,23 +866,21 @@ def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
     n_loc = int(buf.n_local.sum().item())
     n_rem = int(buf.n_remote.sum().item())
     rowb = 2 * d * pre["k"].element_size()
-    e0, e1, e2, e3 = ev(), ev(), ev(), ev()
-    e0.record()
-    sg.sg_fetch(row_off, rows * per, buf.local, buf.n_local, base, store_k, store_v, page_table, P, buf.n_remote,
-                kp, vp)
-    e1.record()
-    sg.sg_fetch(row_off, rows * per, buf.remote, buf.n_remote, base, src_k, src_v, page_table, P, zeros, kp, vp)
-    e2.record()
-    sg.sg_decode_attn(qdec[1], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P, out, ws=ws)
-    e3.record()
-    torch.cuda.synchronize()
-    t_loc, t_rem, t_dec = e0.elapsed_time(e1), e1.elapsed_time(e2), e2.elapsed_time(e3)
+    t_loc = median_ms(lambda i: sg.sg_fetch(row_off, rows * per, buf.local, buf.n_local, base, store_k, store_v,
+                                            page_table, P, buf.n_remote, kp, vp))
+    t_rem = median_ms(lambda i: sg.sg_fetch(row_off, rows * per, buf.remote, buf.n_remote, base, src_k, src_v,
+                                            page_table, P, zeros, kp, vp))
+    t_dec = median_ms(lambda i: sg.sg_decode_attn(qdec[1], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P,
+                                                  out, ws=ws))
     # decode attention alone and beside a speculative push on another stream
-    rem.copy_(imp.view(-1))
-    sg.sg_topk(rem.view(1, 1, LM), cu_row, LM, LM, cu_q[quota], quota, ids.view(1, 1, quota))
+    rem = imp.view(-1).clone()
+    ids = torch.empty(quota, dtype=torch.int32, device=dev)
+    cu_row = torch.tensor([0, LM], dtype=torch.int32, device=dev)
+    cu_q = torch.tensor([0, quota], dtype=torch.int32, device=dev)
+    sg.sg_topk(rem.view(1, 1, LM), cu_row, LM, LM, cu_q, quota, ids.view(1, 1, quota))
+    spec_stream = torch.cuda.Stream()
     torch.cuda.synchronize()
-    f0, f1 = ev(), ev()
-    s0, s1 = ev(), ev()
+    f0, f1, s0, s1 = ev(), ev(), ev(), ev()
     s0.record(spec_stream)
     sg.sg_spec_push(src_k, src_v, ids, 0, N, M, store_k, store_v, mask, None, stream=spec_stream)
     s1.record(spec_stream)
@@ -533,31 +891,22 @@ def decode_side(sg, nsteps=12, ratio_bp=1000, M=1024):
     torch.cuda.synchronize()
     t_dec_busy = f0.elapsed_time(f1) / 10
     t_push = s0.elapsed_time(s1)
-    g0, g1 = ev(), ev()
-    g0.record()
-    for r in range(10):
-        sg.sg_decode_attn(qdec[r % nsteps], kp, vp, page_table.view(L, Hkv, max_pages), buf.n_kept, P, out, ws=ws)
-    g1.record()
-    torch.cuda.synchronize()
-    t_dec_alone = g0.elapsed_time(g1) / 10
     Nb = -(-N // M)
     push_bytes = quota * Hkv * Nb * rowb
-    res["lanes"] = {"local_rows": n_loc, "local_ms": round(t_loc, 4),
-                    "local_gbs": round(n_loc * rowb * 2 / (t_loc * 1e-3) / 1e9, 1),
-                    "remote_rows": n_rem, "remote_ms": round(t_rem, 4),
-                    "remote_host_link_gbs": round(n_rem * rowb / (t_rem * 1e-3) / 1e9, 1),
-                    "decode_ms": round(t_dec, 4)}
+    res["lanes"] = {"local_rows": n_loc, "local_ms": r4(t_loc), "local_gbs": round(gbs(n_loc * rowb * 2, t_loc), 1),
+                    "remote_rows": n_rem, "remote_ms": r4(t_rem),
+                    "remote_host_link_gbs": round(gbs(n_rem * rowb, t_rem), 1), "decode_ms": r4(t_dec)}
     res["spec_push"] = {"blocks": quota, "mb": round(push_bytes / 1e6, 1), "ms": round(t_push, 3),
-                        "host_link_gbs": round(push_bytes / (t_push * 1e-3) / 1e9, 1),
-                        "decode_ms_alone": round(t_dec_alone, 4), "decode_ms_beside_push": round(t_dec_busy, 4),
-                        "decode_slowdown": round(t_dec_busy / t_dec_alone, 3)}
+                        "host_link_gbs": round(gbs(push_bytes, t_push), 1),
+                        "decode_ms_alone": r4(t_dec), "decode_ms_beside_push": r4(t_dec_busy),
+                        "decode_slowdown": round(t_dec_busy / t_dec, 3)}
     del pre, src_k, src_v, store_k, store_v
     torch.cuda.synchronize()
     return res
 
 
-def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=5.0, cap_bp=2000, nrep=10):
-    """Selector variants on the request of the main step: the alpha-rule
+def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=5.0, cap_bp=2000):
+    """Selector variants on the request of the 8B 8K workload: the alpha-rule
     selection-frequency score (Section 4.1 importance under the Section 5.1
     selector) and decode-time dynamic selection (Section 2.3; alpha 5, at most
     20% of the tokens), each timed on its own; then the on-demand ratio
@@ -572,23 +921,10 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     dev = "cuda"
     L, Hq, Hkv, d, W = cfg.L, cfg.Hq, cfg.Hkv, cfg.d, cfg.W
     esize = pre["k"].element_size()
-    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     units = L * Hkv
-
-    def timed(fn):
-        fn()
-        torch.cuda.synchronize()
-        a, b = ev(), ev()
-        a.record()
-        for _ in range(nrep):
-            fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / nrep
-
     counts = torch.empty((L, Hkv, T), device=dev)
     ws = torch.empty(sg.score_workspace_size(1, L, Hq, Hkv, d, W, N), dtype=torch.uint8, device=dev)
-    t_count = timed(lambda: sg.sg_score_count(pre["q_win"], pre["k"], cus, T, N, Hkv, counts, alpha, ws))
+    t_count = median_ms(lambda i: sg.sg_score_count(pre["q_win"], pre["k"], cus, T, N, Hkv, counts, alpha, ws))
     idx_count = torch.empty_like(idx_score)
     sg.sg_topk(counts, cus, T, N, cuk, K_total, idx_count)
     cap = N * cap_bp // 10000
@@ -597,16 +933,16 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     idx_dec = torch.empty((L, Hkv, cap), dtype=torch.int32, device=dev)
     n_sel = torch.empty((1, L, Hkv), dtype=torch.int32, device=dev)
     qs = [inputs.decode_queries(cfg, s, device=dev, mu=pre["mu"]) for s in range(nsteps)]     # [1][L][Hq][d]
-    t_sel = timed(lambda: sg.sg_decode_select(qs[0], pre["k"], cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha,
-                                              ws_sel))
+    t_sel = median_ms(lambda i: sg.sg_decode_select(qs[0], pre["k"], cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel,
+                                                    alpha, ws_sel))
     # InfiniGen's partial ratio 0.3: 40 of the 128 channels (here the first 40;
     # the paper's selector picks them with skewing matrices from the weights),
     # kept as a contiguous partial-key cache, with the full head's scale
     dp = 40
     k_part = pre["k"][..., :dp].contiguous()
     qp = [x[..., :dp].contiguous() for x in qs]
-    t_sel_p = timed(lambda: sg.sg_decode_select(qp[0], k_part, cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel, alpha,
-                                                ws_sel, scale=d ** -0.5))
+    t_sel_p = median_ms(lambda i: sg.sg_decode_select(qp[0], k_part, cus, T, N, Hkv, cu_cap, cap, idx_dec, n_sel,
+                                                      alpha, ws_sel, scale=d ** -0.5))
     kp_bytes = units * N * dp * esize
     score_flops = 2.0 * d * cfg.G * (W * N - W * (W - 1) / 2) * units
     k_bytes = units * N * d * esize
@@ -624,7 +960,8 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     ratios = {}
     sel_frac = []
     for name, sel, partial in (("score", idx_score, False), ("count", idx_count, False),
-                               ("sequential", seq, False), ("random", rnd, False), ("score_partial_selector", idx_score, True)):
+                               ("sequential", seq, False), ("random", rnd, False),
+                               ("score_partial_selector", idx_score, True)):
         mask = torch.full((units, N), 2, dtype=torch.int8, device=dev)
         mask.scatter_(1, sel.view(units, K_total).long(), 1)
         rs = []
@@ -638,40 +975,19 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
             rs.append(nr.sum().item() / max(1, nk.sum().item()))
             if name == "score":
                 sel_frac.append(n_sel.float().mean().item() / N)
-        ratios[name] = round(float(np.mean(rs)), 4)
-    return {"alpha": alpha, "count_score": {"ms": round(t_count, 4),
-                                            "tflops": round(score_flops / (t_count * 1e-3) / 1e12, 2),
-                                            "frac_mfma_peak": round(score_flops / (t_count * 1e-3) / 1e12
-                                                                    / BF16_MFMA_PEAK_TFLOPS, 4)},
-            "decode_select": {"ms": round(t_sel, 4), "cap": cap,
-                              "k_read_gbs": round(k_bytes / (t_sel * 1e-3) / 1e9, 1),
-                              "frac_hbm_peak": round(k_bytes / (t_sel * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                              "selected_fraction": round(float(np.mean(sel_frac)), 4)},
-            "decode_select_partial_40_of_128": {"ms": round(t_sel_p, 4),
-                                                "k_read_gbs": round(kp_bytes / (t_sel_p * 1e-3) / 1e9, 1),
-                                                "frac_hbm_peak": round(kp_bytes / (t_sel_p * 1e-3) / 1e9
-                                                                       / HBM_PEAK_GBS, 4)},
+        ratios[name] = r4(np.mean(rs))
+    return {"alpha": alpha, "count_score": {"ms": r4(t_count), "tflops": round(score_flops / (t_count * 1e-3) / 1e12, 1),
+                                            "frac_mfma_peak": r4(score_flops / (t_count * 1e-3) / 1e12
+                                                                 / BF16_MFMA_PEAK_TFLOPS)},
+            "decode_select": {"ms": r4(t_sel), "cap": cap, "k_read_gbs": round(gbs(k_bytes, t_sel), 1),
+                              "frac_hbm_peak": r4(gbs(k_bytes, t_sel) / HBM_PEAK_GBS),
+                              "selected_fraction": r4(np.mean(sel_frac))},
+            "decode_select_partial_40_of_128": {"ms": r4(t_sel_p), "k_read_gbs": round(gbs(kp_bytes, t_sel_p), 1),
+                                                "frac_hbm_peak": r4(gbs(kp_bytes, t_sel_p) / HBM_PEAK_GBS)},
             "on_demand_ratio_by_proactive_choice": ratios, "budget_k": K_total, "steps": nsteps}
 
 
-def window_lse(q_win, k, N, Hkv, W, d):
-    """[1][L][Hq][W] natural-log LSE of the scaled causal logits of the window
-    rows (row w sits at position N - W + w), in fp32 with torch."""
-    import torch
-    _, L, Hq, _, _ = q_win.shape
-    G = Hq // Hkv
-    out = torch.empty((1, L, Hq, W), dtype=torch.float32, device=q_win.device)
-    pos = torch.arange(N - W, N, device=q_win.device)[:, None]
-    late = torch.arange(N, device=q_win.device)[None, :] > pos          # [W][N] keys past the row
-    for l in range(L):
-        for h in range(Hkv):
-            q = q_win[0, l, h * G:(h + 1) * G].float().reshape(G * W, d)
-            kt = k[l, h].float().t().contiguous()                       # [d][N]
-            z = (q @ kt) * (d ** -0.5)
-            z = z.view(G, W, N).masked_fill(late, float("-inf"))
-            out[0, l, h * G:(h + 1) * G] = torch.logsumexp(z, dim=-1)
-    return out
-
+# --------------------------------------------------------------------------- counters
 
 def sources_sha256(paths) -> str:
     import hashlib
@@ -699,104 +1015,89 @@ def measured_traffic():
     return int(t.group(1))
 
 
-def per_layer_mode(sg, q, k_pool, v_pool, page_table, n_rows, P, nrep=20):
-    """One decode step as a model runs it: one sg_decode_attn launch per layer
-    (B = 1, the layer's KV heads), the layers in order, captured once in a HIP
-    graph and replayed.  Every replay is checked bit for bit against the same
-    launches made eagerly (with eager work between the replays) before it is
-    timed."""
+# --------------------------------------------------------------------------- oracle baseline
+
+def cpu_inputs(p: Path):
+    """Host copies of the oracle's samples, taken from the seeded inputs (never
+    from a GPU result):
+      select half - request 0, every layer and KV head;
+      decode half - layer 0 of decode step 0 for every request and KV head,
+                    attending over a seeded random selection of k_b rows plus
+                    the e_b extras drawn from its complement (the workload's
+                    sizes), gathered into a contiguous float32 pool."""
+    import numpy as np
     import torch
-    L, Hkv, npg = page_table.shape
-    Hq, d = q.shape[1], q.shape[2]
-    dev = q.device
-    ws = torch.zeros(max(sg.decode_workspace_size(1, Hq, Hkv, d, npg, P), 16), dtype=torch.uint8, device=dev)
-    out = torch.empty((L, Hq, d), device=dev)
-
-    def layers():
-        for l in range(L):
-            sg.sg_decode_attn(q[l:l + 1], k_pool, v_pool, page_table[l:l + 1], n_rows[l:l + 1], P, out[l:l + 1],
-                              ws=ws)
-
-    def timed(fn):
-        fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(nrep):
-            fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / nrep
-
-    layers()
-    torch.cuda.synchronize()
-    ref = out.clone()
-    t_eager = timed(layers)
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        layers()
-    torch.cuda.current_stream().wait_stream(side)
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        layers()
-    for _ in range(3):
-        out.fill_(float("nan"))
-        graph.replay()
-        torch.cuda.synchronize()
-        assert torch.equal(out, ref), "graph replay differs from the eager launches"
-        layers()
-        torch.cuda.synchronize()
-    t_graph = timed(graph.replay)
-    graph.replay()
-    torch.cuda.synchronize()
-    assert torch.equal(out, ref), "graph replay differs from the eager launches"
-    return {"launches": f"{L} sg_decode_attn calls per step, one per layer ({Hkv} KV heads, {Hq} q heads each)",
-            "graph_ms": round(t_graph, 4), "eager_ms": round(t_eager, 4),
-            "tokens_per_s_graph": round(1.0 / (t_graph * 1e-3), 1),
-            "note": "graph replays checked bit for bit against eager launches"}
+    from datagen import inputs
+    c = p.cfg
+    n0 = p.lens[0]
+    q0 = p.pre["q_win"][:1].float().cpu().numpy()
+    lk = 1 if c.kv_shared_layers else c.L
+    k0 = p.pre["k"][:lk, :, :n0].float().cpu().numpy()
+    u16 = lambda t: t.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)  # noqa: E731
+    kraw0 = u16(p.pre["k"][:lk, :, :n0])
+    vraw0 = u16(p.pre["v"][:lk, :, :n0])
+    sel = inputs.random_selection(c.with_(L=1), p.lens, p.kb, device=p.idx.device, tag_extra=11)[0]   # [Hkv][K]
+    ex, cu_e = inputs.extras_layer(c, 0, p.lens, sel, p.cu_k, 0)
+    kf = p.pre["k"][0].float()                  # [Hkv][T][d] (layer 0's source)
+    vf = p.pre["v"][0].float()
+    rows_k, rows_v, n_rows = [], [], np.zeros((p.B, c.Hkv), np.int32)
+    for b in range(p.B):
+        for h in range(c.Hkv):
+            ids = torch.cat([ex[h, cu_e[b]:cu_e[b + 1]], sel[h, p.cu_k[b]:p.cu_k[b + 1]]]).long() + p.pre["cu_seqlens"][b]
+            rows_k.append(kf[h, ids])
+            rows_v.append(vf[h, ids])
+            n_rows[b, h] = ids.numel()
+    P = c.page_size
+    per = -(-int(n_rows.max()) // P) * P
+    kp = np.zeros((p.B * c.Hkv * per, c.d), np.float32)
+    vp = np.zeros_like(kp)
+    for u, (rk, rv) in enumerate(zip(rows_k, rows_v)):
+        kp[u * per:u * per + rk.shape[0]] = rk.cpu().numpy()
+        vp[u * per:u * per + rv.shape[0]] = rv.cpu().numpy()
+    npg = per // P
+    pt = ((np.arange(p.B * c.Hkv)[:, None] * per + np.arange(npg)[None, :] * P).astype(np.int32)
+          .reshape(p.B, c.Hkv, npg))
+    qd = p.qdec[0][0].float().cpu().numpy()     # layer 0: [B][Hq][d]
+    return {"q0": q0, "k0": k0, "kraw0": kraw0, "vraw0": vraw0, "n0": n0, "k_b0": p.kb[0],
+            "dec": (qd, kp, vp, pt, n_rows, P), "dec_rows": int(n_rows.sum()), "esize": p.esize}
 
 
-def cpu_baseline(cfg, pre, bud, layers, min_seconds):
-    """The oracle's select+pack (score, top-k, pack) timed on a bounded sample:
-    the first ``layers`` layers of the same request, all KV heads, repeated
-    until at least ``min_seconds`` have passed."""
+def cpu_baseline(cfg, s, min_seconds):
+    """The oracle timed on the host cores on the bounded samples of cpu_inputs,
+    each repeated until at least `min_seconds` have passed; reported in the
+    metric's units (select+pack GB/s of KV cache, decode tokens/s)."""
     import numpy as np
 
     import oracle
     if not os.path.exists(oracle.LIB_PATH):
         from oracle import build as ob
         ob.build()
-    layers = max(1, min(layers, cfg.L))
-    q = pre["q_win"][:, :layers].float().cpu().numpy()
-    k = pre["k"][:layers].float().cpu().numpy()
-    kraw = pre["k"][:layers].cpu().contiguous().view(__import__("torch").int16).numpy().view(np.uint16)
-    vraw = pre["v"][:layers].cpu().contiguous().view(__import__("torch").int16).numpy().view(np.uint16)
-    units = layers * cfg.Hkv
     threads = oracle.threads()
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        s = oracle.score(q, k, pre["cu_seqlens"], cfg.Hkv)
-        idx = oracle.topk(s.astype(np.float32), pre["cu_seqlens"], bud["cu_k"])
-        oracle.pack(kraw, vraw, idx, pre["cu_seqlens"], bud["cu_k"])
-        reps += 1
-        if time.perf_counter() - t0 >= min_seconds:
-            break
-    dt = (time.perf_counter() - t0) / reps
-    esize = 2 if cfg.dtype == "bf16" else 4
-    kv_bytes = 2 * units * pre["T"] * cfg.d * esize
-    # one thread on the first layer alone
-    oracle.set_threads(1)
-    try:
-        t1 = time.perf_counter()
-        s1 = oracle.score(q[:, :1], k[:1], pre["cu_seqlens"], cfg.Hkv)
-        i1 = oracle.topk(s1.astype(np.float32), pre["cu_seqlens"], bud["cu_k"])
-        oracle.pack(kraw[:1], vraw[:1], i1, pre["cu_seqlens"], bud["cu_k"])
-        dt1 = time.perf_counter() - t1
-    finally:
-        oracle.set_threads(threads)
-    kv1 = 2 * cfg.Hkv * pre["T"] * cfg.d * esize
+    cu = [0, s["n0"]]
+    ck = [0, s["k_b0"]]
+    units = cfg.L * cfg.Hkv
+
+    def select_once():
+        sc = oracle.score(s["q0"], s["k0"], cu, cfg.Hkv)
+        ix = oracle.topk(sc.astype(np.float32), cu, ck)
+        oracle.pack(s["kraw0"], s["vraw0"], ix, cu, ck, kv_layer_rows=0 if cfg.kv_shared_layers else None)
+
+    def decode_once():
+        oracle.decode_attn(*s["dec"])
+
+    def timed(fn):
+        reps = 0
+        t0 = time.perf_counter()
+        while True:
+            fn()
+            reps += 1
+            if time.perf_counter() - t0 >= min_seconds:
+                break
+        return (time.perf_counter() - t0) / reps, reps
+
+    dt, reps = timed(select_once)
+    kv_bytes = 2 * units * s["n0"] * cfg.d * s["esize"]
+    ddt, dreps = timed(decode_once)
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -806,13 +1107,18 @@ def cpu_baseline(cfg, pre, bud, layers, min_seconds):
                     break
     except OSError:
         pass
-    return {"value": round(kv_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": min(threads, units),
-            "kind": "oracle", "seconds_per_pass": round(dt, 3), "passes": reps,
-            "sample": f"score+topk+pack of layers 0..{layers - 1} ({units} of {cfg.L * cfg.Hkv} units), "
-                      f"same request, fp64 C oracle with OpenMP over units, repeated {reps}x",
-            "cpu_model": cpu, "host": platform.node(),
-            "single_thread": {"value": round(kv1 / dt1 / 1e9, 4), "unit": "GB/s", "seconds": round(dt1, 3),
-                              "sample": f"score+topk+pack of layer 0 ({cfg.Hkv} units), one thread"}}
+    dec_bytes = s["dec_rows"] * 2 * cfg.d * s["esize"]
+    B = s["dec"][4].shape[0]
+    return {"value": round(kv_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": min(threads, units), "kind": "oracle",
+            "seconds_per_pass": round(dt, 3), "passes": reps,
+            "sample": f"score+topk+pack of request 0 ({s['n0']} tokens), all {cfg.L} layers x {cfg.Hkv} KV heads "
+                      f"({units} units); fp64 C oracle, OpenMP over units, repeated {reps}x",
+            "decode": {"tokens_per_s": round(B / (ddt * cfg.L), 2), "gbs": round(dec_bytes / ddt / 1e9, 4),
+                       "seconds_per_pass": round(ddt, 3), "passes": dreps,
+                       "sample": f"decode attention of layer 0, decode step 0, all {B} requests x {cfg.Hkv} KV heads "
+                                 f"({s['dec_rows']} rows: seeded selection + extras at the workload's sizes); "
+                                 f"tokens/s = requests / (seconds per layer x {cfg.L} layers)"},
+            "cpu_model": cpu, "host": platform.node()}
 
 
 if __name__ == "__main__":
