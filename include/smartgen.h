@@ -13,7 +13,8 @@
  *                   (parallel on-demand transfer, Section 4.2; non-GDR mode,
  *                   Section 4.4)
  *   sg_decode_attn  decode attention over a partial KV set addressed through a
- *                   page table (Section 2.1; order invariance, Section 4.2)
+ *                   page table (Section 2.1; order invariance, Section 4.2);
+ *                   sg_decode_attn_noalloc, the same without a workspace
  *   sg_block_importance, sg_block_budget, sg_pack_blocks
  *                   block-granular proactive selection: eq. 1 block
  *                   importance, eq. 2 block budget, and the push of the chosen
@@ -36,7 +37,8 @@
  *     the GPU: device memory, or pinned host memory allocated with
  *     hipHostMalloc (device-accessible through the same address).  The library
  *     never allocates or frees memory; scratch comes from a caller workspace
- *     sized by the matching *_workspace_size call.
+ *     sized by the matching *_workspace_size call (sg_decode_attn_noalloc uses
+ *     a static device array of the library instead).
  *   - Scalars are checked on the host before anything is enqueued; a failing
  *     check returns a negative sg_status, enqueues nothing, and leaves a
  *     description in sg_last_error() (thread-local).  Device-resident metadata
@@ -290,6 +292,27 @@ int sg_decode_attn(void *stream, sg_dtype dt, int B, int Hq, int Hkv, int d, flo
                    const void *q, const void *k_pool, const void *v_pool, int64_t pool_rows,
                    const int32_t *page_table, const int32_t *n_rows, int page_size, int max_pages,
                    float *out, void *ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------- sg_decode_attn_noalloc
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * operation, arguments and kernels as sg_decode_attn, without a workspace.
+ * The split states live in a static device array of the library (one per
+ * GPU, sg_decode_attn_noalloc_scratch_bytes() = 16 MiB, held until the
+ * process ends); its device address is resolved once per device on the first
+ * call there, with that device current.  The call allocates and frees
+ * nothing.  A call whose split states would need more than the array holds
+ * returns SG_EWORKSPACE and enqueues nothing (sg_decode_attn with a caller
+ * workspace serves it).  Every call on one GPU shares that GPU's array and
+ * every split state is written before it is read, so nothing needs clearing;
+ * calls that overlap on one GPU (other streams, other threads) race on it and
+ * must be ordered by the caller.
+ */
+size_t sg_decode_attn_noalloc_scratch_bytes(void);
+int sg_decode_attn_noalloc(void *stream, sg_dtype dt, int B, int Hq, int Hkv, int d, float scale,
+                           const void *q, const void *k_pool, const void *v_pool, int64_t pool_rows,
+                           const int32_t *page_table, const int32_t *n_rows, int page_size, int max_pages,
+                           float *out);
 
 /* ---------------------------------------------------------------- block mode
  * Block-granular proactive selection (Section 4.1).  Per layer the sequence of

@@ -33,6 +33,8 @@
 // directly; otherwise the split's state goes to the workspace and a merge
 // kernel combines the splits in a fixed order.  All reductions have a fixed
 // order, so results are deterministic.
+#include <mutex>
+
 #include "sg_internal.h"
 
 namespace sg {
@@ -521,9 +523,9 @@ static int64_t plan_split_rows(int64_t wgs_per_split, int64_t max_rows, int page
 }
 
 template <typename T, int D, int G>
-static int launch_decode(hipStream_t s, int B, int Hq, int Hkv, float scale_log2, const void *q, const void *k_pool,
-                         const void *v_pool, int64_t pool_rows, const int32_t *page_table, const int32_t *n_rows,
-                         int page_size, int max_pages, float *out, float *ws, size_t ws_bytes) {
+static int launch_decode(const char *fn, hipStream_t s, int B, int Hq, int Hkv, float scale_log2, const void *q,
+                         const void *k_pool, const void *v_pool, int64_t pool_rows, const int32_t *page_table,
+                         const int32_t *n_rows, int page_size, int max_pages, float *out, float *ws, size_t ws_bytes) {
     constexpr int HG = G < DEC_MAX_HG ? G : DEC_MAX_HG;
     constexpr int NHG = G / HG;
     constexpr int WAVES = DecodeShape<T, D, HG>::WAVES;
@@ -535,12 +537,12 @@ static int launch_decode(hipStream_t s, int B, int Hq, int Hkv, float scale_log2
     // the device) whenever a unit's whole page row fits the LDS stage
     const int balanced = max_pages <= DEC_PT_CAP ? 1 : 0;
     if (nsplit > 65535 || nsplit > max_splits(max_rows)) {
-        set_error("sg_decode_attn: %lld splits of %lld rows are not supported", (long long)nsplit, (long long)split_rows);
+        set_error("%s: %lld splits of %lld rows are not supported", fn, (long long)nsplit, (long long)split_rows);
         return SG_EUNSUPPORTED;
     }
     const size_t need = nsplit > 1 ? (size_t)units * nsplit * G * (D + 2) * sizeof(float) : 0;
     if (need > ws_bytes || (need && !ws)) {
-        set_error("sg_decode_attn: workspace %zu < %zu", ws_bytes, need);
+        set_error("%s: the split states need %zu bytes of workspace, %zu given", fn, need, ws_bytes);
         return SG_EWORKSPACE;
     }
     // division by the page size as a multiply-shift, exact for dividends below
@@ -557,21 +559,87 @@ static int launch_decode(hipStream_t s, int B, int Hq, int Hkv, float scale_log2
         reinterpret_cast<const v4u *>(v_pool), pool_rows, page_table, n_rows, page_size, page_mul, page_shift,
         max_pages, split_rows, balanced, out, ws);
     if (nsplit > 1) decode_merge_kernel<D, G><<<(unsigned)units, 256, 0, s>>>(Hq, Hkv, (int)nsplit, ws, out);
-    return launch_status("sg_decode_attn");
+    return launch_status(fn);
 }
 
 template <typename T, int D>
-static int dispatch_g(int G, hipStream_t s, int B, int Hq, int Hkv, float sl2, const void *q, const void *kp,
+static int dispatch_g(const char *fn, int G, hipStream_t s, int B, int Hq, int Hkv, float sl2, const void *q, const void *kp,
                       const void *vp, int64_t pr, const int32_t *pt, const int32_t *nr, int ps, int mp, float *out,
                       float *ws, size_t wsb) {
     switch (G) {
-        case 1: return launch_decode<T, D, 1>(s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
-        case 2: return launch_decode<T, D, 2>(s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
-        case 4: return launch_decode<T, D, 4>(s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
-        case 8: return launch_decode<T, D, 8>(s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
-        case 16: return launch_decode<T, D, 16>(s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
-        default: set_error("sg_decode_attn: group size %d not supported (1, 2, 4, 8, 16)", G); return SG_EUNSUPPORTED;
+        case 1: return launch_decode<T, D, 1>(fn, s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
+        case 2: return launch_decode<T, D, 2>(fn, s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
+        case 4: return launch_decode<T, D, 4>(fn, s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
+        case 8: return launch_decode<T, D, 8>(fn, s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
+        case 16: return launch_decode<T, D, 16>(fn, s, B, Hq, Hkv, sl2, q, kp, vp, pr, pt, nr, ps, mp, out, ws, wsb);
+        default: set_error("%s: group size %d not supported (1, 2, 4, 8, 16)", fn, G); return SG_EUNSUPPORTED;
     }
+}
+
+// The checks and the dispatch shared by sg_decode_attn and
+// sg_decode_attn_noalloc (which differ only in where the split states live).
+static int decode_attn_call(const char *fn, void *stream, sg_dtype dt, int B, int Hq, int Hkv, int d, float scale,
+                            const void *q, const void *k_pool, const void *v_pool, int64_t pool_rows,
+                            const int32_t *page_table, const int32_t *n_rows, int page_size, int max_pages,
+                            float *out, void *ws, size_t ws_bytes) {
+    SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "%s: unknown dtype %d", fn, (int)dt);
+    SG_REQUIRE(B >= 0 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0, SG_EINVAL,
+               "%s: need Hq %% Hkv == 0 (Hq=%d, Hkv=%d)", fn, Hq, Hkv);
+    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "%s: head dimension %d not supported", fn, d);
+    SG_REQUIRE(page_size >= 1 && max_pages >= 1 && pool_rows >= 0, SG_EINVAL, "%s: bad page geometry", fn);
+    SG_REQUIRE((int64_t)max_pages * page_size <= (1ll << 30), SG_EINVAL, "%s: page table too large", fn);
+    SG_REQUIRE(pool_rows <= 0x7fffffffll, SG_EUNSUPPORTED, "%s: pool above 2^31 rows", fn);
+    SG_REQUIRE(scale == scale && scale > 0.f, SG_EINVAL, "%s: scale must be positive", fn);
+    if (B == 0) return SG_OK;
+    SG_REQUIRE(q && k_pool && v_pool && page_table && n_rows && out, SG_EINVAL, "%s: null pointer", fn);
+    SG_REQUIRE(aligned16(k_pool) && aligned16(v_pool) && aligned16(q), SG_EINVAL,
+               "%s: q and pools must be 16-byte aligned", fn);
+    SG_REQUIRE((int64_t)B * Hkv <= 0x7fffffffll, SG_EINVAL, "%s: too many units", fn);
+    const float sl2 = scale * 1.4426950408889634f;  // log2(e)
+    const int G = Hq / Hkv;
+    hipStream_t s = as_stream(stream);
+    float *w = reinterpret_cast<float *>(ws);
+    if (dt == SG_F32) {
+        if (d == 64) return dispatch_g<float, 64>(fn, G, s, B, Hq, Hkv, sl2, q, k_pool, v_pool, pool_rows, page_table, n_rows, page_size, max_pages, out, w, ws_bytes);
+        return dispatch_g<float, 128>(fn, G, s, B, Hq, Hkv, sl2, q, k_pool, v_pool, pool_rows, page_table, n_rows, page_size, max_pages, out, w, ws_bytes);
+    }
+    if (d == 64) return dispatch_g<uint16_t, 64>(fn, G, s, B, Hq, Hkv, sl2, q, k_pool, v_pool, pool_rows, page_table, n_rows, page_size, max_pages, out, w, ws_bytes);
+    return dispatch_g<uint16_t, 128>(fn, G, s, B, Hq, Hkv, sl2, q, k_pool, v_pool, pool_rows, page_table, n_rows, page_size, max_pages, out, w, ws_bytes);
+}
+
+// Split states of sg_decode_attn_noalloc: a file-scope device array, one copy
+// per GPU, held until the process ends.  Host code never passes the array's
+// name to a kernel (on the host it only stands for the symbol); it uses the
+// device address resolved once per device below.
+constexpr size_t DEC_SCRATCH_BYTES = (size_t)16 << 20;
+static __device__ __align__(256) char scratch[DEC_SCRATCH_BYTES];
+constexpr int DEC_SCRATCH_DEVICES = 64;
+
+// Device address of `scratch` on the current device, resolved with
+// hipGetSymbolAddress on the first call per device; nullptr (with the error
+// set) when that fails.
+static void *scratch_address(const char *fn) {
+    static std::mutex mu;
+    static void *addr[DEC_SCRATCH_DEVICES] = {};
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= DEC_SCRATCH_DEVICES) {
+        (void)hipGetLastError();
+        set_error("%s: no usable current device (%d)", fn, dev);
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            (void)hipGetLastError();
+            set_error("%s: hipGetSymbolAddress of the scratch array failed on device %d: %s", fn, dev,
+                      hipGetErrorString(e));
+            return nullptr;
+        }
+        addr[dev] = p;
+    }
+    return addr[dev];
 }
 
 }  // namespace sg
@@ -590,27 +658,18 @@ extern "C" int sg_decode_attn(void *stream, sg_dtype dt, int B, int Hq, int Hkv,
                               const void *k_pool, const void *v_pool, int64_t pool_rows, const int32_t *page_table,
                               const int32_t *n_rows, int page_size, int max_pages, float *out, void *ws,
                               size_t ws_bytes) {
-    SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "sg_decode_attn: unknown dtype %d", (int)dt);
-    SG_REQUIRE(B >= 0 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0, SG_EINVAL,
-               "sg_decode_attn: need Hq %% Hkv == 0 (Hq=%d, Hkv=%d)", Hq, Hkv);
-    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "sg_decode_attn: head dimension %d not supported", d);
-    SG_REQUIRE(page_size >= 1 && max_pages >= 1 && pool_rows >= 0, SG_EINVAL, "sg_decode_attn: bad page geometry");
-    SG_REQUIRE((int64_t)max_pages * page_size <= (1ll << 30), SG_EINVAL, "sg_decode_attn: page table too large");
-    SG_REQUIRE(pool_rows <= 0x7fffffffll, SG_EUNSUPPORTED, "sg_decode_attn: pool above 2^31 rows");
-    SG_REQUIRE(scale == scale && scale > 0.f, SG_EINVAL, "sg_decode_attn: scale must be positive");
-    if (B == 0) return SG_OK;
-    SG_REQUIRE(q && k_pool && v_pool && page_table && n_rows && out, SG_EINVAL, "sg_decode_attn: null pointer");
-    SG_REQUIRE(aligned16(k_pool) && aligned16(v_pool) && aligned16(q), SG_EINVAL,
-               "sg_decode_attn: q and pools must be 16-byte aligned");
-    SG_REQUIRE((int64_t)B * Hkv <= 0x7fffffffll, SG_EINVAL, "sg_decode_attn: too many units");
-    const float sl2 = scale * 1.4426950408889634f;  // log2(e)
-    const int G = Hq / Hkv;
-    hipStream_t s = as_stream(stream);
-    float *w = reinterpret_cast<float *>(ws);
-    if (dt == SG_F32) {
-        if (d == 64) return dispatch_g<float, 64>(G, s, B, Hq, Hkv, sl2, q, k_pool, v_pool, pool_rows, page_table, n_rows, page_size, max_pages, out, w, ws_bytes);
-        return dispatch_g<float, 128>(G, s, B, Hq, Hkv, sl2, q, k_pool, v_pool, pool_rows, page_table, n_rows, page_size, max_pages, out, w, ws_bytes);
-    }
-    if (d == 64) return dispatch_g<uint16_t, 64>(G, s, B, Hq, Hkv, sl2, q, k_pool, v_pool, pool_rows, page_table, n_rows, page_size, max_pages, out, w, ws_bytes);
-    return dispatch_g<uint16_t, 128>(G, s, B, Hq, Hkv, sl2, q, k_pool, v_pool, pool_rows, page_table, n_rows, page_size, max_pages, out, w, ws_bytes);
+    return decode_attn_call("sg_decode_attn", stream, dt, B, Hq, Hkv, d, scale, q, k_pool, v_pool, pool_rows,
+                            page_table, n_rows, page_size, max_pages, out, ws, ws_bytes);
+}
+
+extern "C" size_t sg_decode_attn_noalloc_scratch_bytes(void) { return DEC_SCRATCH_BYTES; }
+
+extern "C" int sg_decode_attn_noalloc(void *stream, sg_dtype dt, int B, int Hq, int Hkv, int d, float scale,
+                                      const void *q, const void *k_pool, const void *v_pool, int64_t pool_rows,
+                                      const int32_t *page_table, const int32_t *n_rows, int page_size, int max_pages,
+                                      float *out) {
+    void *ws = scratch_address("sg_decode_attn_noalloc");
+    if (!ws) return SG_EHIP;
+    return decode_attn_call("sg_decode_attn_noalloc", stream, dt, B, Hq, Hkv, d, scale, q, k_pool, v_pool, pool_rows,
+                            page_table, n_rows, page_size, max_pages, out, ws, DEC_SCRATCH_BYTES);
 }

@@ -26,7 +26,8 @@ EXPORTS = [
     "sg_pack_bytes", "sg_pack",
     "sg_split",
     "sg_fetch",
-    "sg_decode_attn_workspace_size", "sg_decode_attn",
+    "sg_decode_attn_workspace_size", "sg_decode_attn", "sg_decode_attn_noalloc_scratch_bytes",
+    "sg_decode_attn_noalloc",
     "sg_block_importance", "sg_block_budget", "sg_pack_blocks_bytes", "sg_pack_blocks",
     "sg_fetch_keep", "sg_spec_quota", "sg_spec_push", "sg_spec_commit", "sg_score_count",
     "sg_decode_select_workspace_size", "sg_decode_select",
@@ -67,6 +68,8 @@ def load() -> ctypes.CDLL:
     lib.sg_decode_attn_workspace_size.argtypes = [_i] * 6
     lib.sg_decode_attn_workspace_size.restype = _sz
     lib.sg_decode_attn.argtypes = [_vp, _i, _i, _i, _i, _i, _f, _vp, _vp, _vp, _l, _vp, _vp, _i, _i, _vp, _vp, _sz]
+    lib.sg_decode_attn_noalloc.argtypes = [_vp, _i, _i, _i, _i, _i, _f, _vp, _vp, _vp, _l, _vp, _vp, _i, _i, _vp]
+    lib.sg_decode_attn_noalloc_scratch_bytes.restype = _sz
     lib.sg_block_importance.argtypes = [_vp, _i, _i, _i, _vp, _l, _i, _vp, _vp]
     lib.sg_block_budget.argtypes = [_i, _i, ctypes.c_double, ctypes.c_double]
     lib.sg_block_budget.restype = _l
@@ -84,7 +87,8 @@ def load() -> ctypes.CDLL:
     lib.sg_spec_quota.restype = _l
     lib.sg_spec_push.argtypes = [_vp, _i, _i, _i, _i, _l, _l, _l, _i, _vp, _vp, _l, _vp, _vp, _l, _i, _vp, _vp, _vp]
     lib.sg_spec_commit.argtypes = [_vp, _i, _i, _l, _l, _l, _i, _i, _vp, _vp, _vp]
-    for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn", "sg_block_importance",
+    for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn", "sg_decode_attn_noalloc",
+              "sg_block_importance",
               "sg_pack_blocks", "sg_fetch_keep", "sg_spec_push", "sg_spec_commit", "sg_score_count",
               "sg_decode_select"):
         getattr(lib, f).restype = _i
@@ -362,6 +366,30 @@ def sg_decode_attn(q, k_pool, v_pool, page_table, n_rows, page_size, out, ws=Non
                                int(max_pages), _ptr(out), _ptr(ws),
                                0 if ws is None else ws.numel() * ws.element_size())
     _check("sg_decode_attn", rc)
+    return out
+
+
+def decode_noalloc_scratch_bytes() -> int:
+    return int(load().sg_decode_attn_noalloc_scratch_bytes())
+
+
+def sg_decode_attn_noalloc(q, k_pool, v_pool, page_table, n_rows, page_size, out, scale=None, stream=None):
+    """sg_decode_attn without a workspace: the split states live in the
+    library's static per-GPU scratch array (calls on one GPU must not overlap)."""
+    B, Hq, d = q.shape
+    Hkv, max_pages = page_table.shape[1], page_table.shape[2]
+    _need(k_pool.dtype == q.dtype and v_pool.dtype == q.dtype, "q and pools must share a dtype")
+    _need(out.dtype == torch.float32 and out.numel() >= B * Hq * d, "out must be float32 [B][Hq][d]")
+    if scale is None:
+        scale = d ** -0.5
+    pool_rows = k_pool.numel() // d
+    _need(v_pool.numel() >= pool_rows * d, "v_pool smaller than k_pool")
+    _need(page_table.shape[0] == B and n_rows.numel() >= B * Hkv, "page_table [B][Hkv][max_pages], n_rows [B][Hkv]")
+    _need(Hq % Hkv == 0, "Hq must be a multiple of Hkv")
+    rc = load().sg_decode_attn_noalloc(_stream(stream), _dtype_code(q), B, Hq, Hkv, d, float(scale), _ptr(q),
+                                       _ptr(k_pool), _ptr(v_pool), pool_rows, _ptr(page_table), _ptr(n_rows),
+                                       int(page_size), int(max_pages), _ptr(out))
+    _check("sg_decode_attn_noalloc", rc)
     return out
 
 
