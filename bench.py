@@ -54,6 +54,7 @@ FP32_MFMA_PEAK_TFLOPS = 157.3
 # the headline workload, and the sources whose hash it records (a changed
 # kernel makes the figure stale)
 TRAFFIC_SUMMARY = os.path.join(_ROOT, "profiles", "decode_attn.batched64.hbm_traffic.md")
+TRACE_SUMMARY = os.path.join(_ROOT, "profiles", "all_kernels.batched64.kernel_trace.md")
 TRAFFIC_SOURCES = ("paper_2607_28150_amd/csrc/decode_attn.hip", "paper_2607_28150_amd/csrc/sg_internal.h")
 REPS, WARM = 20, 3
 
@@ -625,8 +626,15 @@ def main():
                      "avg_launch_ms": round(t_attn / L, 5),
                      "basis": f"HIP events around each decode step's graph of {L} per-layer launches in the timed "
                               "steps (median), divided by the launches; includes the gaps between launches"},
+        "roofline_kernel_trace": None,
         "setup_s": round(setup_s, 1),
     }
+    kt = _summary_figure(TRACE_SUMMARY, "kernel_trace_avg_us")
+    if kt:
+        line["roofline_kernel_trace"] = {
+            "avg_launch_us": kt, "achieved": round(lb / (kt * 1e-6) / 1e9, 1),
+            "frac": r4(lb / (kt * 1e-6) / 1e9 / HBM_PEAK_GBS),
+            "basis": "rocprofv3 kernel-trace average of the same launches (committed summary), gaps excluded"}
     if not args.no_ops:
         ops = path_ops(p)
         ops["host_link"] = host_link()
@@ -998,21 +1006,27 @@ def sources_sha256(paths) -> str:
     return h.hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per decode launch from the committed counter summary
-    (FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy's reading), or None
-    when the summary is missing or the kernel sources changed since."""
+def _summary_figure(path, key):
+    """A figure of a committed profile summary, or None when the summary is
+    missing or the decode kernel's sources changed since it was taken."""
     import re
     try:
-        with open(TRAFFIC_SUMMARY) as f:
+        with open(path) as f:
             text = f.read()
     except OSError:
         return None
     h = re.search(r"^kernel_sources_sha256:\s*([0-9a-f]{64})\s*$", text, re.M)
-    t = re.search(r"^traffic_bytes_per_launch:\s*([0-9]+)\s*$", text, re.M)
+    t = re.search(r"^" + key + r":\s*([0-9.]+)\s*$", text, re.M)
     if not h or not t or h.group(1) != sources_sha256(TRAFFIC_SOURCES):
         return None
-    return int(t.group(1))
+    return float(t.group(1))
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy's reading)."""
+    v = _summary_figure(TRAFFIC_SUMMARY, "traffic_bytes_per_launch")
+    return None if v is None else int(v)
 
 
 # --------------------------------------------------------------------------- oracle baseline

@@ -246,6 +246,9 @@ def _paged_set(g, B, Hkv, d, nmax, P, td, empty_some=True):
     ("f32", 128, 8, 500, 16, 2),
     ("f32", 64, 4, 611, 2, 3),
     ("f32", 128, 4, 410, 16, 140),
+    # more units than CUs, one row per lane group and two head groups
+    ("f32", 64, 1, 204, 16, 129),
+    ("bf16", 64, 16, 300, 4, 130),
 ])
 def test_decode_parity(gpu_lib, dtype, d, G, nmax, P, B):
     g = np.random.default_rng(nmax + G + d + P)
@@ -297,7 +300,8 @@ def test_decode_invalid_pages_are_skipped(gpu_lib):
     n = np.array([[64]], np.int32)
     q = torch.randn((1, 4, d)).to(torch.bfloat16)
     out = torch.empty((1, 4, d), device="cuda")
-    gpu_lib.sg_decode_attn(q.cuda(), kp.cuda(), vp.cuda(), cu(pages), cu(n), P, out)
+    ws = torch.empty(max(16, gpu_lib.decode_workspace_size(1, 4, 1, d, 4, P)), dtype=torch.uint8, device="cuda")
+    gpu_lib.sg_decode_attn(q.cuda(), kp.cuda(), vp.cuda(), cu(pages), cu(n), P, out, ws=ws)
     torch.cuda.synchronize()
     ref = oracle.decode_attn(f32(q), f32(kp), f32(vp), pages, n, P)
     np.testing.assert_allclose(out.cpu().numpy(), ref, atol=2e-2, rtol=0)
