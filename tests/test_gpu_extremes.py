@@ -1,0 +1,170 @@
+"""GPU parity where the kernels leave their common paths: decode attention
+whose reference maximum must be raised mid-stream (a row 20-40 nats above the
+rest, late in a wavefront's range and in a later split), scores whose logits
+pass +-45 nats (the exact statistics fallback), bf16 decode checked far
+inside the stated tolerance, and a row-coverage case in which every logical
+row leaves its own trace in the output."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from datagen import inputs
+from datagen.configs import Config
+from tests.gpu_util import assert_scores_close, cu, f32, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _pool(g, B, Hkv, d, rows, P, td):
+    """Contiguous per-unit pages at seeded random pool pages; K, V ~ N(0, 1)."""
+    npg = max(-(-max(rows) // P), 1)
+    units = B * Hkv
+    perm = g.permutation(units * npg + 2)[: units * npg]
+    pages = (perm.reshape(B, Hkv, npg) * P).astype(np.int32)
+    pool_rows = (units * npg + 2) * P
+    k = g.standard_normal((pool_rows, d)).astype(np.float32)
+    v = g.standard_normal((pool_rows, d)).astype(np.float32)
+    n = np.array(rows, np.int32).reshape(B, Hkv)
+    return pages, n, k, v
+
+
+def _pool_row(pages, b, h, r, P):
+    return int(pages[b, h, r // P]) + r % P
+
+
+def _run_decode(gpu_lib, q, k, v, pages, n, P, td):
+    B, Hq, d = q.shape
+    Hkv = pages.shape[1]
+    out = torch.full((B, Hq, d), float("nan"), device="cuda")
+    ws = torch.empty(max(16, gpu_lib.decode_workspace_size(B, Hq, Hkv, d, pages.shape[2], P)), dtype=torch.uint8,
+                     device="cuda")
+    qt, kt, vt = (torch.from_numpy(x).to(td).cuda() for x in (q, k, v))
+    gpu_lib.sg_decode_attn(qt, kt, vt, cu(pages), cu(n), P, out, ws=ws)
+    torch.cuda.synchronize()
+    ref = oracle.decode_attn(f32(qt), f32(kt), f32(vt), pages, n, P)
+    return out.cpu().numpy(), ref
+
+
+# (dtype, G, B, Hkv, rows per unit): few units (rows split over several
+# workgroups) and more units than CUs (one workgroup of four wavefronts each)
+@pytest.mark.parametrize("dtype,G,B,Hkv,nrows", [
+    ("f32", 4, 1, 2, 1500),
+    ("f32", 8, 1, 2, 1500),
+    ("bf16", 4, 1, 2, 1500),
+    ("f32", 4, 130, 2, 400),
+    ("bf16", 8, 130, 2, 400),
+])
+def test_decode_reference_max_raised_mid_stream(gpu_lib, dtype, G, B, Hkv, nrows):
+    d, P = 128, 16
+    say("decode rescale", dtype, G, B, Hkv, nrows)
+    g = np.random.default_rng(1000 + G + B)
+    td = torch.float32 if dtype == "f32" else torch.bfloat16
+    Hq = G * Hkv
+    rows = [nrows] * (B * Hkv)
+    pages, n, k, v = _pool(g, B, Hkv, d, rows, P, td)
+    base = g.standard_normal((B, Hkv, d)).astype(np.float32)
+    q = (base[:, :, None, :] + 0.3 * g.standard_normal((B, Hkv, G, d))).astype(np.float32).reshape(B, Hq, d)
+    if dtype == "bf16":
+        q = torch.from_numpy(q).to(torch.bfloat16).float().numpy()
+    # per unit, rows whose logits stand above the rest for every head of the
+    # group: a moderate one early, then 20-40 nats higher ones later in the
+    # same wavefront's and later workgroups' ranges
+    for b in range(B):
+        for h in range(Hkv):
+            qs = q[b, h * G:(h + 1) * G]
+            u = qs.mean(axis=0)
+            u /= np.linalg.norm(u)
+            proj = qs @ u                                  # every head's component along u (positive)
+            for r, nats in ((5, 6.0), (nrows // 3 + 37, 28.0), (nrows - 9, 40.0), (2 * nrows // 3 + 11, 22.0)):
+                pr = _pool_row(pages, b, h, r, P)
+                k[pr] = 0.02 * k[pr] + u * (nats * np.sqrt(d) / proj.min())
+    if dtype == "bf16":
+        k = torch.from_numpy(k).to(torch.bfloat16).float().numpy()
+    got, ref = _run_decode(gpu_lib, q, k, v, pages, n, P, td)
+    assert np.isfinite(got).all()
+    np.testing.assert_allclose(got, ref, atol=1e-4, rtol=0)
+
+
+@pytest.mark.parametrize("G", [4, 8])
+def test_decode_bf16_far_inside_tolerance(gpu_lib, G):
+    """bf16 inputs, fp32 accumulation: against the fp64 oracle on the widened
+    inputs the outputs agree to 1e-4, far inside the stated 2e-2, so a dropped
+    or repeated row (about 1/n of an output) cannot hide."""
+    d, P, B, Hkv = 128, 16, 3, 8
+    say("decode bf16 tight", G)
+    g = np.random.default_rng(77 + G)
+    rows = list(g.integers(600, 2400, B * Hkv))
+    pages, n, k, v = _pool(g, B, Hkv, d, rows, P, torch.bfloat16)
+    q = (2 * g.standard_normal((B, G * Hkv, d))).astype(np.float32)
+    got, ref = _run_decode(gpu_lib, q, k, v, pages, n, P, torch.bfloat16)
+    np.testing.assert_allclose(got, ref, atol=2e-2, rtol=0)
+    assert np.abs(got - ref).max() <= 1e-4
+
+
+@pytest.mark.parametrize("dtype,G,B,Hkv,nrows,P", [
+    ("bf16", 4, 2, 2, 1337, 16),      # rows split over several workgroups
+    ("bf16", 8, 130, 2, 211, 16),     # one workgroup per unit
+    ("f32", 4, 1, 3, 700, 1),         # per-row index table
+])
+def test_decode_every_row_counted_once(gpu_lib, dtype, G, B, Hkv, nrows, P):
+    """Equal keys give every row the same weight 1/n; V row r is (1 + r // d)
+    at column r % d and zero elsewhere, so output column c is
+    sum over r = c (mod d) of (1 + r // d) / n: dropping or repeating any row
+    changes its column by at least 1/n."""
+    d = 128
+    say("decode row coverage", dtype, G, B, Hkv, nrows, P)
+    g = np.random.default_rng(5 + G)
+    td = torch.float32 if dtype == "f32" else torch.bfloat16
+    rows = [nrows - (3 * i) % (nrows // 2) for i in range(B * Hkv)]
+    pages, n, k, v = _pool(g, B, Hkv, d, rows, P, td)
+    k[:] = 0.5
+    v[:] = 0.0
+    for b in range(B):
+        for h in range(Hkv):
+            for r in range(int(n[b, h])):
+                pr = _pool_row(pages, b, h, r, P)
+                v[pr, r % d] = 1 + r // d
+    q = g.standard_normal((B, G * Hkv, d)).astype(np.float32)
+    got, ref = _run_decode(gpu_lib, q, k, v, pages, n, P, td)
+    for b in range(B):
+        for h in range(Hkv):
+            nn = int(n[b, h])
+            want = np.zeros(d)
+            for r in range(nn):
+                want[r % d] += (1 + r // d) / nn
+            np.testing.assert_allclose(ref[b, h * G:(h + 1) * G], np.broadcast_to(want, (G, d)), atol=1e-12)
+            np.testing.assert_allclose(got[b, h * G:(h + 1) * G], np.broadcast_to(want, (G, d)), atol=2e-5)
+            assert (1.0 / nn) > 20 * 2e-5
+
+
+@pytest.mark.parametrize("scale", [12.0, -12.0, 25.0])
+def test_score_logits_beyond_45_nats(gpu_lib, scale):
+    """Window queries scaled so logits pass +-45 nats: blocks whose terms leave
+    the fast path's range take the exact update."""
+    cfg = Config(name="t", L=2, Hq=8, Hkv=2, d=128, dtype="bf16", W=32, budget_bp=1000, extra_bp=0, steps=1,
+                 seqlens=(1500, 700), B=2, heavy_bp=100, sinks=4, seed=21)
+    say("score extreme logits", scale)
+    pre = inputs.make_prefill(cfg, device="cuda", want_v=False)
+    # scale half the window rows up, half down (per q head), so rows reach both ends
+    sgn = torch.ones(cfg.Hq, device="cuda")
+    sgn[::2] = -1.0
+    q = (pre["q_win"].float() * scale * sgn[None, None, :, None, None]).to(torch.bfloat16).contiguous()
+    qf = f32(q)
+    kf = f32(pre["k"])
+    zmax = 0.0
+    c = pre["cu_seqlens"]
+    for b in range(cfg.B):
+        for l in range(cfg.L):
+            for hq in range(cfg.Hq):
+                z = qf[b, l, hq] @ kf[l, hq // (cfg.Hq // cfg.Hkv), c[b]:c[b + 1]].T / np.sqrt(cfg.d)
+                zmax = max(zmax, float(np.abs(z).max()))
+    assert zmax > 45.0
+    T = pre["T"]
+    scores = torch.full((cfg.L, cfg.Hkv, T), float("nan"), device="cuda")
+    ws = torch.empty(gpu_lib.score_workspace_size(cfg.B, cfg.L, cfg.Hq, cfg.Hkv, cfg.d, cfg.W, max(cfg.seqlens)),
+                     dtype=torch.uint8, device="cuda")
+    gpu_lib.sg_score(q, pre["k"], cu(c), T, max(cfg.seqlens), cfg.Hkv, scores, ws=ws)
+    torch.cuda.synchronize()
+    ref = oracle.score(qf, kf, c, cfg.Hkv)
+    assert_scores_close(scores.cpu().numpy(), ref)

@@ -26,9 +26,12 @@ def _widen(a):
     return (a.astype(np.uint32) << 16).view(np.float32)
 
 
-def test_batched64_headline_step(gpu_lib):
+@pytest.mark.parametrize("seed", [None, 105])
+def test_batched64_headline_step(gpu_lib, seed):
     cfg = configs.get("batched64")
-    say("headline batched64: inputs")
+    if seed is not None:
+        cfg = cfg.with_(seed=seed)
+    say("headline batched64: inputs, seed", cfg.seed)
     p = bench.Path(gpu_lib, cfg, decode_steps=1)
     sel = inputs.random_selection(cfg, p.lens, p.kb, device="cuda", tag_extra=5)
     say("headline batched64: prepare (pack, receive, mask, index, graph)")

@@ -26,6 +26,11 @@ def rows_as_f32(a: np.ndarray, dtype: torch.dtype) -> np.ndarray:
     return bf16_bits_to_f32(a) if dtype == torch.bfloat16 else a.view(np.float32)
 
 
+def _seeded(cfg, seed):
+    """The workload as configured, or re-drawn from another seed (the robustness reruns)."""
+    return cfg if seed is None else cfg.with_(seed=seed)
+
+
 def _score_units(gpu_lib, cfg, pre, units):
     """GPU scores of the whole workload, compared with the oracle on `units` = [(l, h)]."""
     T, lens = pre["T"], pre["seqlens"]
@@ -145,9 +150,10 @@ def _decode_check(gpu_lib, q, kp, vp, pt, nr, P, ref_k, ref_v, ref_pt, seqs=None
 
 # ----------------------------------------------------------------------------- tiny (whole pipeline, in full)
 
-def test_tiny_whole_pipeline(gpu_lib):
-    cfg = configs.get("tiny")
-    say("workload tiny")
+@pytest.mark.parametrize("seed", [None, 101])
+def test_tiny_whole_pipeline(gpu_lib, seed):
+    cfg = _seeded(configs.get("tiny"), seed)
+    say("workload tiny", "seed", cfg.seed)
     pre = inputs.make_prefill(cfg, device="cuda")
     lens, T = pre["seqlens"], pre["T"]
     bud = inputs.make_budget(cfg, lens)
@@ -181,9 +187,10 @@ def test_tiny_whole_pipeline(gpu_lib):
 
 # ----------------------------------------------------------------------------- Llama-3-8B shape, 8K prompt
 
-def test_llama8b_8k(gpu_lib):
-    cfg = configs.get("llama8b_8k")
-    say("workload llama8b_8k")
+@pytest.mark.parametrize("seed", [None, 102])
+def test_llama8b_8k(gpu_lib, seed):
+    cfg = _seeded(configs.get("llama8b_8k"), seed)
+    say("workload llama8b_8k", "seed", cfg.seed)
     pre = inputs.make_prefill(cfg, device="cuda")
     bud = inputs.make_budget(cfg, pre["seqlens"])
     K = bud["K_total"]
@@ -304,9 +311,10 @@ def _layer_rows(kr, vr, i, cfg, K):
     return kr[i * n:(i + 1) * n], vr[i * n:(i + 1) * n]
 
 
-def test_llama8b_32k_long_context(gpu_lib):
-    cfg = configs.get("llama8b_32k")
-    say("workload llama8b_32k")
+@pytest.mark.parametrize("seed", [None, 103])
+def test_llama8b_32k_long_context(gpu_lib, seed):
+    cfg = _seeded(configs.get("llama8b_32k"), seed)
+    say("workload llama8b_32k", "seed", cfg.seed)
     pre = inputs.make_prefill(cfg, device="cuda")
     bud = inputs.make_budget(cfg, pre["seqlens"])
     K = bud["K_total"]
@@ -326,9 +334,10 @@ def test_llama8b_32k_long_context(gpu_lib):
 
 # ----------------------------------------------------------------------------- 70B-shaped slice, pinned-host staging
 
-def test_llama70b_16k_staging(gpu_lib):
-    cfg = configs.get("llama70b_16k")
-    say("workload llama70b_16k")
+@pytest.mark.parametrize("seed", [None, 104])
+def test_llama70b_16k_staging(gpu_lib, seed):
+    cfg = _seeded(configs.get("llama70b_16k"), seed)
+    say("workload llama70b_16k", "seed", cfg.seed)
     pre = inputs.make_prefill(cfg, device="cuda")
     bud = inputs.make_budget(cfg, pre["seqlens"])
     K = bud["K_total"]
@@ -349,9 +358,10 @@ def test_llama70b_16k_staging(gpu_lib):
 
 # ----------------------------------------------------------------------------- 64 varlen requests, paged
 
-def test_batched64_paged(gpu_lib):
-    cfg = configs.get("batched64")
-    say("workload batched64")
+@pytest.mark.parametrize("seed", [None, 105])
+def test_batched64_paged(gpu_lib, seed):
+    cfg = _seeded(configs.get("batched64"), seed)
+    say("workload batched64", "seed", cfg.seed)
     pre = inputs.make_prefill(cfg, device="cuda")
     lens = pre["seqlens"]
     assert min(lens) >= 2048 and max(lens) <= 32768
