@@ -65,7 +65,14 @@
 extern "C" {
 #endif
 
-typedef enum { SG_F32 = 0, SG_BF16 = 1 } sg_dtype;
+typedef enum {
+    SG_F32 = 0,
+    SG_BF16 = 1,
+    /* range markers: a dtype argument may hold any int (others are rejected
+       with SG_EINVAL); they give the enum the range of int in C++ too */
+    SG_DTYPE_INT_MIN_ = -2147483647 - 1,
+    SG_DTYPE_INT_MAX_ = 2147483647
+} sg_dtype;
 
 typedef enum {
     SG_OK = 0,

@@ -14,7 +14,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsg_oracle.so")
+# SG_ORACLE_LIB points at another build of the same source (the sanitizer run)
+LIB_PATH = os.environ.get("SG_ORACLE_LIB") or os.path.join(_HERE, "libsg_oracle.so")
 _lib = None
 
 _i32p = ctypes.POINTER(ctypes.c_int32)

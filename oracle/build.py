@@ -12,11 +12,15 @@ import sys
 _HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, sanitize: bool = False, out: str | None = None) -> str:
+    """Builds libsg_oracle.so; with `sanitize`, an AddressSanitizer and
+    UndefinedBehaviorSanitizer build (load it with gcc's libasan preloaded)."""
     src = os.path.join(_HERE, "sg_oracle.c")
-    out = os.path.join(_HERE, "libsg_oracle.so")
+    out = out or os.path.join(_HERE, "libsg_oracle.so")
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+    opt = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=undefined"] if sanitize else ["-O2"]
+    cmd = ["gcc", "-std=c11", *opt, "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
            "-fno-fast-math", src, "-o", tmp, "-lm"]
     if verbose:
         print(" ".join(cmd))

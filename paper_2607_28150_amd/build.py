@@ -59,5 +59,32 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     return LIB_PATH
 
 
+def build_host_sanitized(out_path: str, jobs: int = 8) -> str:
+    """The library with its host code (argument checks, dispatch) built with
+    AddressSanitizer and UndefinedBehaviorSanitizer (device code unoptimised:
+    this build is for CPU-only checks of the host side).  Load it with the
+    clang ASan runtime preloaded."""
+    srcs = sorted(glob.glob(os.path.join(_HERE, "csrc", "*.hip")))
+    bdir = os.path.join(os.path.dirname(os.path.abspath(out_path)), "objs")
+    os.makedirs(bdir, exist_ok=True)
+    objs = [os.path.join(bdir, os.path.basename(s)[:-4] + ".o") for s in srcs]
+    san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+           "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+    flags = ["-Xarch_host", "-O1", "-Xarch_host", "-g", "-Xarch_device", "-O0", "-std=c++17", "-fPIC",
+             f"--offload-arch={ARCH}", *san,
+             "-I", os.path.join(_ROOT, "include")]
+
+    def one(so):
+        r = subprocess.run([_hipcc(), *flags, "-c", so[0], "-o", so[1]], capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc (host, sanitized) failed for {so[0]}:\n{r.stderr}")
+
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        list(ex.map(one, zip(srcs, objs)))
+    subprocess.run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *san, *objs, "-o", out_path], check=True,
+                   capture_output=True)
+    return out_path
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

@@ -14,7 +14,8 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsmartgen.so")
+# SG_LIB_PATH points at another build of the same sources (the sanitizer run)
+LIB_PATH = os.environ.get("SG_LIB_PATH") or os.path.join(_HERE, "libsmartgen.so")
 
 SG_F32, SG_BF16 = 0, 1
 SG_OK, SG_EINVAL, SG_EUNSUPPORTED, SG_EWORKSPACE, SG_EHIP, SG_EINTERNAL = 0, -1, -2, -3, -4, -5

@@ -56,7 +56,6 @@ def test_sizes(lib):
     assert smartgen.decode_workspace_size(1, 32, 8, 128, 1, 16) == 0          # one split: no workspace
     # workspace bound: 2400 units x up to 8 splits of 128 rows x 4 heads x 130 floats
     assert smartgen.decode_workspace_size(300, 32, 8, 128, 64, 16) == 2400 * 8 * 4 * 130 * 4
-
     assert smartgen.decode_workspace_size(2, 32, 8, 128, 64, 16) == 2 * 8 * 8 * 4 * 130 * 4   # <= 8 splits of 128 rows
 
 
