@@ -804,12 +804,16 @@ def decode_side(sg, nsteps=12, long_steps=256, ratio_bp=1000, M=1024):
     ev = _ev
     counts = torch.empty((nidx, 2, rows), dtype=torch.int32, device=dev)
 
-    def run(mode, quota_blocks=quota, steps=nsteps):
+    def run(mode, quota_blocks=quota, steps=nsteps, serving=False):
+        # serving: the host waits for every step before it launches the next,
+        # as a serving loop does (it needs the step's token), so the pusher's
+        # completion checks see the device's progress
         reset()
         pusher = SpecPusher(src_k, src_v, imp.view(-1), 0, N, M, store_k, store_v, mask, quota_blocks) \
             if mode.startswith("speculative") else None
         torch.cuda.synchronize()
         t = []
+        t_host = time.perf_counter()
         for s in range(steps):
             a, b = ev(), ev()
             a.record(main)
@@ -835,6 +839,8 @@ def decode_side(sg, nsteps=12, long_steps=256, ratio_bp=1000, M=1024):
             counts[s, 0].copy_(buf.n_remote)
             counts[s, 1].copy_(buf.n_kept)
             t.append((a, b))
+            if serving:
+                b.synchronize()
         torch.cuda.synchronize()
         c = counts[:steps].double().sum(dim=2).cpu().numpy()
         ratio = c[:, 0] / c[:, 1]
@@ -851,6 +857,8 @@ def decode_side(sg, nsteps=12, long_steps=256, ratio_bp=1000, M=1024):
                         "on_demand_ratio_mean": r4(ratio.mean())})
         if pusher is not None:
             res.update({"pushes_done": pusher.pushes, "blocks_left": pusher.left})
+        if serving:
+            res["ms_total_host_clock"] = round((time.perf_counter() - t_host) * 1e3, 2)
         return res
 
     res = {"workload": cfg.name, "steps": nsteps, "rows_per_unit": per, "selected": kb, "extras": e}
@@ -861,8 +869,9 @@ def decode_side(sg, nsteps=12, long_steps=256, ratio_bp=1000, M=1024):
     res["speculative"]["pushes_to_complete"] = -(-LM // quota)
     # the workload's whole decode: two lanes with reuse, without and with
     # speculative transfer, cumulative time over every step
-    res["over_all_steps"] = {"two_lane": run("two_lane", steps=long_steps),
-                             "speculative": run("speculative", steps=long_steps)}
+    res["over_all_steps"] = {"two_lane": run("two_lane", steps=long_steps, serving=True),
+                             "speculative": run("speculative", steps=long_steps, serving=True),
+                             "note": "the host waits for each step before launching the next (a serving loop)"}
     a, b2 = res["over_all_steps"]["two_lane"]["ms_total"], res["over_all_steps"]["speculative"]["ms_total"]
     res["over_all_steps"]["speculative_speedup"] = round(a / b2, 3)
     # lane rates and interference, each on its own
