@@ -27,11 +27,12 @@ void clear_error();
 // map the state after a launch to a status
 int launch_status(const char *what);
 // True for pinned host memory (reached over the host link).  Copies from it
-// run on HOST_LINK_WORKGROUPS workgroups, about 0.5 MB of reads in flight:
-// measured on MI355X, that keeps the link at its full rate (57 GB/s), while
-// every further outstanding host read also delays the HBM reads of kernels
-// on other streams (decode attention beside a host-source copy ran 1.5x
-// slower with 16 workgroups, 2.7x with 32 and 7x with 64 or more).
+// run on HOST_LINK_WORKGROUPS workgroups, two per XCD (host reads are served
+// per XCD: 8 workgroups reached 33 GB/s, 12 reached 48): measured on MI355X,
+// that keeps the link near its full rate (57 GB/s), while every further
+// outstanding host read also delays the HBM reads of kernels on other streams
+// (decode attention beside a host-source copy ran 1.5x slower with 16
+// workgroups, 2.7x with 32 and 7x with 64 or more).
 bool host_memory(const void *p);
 constexpr int HOST_LINK_WORKGROUPS = 16;
 
