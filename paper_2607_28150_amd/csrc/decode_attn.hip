@@ -2,8 +2,12 @@
 //
 // Grid: x = (sequence, KV head) unit, y = split of the unit's rows (one split
 // whenever the units fill the chip), z = group of up to 8 q heads of the KV
-// head.  A workgroup serves all the q heads of its group, so each K/V row is
-// read from HBM once per step (twice for 16-head groups).
+// head.  Between one and four units per CU the grid is instead one-dimensional
+// over (shader engine, part): every unit is cut into four equal parts, one per
+// engine of its XCD, and each engine takes its parts longest first (the
+// equal-parts mode in the kernel).  A workgroup serves all the q heads of its
+// group, so each K/V row is read from HBM once per step (twice for 16-head
+// groups).
 //
 // Memory side.  The split's page entries are staged in LDS once (one round
 // trip, overlapped with the query loads); every wavefront owns one contiguous
@@ -88,6 +92,14 @@ constexpr int DEC_MAX_HG = 8;       // heads served by one workgroup; larger gro
 constexpr int DEC_PT_CAP = 2048;    // page entries of one split staged in LDS
 constexpr int DEC_MIN_SPLIT_ROWS = 128;
 constexpr int64_t DEC_CAP_ROWS = 1024;    // split length when units number one to four per CU
+// The workgroup dispatcher of MI355X sends consecutive workgroup ids round
+// robin over its 8 XCDs, and the ids an XCD receives round robin over its 4
+// shader engines (measured: workgroup L runs on XCD L mod 8 and on engine
+// (L / 8) mod 4 of that XCD's rotation), each engine then filling its own
+// CUs.  Work handed to one engine never moves to another.
+constexpr int DEC_XCDS = 8;
+constexpr int DEC_ENGINES = 4;
+constexpr int DEC_BIN_MAX = 128;          // units of one XCD in the equal-parts mode
 constexpr float DEC_LAZY = 16.f;    // log2 headroom before the reference max is raised
 
 // partial state of one split: per head (m, l) then o[d]
@@ -137,7 +149,7 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     int Hq, int Hkv, float scale_log2, const T *__restrict__ q, const v4u *__restrict__ k_pool,
     const v4u *__restrict__ v_pool, int64_t pool_rows, const int32_t *__restrict__ page_table,
     const int32_t *__restrict__ n_rows, int page_size, uint32_t page_mul, int page_shift, int max_pages,
-    int64_t split_rows, float *__restrict__ out, float *__restrict__ ws) {
+    int64_t split_rows, float *__restrict__ out, float *__restrict__ ws, int nunits, int parts) {
     using S = DecodeShape<T, D, HG>;
     constexpr int PER16 = Elem<T>::PER16;  // elements per 16-byte vector
     constexpr int LPR = S::LPR, VPL = S::VPL, RPS = S::RPS, WAVES = S::WAVES, NS = S::NS;
@@ -152,13 +164,74 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     __shared__ int32_t pte[DEC_PT_CAP];
     __shared__ float m_s[WAVES][HG], l_s[NPART][HG];
 
-    const int64_t unit = blockIdx.x;        // b * Hkv + h
-    const int b = (int)(unit / Hkv), h = (int)(unit % Hkv);
-    const int split = blockIdx.y, nsplit = gridDim.y;
-    const int G = Hq / Hkv;
-    const int gq0 = h * G + (int)blockIdx.z * HG;      // first q head served
     const int tid = threadIdx.x, lane = tid % 64;
     const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
+    const int64_t max_rows = (int64_t)max_pages * page_size;
+
+    // Which rows this workgroup reads: [r0, rend) of unit `unit`.
+    //   split mode: unit blockIdx.x, fixed split blockIdx.y of split_rows rows;
+    //   equal-parts mode (parts > 0, a one-dimensional grid): workgroup L
+    //     belongs to the engine bin (x, k) = (L mod 8, (L / 8) mod 4) and
+    //     takes part k of the (L / 32)-th longest unit among the bin's units
+    //     x, x + 8, ..., each unit cut into `parts` equal parts.  Every engine
+    //     so receives the same share of every unit, and each engine's queue
+    //     runs longest first.
+    int64_t unit, n, r0, rend;
+    int split, nsplit;
+    if (parts > 0) {
+        static_assert(DEC_BIN_MAX == 128 && WAVES == 4, "the rank below splits 128 members over 4 quarters");
+        __shared__ __attribute__((aligned(16))) int32_t bin_n[DEC_BIN_MAX];
+        __shared__ int32_t chosen;
+        const int L = (int)blockIdx.x;
+        const int bx = L % DEC_XCDS, bk = (L / DEC_XCDS) % DEC_ENGINES, bj = L / (DEC_XCDS * DEC_ENGINES);
+        const int members = (nunits - bx + DEC_XCDS - 1) / DEC_XCDS;
+        if (bj >= members) return;          // uniform: the bins' last slots past the units
+        if (tid < DEC_BIN_MAX)
+            bin_n[tid] = tid < members
+                             ? (int32_t)max<int64_t>(0, min<int64_t>(n_rows[bx + (int64_t)DEC_XCDS * tid], max_rows))
+                             : -1;
+        __syncthreads();
+        // rank of member m = the members longer than it, or as long and listed
+        // earlier.  Four adjacent threads count for one member, each over a
+        // quarter of the list (32 entries, eight 16-byte LDS reads), and quad
+        // DPP adds join the counts; 64 members per pass.
+        for (int mbase = 0; mbase < members; mbase += 64) {
+            const int m = mbase + tid / 4, qtr = tid % 4;
+            const int32_t v = m < members ? bin_n[m] : -1;
+            const int4 *row = reinterpret_cast<const int4 *>(bin_n + qtr * 32);
+            int cnt = 0;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int4 w = row[i];
+                const int t = qtr * 32 + 4 * i;
+                cnt += (w.x > v) || (w.x == v && t < m);
+                cnt += (w.y > v) || (w.y == v && t + 1 < m);
+                cnt += (w.z > v) || (w.z == v && t + 2 < m);
+                cnt += (w.w > v) || (w.w == v && t + 3 < m);
+            }
+            cnt += __builtin_amdgcn_update_dpp(0, cnt, DPP_XOR1, 0xf, 0xf, false);
+            cnt += __builtin_amdgcn_update_dpp(0, cnt, DPP_XOR2, 0xf, 0xf, false);
+            if (qtr == 0 && m < members && cnt == bj) chosen = m;
+        }
+        __syncthreads();
+        const int sel = min(max((int)chosen, 0), members - 1);   // the ranks are a permutation: one match
+        unit = bx + (int64_t)DEC_XCDS * sel;
+        n = bin_n[sel];
+        split = bk;
+        nsplit = parts;
+        r0 = n * bk / parts;
+        rend = n * (bk + 1) / parts;
+    } else {
+        unit = blockIdx.x;
+        split = blockIdx.y;
+        nsplit = gridDim.y;
+        r0 = (int64_t)split * split_rows;
+        rend = r0 + split_rows;
+        n = -1;                           // loaded below, beside the query and the page entries
+    }
+    const int b = (int)(unit / Hkv), h = (int)(unit % Hkv);
+    const int G = Hq / Hkv;
+    const int gq0 = h * G + (int)blockIdx.z * HG;      // first q head served
     const int c = lane % LPR, r = lane / LPR;       // slice within the row, row within the step
 
     // this lane's slices of the HG query vectors: vectors j * LPR + c, j < VPL
@@ -170,20 +243,17 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
 #pragma unroll
             for (int j = 0; j < VPL; ++j) qs[g][j] = qv[g * CPR + j * LPR + c];
     }
-    // page entries covering the split's rows [r0, r0 + split_rows)
-    const int64_t max_rows = (int64_t)max_pages * page_size;
-    const int64_t r0 = (int64_t)split * split_rows;
+    // page entries covering the rows [r0, rend)
     const int64_t pg0 = r0 / page_size;
-    const int64_t pg1 = min<int64_t>(max_pages, ceil_div(min<int64_t>(max_rows, r0 + split_rows), page_size));
+    const int64_t pg1 = min<int64_t>(max_pages, ceil_div(min<int64_t>(max_rows, rend), page_size));
     const int npg = (int)min<int64_t>(DEC_PT_CAP, max<int64_t>(0, pg1 - pg0));   // the host keeps it within the cap
     const int32_t *pt = page_table + unit * max_pages + pg0;
     for (int i = tid; i < npg; i += 64 * WAVES) pte[i] = pt[i];
 
-    int64_t n = n_rows[unit];
-    n = max<int64_t>(0, min<int64_t>(n, max_rows));
+    if (parts == 0) n = max<int64_t>(0, min<int64_t>((int64_t)n_rows[unit], max_rows));
     // rows whose pages lie past the staged entries are not reached (the host
     // sizes splits so that this never cuts anything)
-    const int64_t r1 = min<int64_t>(min<int64_t>(n, r0 + split_rows), (pg0 + npg) * (int64_t)page_size);
+    const int64_t r1 = min<int64_t>(min<int64_t>(n, rend), (pg0 + npg) * (int64_t)page_size);
     const int64_t len = pool_rows > 0 ? max<int64_t>(0, r1 - r0) : 0;     // an empty pool: every row is skipped
     const int64_t per = ceil_div(ceil_div(len, WAVES), RPS) * RPS;
     const int64_t w0 = r0 + (int64_t)wave * per;
@@ -195,6 +265,11 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     for (int g = 0; g < HG; ++g)
 #pragma unroll
         for (int j = 0; j < VPL; ++j) asm volatile("" ::"v"(qs[g][j]));
+    // a split that starts past the unit's rows writes no state (the merge
+    // reads the row count and skips it): it ends after one round trip instead
+    // of holding a workgroup slot through the barriers and the state stores.
+    // Every part of a unit with rows starts below its row count.
+    if (nsplit > 1 && r0 >= n) return;
     __syncthreads();    // page entries staged
 
     // m: reference max per head, wavefront-uniform; l and o: this lane's
@@ -457,19 +532,25 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     }
 }
 
+// Combines the states of a unit's splits; splits that start at or past the
+// unit's (clamped) row count wrote none and are skipped.  split_rows == 0:
+// equal parts, all of which a unit with rows wrote.
 template <int D, int G>
-__global__ __launch_bounds__(256) void decode_merge_kernel(int Hq, int Hkv, int nsplit, const float *__restrict__ ws,
-                                                          float *__restrict__ out) {
+__global__ __launch_bounds__(256) void decode_merge_kernel(int Hq, int Hkv, int nsplit, const int32_t *__restrict__ n_rows,
+                                                          int64_t max_rows, int64_t split_rows,
+                                                          const float *__restrict__ ws, float *__restrict__ out) {
     const int64_t unit = blockIdx.x;
     const int b = (int)(unit / Hkv), h = (int)(unit % Hkv);
+    const int64_t n = max<int64_t>(0, min<int64_t>(n_rows[unit], max_rows));
+    const int used = split_rows > 0 ? (int)min<int64_t>(nsplit, ceil_div(n, split_rows)) : (n > 0 ? nsplit : 0);
     float *w = const_cast<float *>(ws);
     for (int i = threadIdx.x; i < G * D; i += 256) {
         const int g = i / D, c = i % D;
         float M = -INFINITY;
-        for (int s = 0; s < nsplit; ++s) M = fmaxf(M, part_ptr(w, unit, nsplit, s, G, D)[g * (D + 2)]);
+        for (int s = 0; s < used; ++s) M = fmaxf(M, part_ptr(w, unit, nsplit, s, G, D)[g * (D + 2)]);
         float Lsum = 0.f, O = 0.f;
         if (M > -INFINITY) {
-            for (int s = 0; s < nsplit; ++s) {
+            for (int s = 0; s < used; ++s) {
                 const float *pp = part_ptr(w, unit, nsplit, s, G, D) + (int64_t)g * (D + 2);
                 if (pp[0] > -INFINITY) {
                     const float a = __builtin_amdgcn_exp2f(pp[0] - M);
@@ -499,13 +580,15 @@ static int device_cus() {
 // least DEC_MIN_SPLIT_ROWS rows long.
 static int64_t max_splits(int64_t max_rows) { return std::max<int64_t>(1, ceil_div(max_rows, DEC_MIN_SPLIT_ROWS)); }
 
-// Rows per split:
+// Rows per split, where the equal-parts mode does not apply:
 //   - fewer units than CUs: enough splits to give every CU a workgroup;
 //   - between one and four units per CU: splits of at most DEC_CAP_ROWS, so
 //     that long units (a batch of prompts of different lengths) do not leave
 //     the chip idle behind them once the short ones are done (measured on
 //     the 64-request workload, one launch per layer: 0.67 of HBM peak against
-//     0.61 with one split per unit; equal-sized parts per unit gave 0.63);
+//     0.61 with one split per unit).  The equal-parts mode, which also
+//     balances the shader engines and orders each engine's work longest
+//     first, reached 0.70 there;
 //   - more units: one split per unit (the workgroups balance by themselves,
 //     and extra splits only add merge work).
 // A split never spans more page entries than the LDS stage holds and starts
@@ -529,8 +612,14 @@ static int launch_decode(const char *fn, hipStream_t s, int B, int Hq, int Hkv, 
     constexpr int WAVES = DecodeShape<T, D, HG>::WAVES;
     const int64_t units = (int64_t)B * Hkv;
     const int64_t max_rows = (int64_t)max_pages * page_size;
-    const int64_t split_rows = plan_split_rows(units * NHG, max_rows, page_size);
-    const int64_t nsplit = ceil_div(max_rows, split_rows);
+    // between one and four units per CU: equal parts spread over the shader
+    // engines (see the kernel), where the unit counts and sizes allow it
+    const int64_t wgs = units * NHG;
+    const bool parts = NHG == 1 && wgs > device_cus() && wgs < 4 * (int64_t)device_cus() &&
+                       ceil_div(units, DEC_XCDS) <= DEC_BIN_MAX && max_rows >= DEC_ENGINES * DEC_MIN_SPLIT_ROWS &&
+                       ceil_div(ceil_div(max_rows, DEC_ENGINES), page_size) + 1 <= DEC_PT_CAP;
+    const int64_t split_rows = parts ? 0 : plan_split_rows(wgs, max_rows, page_size);
+    const int64_t nsplit = parts ? DEC_ENGINES : ceil_div(max_rows, split_rows);
     if (nsplit > 65535 || nsplit > max_splits(max_rows)) {
         set_error("%s: %lld splits of %lld rows are not supported", fn, (long long)nsplit, (long long)split_rows);
         return SG_EUNSUPPORTED;
@@ -549,11 +638,14 @@ static int launch_decode(const char *fn, hipStream_t s, int B, int Hq, int Hkv, 
     const int page_shift = 30 + lg;
     const uint32_t page_mul = (uint32_t)(((1ull << page_shift) + (uint64_t)page_size - 1) / (uint64_t)page_size);
     dim3 grid((unsigned)units, (unsigned)nsplit, (unsigned)NHG);
+    if (parts) grid = dim3((unsigned)(DEC_XCDS * DEC_ENGINES * ceil_div(units, DEC_XCDS)), 1, 1);
     decode_kernel<T, D, HG><<<grid, 64 * WAVES, 0, s>>>(
         Hq, Hkv, scale_log2, reinterpret_cast<const T *>(q), reinterpret_cast<const v4u *>(k_pool),
         reinterpret_cast<const v4u *>(v_pool), pool_rows, page_table, n_rows, page_size, page_mul, page_shift,
-        max_pages, split_rows, out, ws);
-    if (nsplit > 1) decode_merge_kernel<D, G><<<(unsigned)units, 256, 0, s>>>(Hq, Hkv, (int)nsplit, ws, out);
+        max_pages, split_rows, out, ws, (int)units, parts ? DEC_ENGINES : 0);
+    if (nsplit > 1)
+        decode_merge_kernel<D, G><<<(unsigned)units, 256, 0, s>>>(Hq, Hkv, (int)nsplit, n_rows, max_rows, split_rows, ws,
+                                                                  out);
     return launch_status(fn);
 }
 

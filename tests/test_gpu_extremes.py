@@ -54,6 +54,7 @@ def _run_decode(gpu_lib, q, k, v, pages, n, P, td):
     ("bf16", 4, 1, 2, 1500),
     ("f32", 4, 130, 2, 400),
     ("bf16", 8, 130, 2, 400),
+    ("f32", 4, 150, 2, 1200),          # equal parts over the shader engines
 ])
 def test_decode_reference_max_raised_mid_stream(gpu_lib, dtype, G, B, Hkv, nrows):
     d, P = 128, 16
@@ -106,6 +107,7 @@ def test_decode_bf16_far_inside_tolerance(gpu_lib, G):
     ("bf16", 4, 2, 2, 1337, 16),      # rows split over several workgroups
     ("bf16", 8, 130, 2, 211, 16),     # one workgroup per unit
     ("f32", 4, 1, 3, 700, 1),         # per-row index table
+    ("bf16", 4, 150, 2, 900, 16),     # equal parts over the shader engines
 ])
 def test_decode_every_row_counted_once(gpu_lib, dtype, G, B, Hkv, nrows, P):
     """Equal keys give every row the same weight 1/n; V row r is (1 + r // d)

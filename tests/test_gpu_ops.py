@@ -249,6 +249,15 @@ def _paged_set(g, B, Hkv, d, nmax, P, td, empty_some=True):
     # more units than CUs, one row per lane group and two head groups
     ("f32", 64, 1, 204, 16, 129),
     ("bf16", 64, 16, 300, 4, 130),
+    # one to four units per CU with at least 512 rows: equal parts over the
+    # shader engines (units not a multiple of 8, engine bins of up to 125 units)
+    ("bf16", 128, 4, 1500, 16, 150),
+    ("f32", 128, 8, 700, 16, 257),
+    ("bf16", 64, 1, 1200, 1, 500),
+    # four or more units per CU: one workgroup per unit (unit counts not a
+    # multiple of 8)
+    ("bf16", 128, 4, 300, 16, 520),
+    ("f32", 64, 2, 150, 16, 1101),
 ])
 def test_decode_parity(gpu_lib, dtype, d, G, nmax, P, B):
     g = np.random.default_rng(nmax + G + d + P)
@@ -268,6 +277,29 @@ def test_decode_parity(gpu_lib, dtype, d, G, nmax, P, B):
     assert np.isfinite(o).all()
     tol = 2e-2 if dtype == "bf16" else 1e-4
     np.testing.assert_allclose(o, ref, atol=tol, rtol=0)
+
+
+def test_decode_equal_parts_tiny_units(gpu_lib):
+    """Equal-parts launches where most units hold 0 to 3 rows: parts of such
+    units are empty or one row long, and all four still meet in the merge."""
+    say("decode equal parts, tiny units")
+    g = np.random.default_rng(4242)
+    B, Hkv, G, d, P = 140, 2, 4, 128, 16
+    Hq = G * Hkv
+    n, pages, kp, vp = _paged_set(g, B, Hkv, d, 640, P, torch.bfloat16)
+    n[:] = g.integers(0, 4, n.shape)
+    n[0, 0], n[77, 1], n[-1, 0] = 640, 513, 3
+    q = (torch.randn((B, Hq, d), generator=torch.Generator().manual_seed(9)) * 2).to(torch.bfloat16)
+    out = torch.full((B, Hq, d), float("nan"), device="cuda")
+    ws = torch.empty((gpu_lib.decode_workspace_size(B, Hq, Hkv, d, pages.shape[-1], P),), dtype=torch.uint8,
+                     device="cuda")
+    gpu_lib.sg_decode_attn(q.cuda(), kp.cuda(), vp.cuda(), cu(pages), cu(n), P, out, ws=ws)
+    torch.cuda.synchronize()
+    ref = oracle.decode_attn(f32(q), f32(kp), f32(vp), pages, n, P)
+    o = out.cpu().numpy()
+    assert np.isfinite(o).all()
+    np.testing.assert_allclose(o, ref, atol=1e-4, rtol=0)
+    assert (o[n.reshape(-1).repeat(G).reshape(B, Hq) == 0] == 0).all()
 
 
 def test_decode_split_workspace_reused(gpu_lib):
