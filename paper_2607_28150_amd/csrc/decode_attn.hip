@@ -22,7 +22,11 @@
 // rows.
 //   logits : each lane dots its slices of q (held in registers) with its K
 //            slices (v_dot2_f32_bf16 for bf16, fp32 accumulation); DPP adds
-//            sum the partials over the row's LPR lanes;
+//            sum the partials over the row's LPR lanes.  With 8 heads over
+//            16-lane rows the sums are transposed instead (each level of
+//            lane pairs halves the values a lane holds), so a lane ends with
+//            one head's logit and takes one exponential, and row broadcasts
+//            hand the probabilities to the row;
 //   softmax: online, against a wavefront-uniform reference max per head that
 //            is raised only when a logit passes it by more than 2^16 (exp2,
 //            log2(e) folded into the scale), so the outputs are rescaled
@@ -117,6 +121,8 @@ constexpr int DPP_XOR2 = 0x4E;        // quad_perm [2,3,0,1]
 constexpr int DPP_HALF_MIRROR = 0x141;
 constexpr int DPP_ROR4 = 0x124;
 constexpr int DPP_ROR8 = 0x128;
+constexpr int DPP_MIRROR = 0x140;     // row_mirror: lane i <-> 15 - i within each 16-lane row
+constexpr int DPP_NEWBCAST = 0x150;   // row_newbcast:n = DPP_NEWBCAST + n: lane n of each row to the row
 
 // sum over each group of N consecutive lanes (N = 4, 8 or 16); every lane of
 // the group receives the group's sum
@@ -275,6 +281,15 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     // m: reference max per head, wavefront-uniform; l and o: this lane's
     // partials over the rows of its row group
     float m[HG], l[HG], o[HG][VPL][PER16];
+    // Transposed logits (8 heads over 16-lane rows): after the reduction lane
+    // i of a row holds the logit of head hd = (i >> 3 & 1) + 2 (i >> 2 & 1) +
+    // 4 (i >> 1 & 1) (lanes i and i ^ 1 alike), so each lane takes one
+    // exponential instead of eight; the probabilities then go to the whole
+    // row by row broadcasts.  m_lane and l_lane are the reference and sum of
+    // the lane's head.
+    constexpr bool TRANS = HG == 8 && LPR == 16;
+    const int hd = ((lane >> 3) & 1) | (((lane >> 2) & 1) << 1) | (((lane >> 1) & 1) << 2);
+    float m_lane = -INFINITY, l_lane = 0.f, z_lane = -INFINITY;
 #pragma unroll
     for (int g = 0; g < HG; ++g) {
         m[g] = -INFINITY;
@@ -318,6 +333,31 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
 #pragma unroll
         for (int j = 0; j < VPL; ++j) kv[j] = *reinterpret_cast<const v4u *>(sb + j * 1024 + lane * 16);
         bool grow = false;
+        if constexpr (TRANS) {
+            float a[HG];
+#pragma unroll
+            for (int g = 0; g < HG; ++g) {
+                a[g] = 0.f;
+#pragma unroll
+                for (int j = 0; j < VPL; ++j) a[g] = SliceDot<T>::run(qs[g][j], kv[j], a[g]);
+            }
+            // each level pairs lanes that differ in one more lane bit (3, 2, 1);
+            // a lane keeps the member of each value pair its bit selects and
+            // adds the partner's copy of it
+            const bool b3 = (lane >> 3) & 1, b2 = (lane >> 2) & 1, b1 = (lane >> 1) & 1;
+            float w[4], x[2];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                w[i] = (b3 ? a[2 * i + 1] : a[2 * i]) + dpp<DPP_MIRROR>(b3 ? a[2 * i] : a[2 * i + 1]);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                x[i] = (b2 ? w[2 * i + 1] : w[2 * i]) + dpp<DPP_HALF_MIRROR>(b2 ? w[2 * i] : w[2 * i + 1]);
+            float y = (b1 ? x[1] : x[0]) + dpp<DPP_XOR2>(b1 ? x[0] : x[1]);
+            y += dpp<DPP_XOR1>(y);
+            z_lane = ok ? y * scale_log2 : -INFINITY;
+            grow = z_lane > m_lane + DEC_LAZY;
+            return __any(grow);
+        }
 #pragma unroll
         for (int g = 0; g < HG; ++g) {
             float a = 0.f;
@@ -335,11 +375,25 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
 #pragma unroll
         for (int j = 0; j < VPL; ++j) vv[j] = *reinterpret_cast<const v4u *>(sb + STEPB + j * 1024 + lane * 16);
         float p[HG];
+        if constexpr (TRANS) {
+            const float ref = m_lane == -INFINITY ? 0.f : m_lane;
+            const float pl = __builtin_amdgcn_exp2f(z_lane - ref);
+            l_lane += pl;
+            p[0] = dpp<DPP_NEWBCAST + 0>(pl);
+            p[1] = dpp<DPP_NEWBCAST + 8>(pl);
+            p[2] = dpp<DPP_NEWBCAST + 4>(pl);
+            p[3] = dpp<DPP_NEWBCAST + 12>(pl);
+            p[4] = dpp<DPP_NEWBCAST + 2>(pl);
+            p[5] = dpp<DPP_NEWBCAST + 10>(pl);
+            p[6] = dpp<DPP_NEWBCAST + 6>(pl);
+            p[7] = dpp<DPP_NEWBCAST + 14>(pl);
+        } else {
 #pragma unroll
-        for (int g = 0; g < HG; ++g) {
-            const float ref = m[g] == -INFINITY ? 0.f : m[g];     // nothing seen yet: z is -inf too
-            p[g] = __builtin_amdgcn_exp2f(z[g] - ref);
-            l[g] += p[g];
+            for (int g = 0; g < HG; ++g) {
+                const float ref = m[g] == -INFINITY ? 0.f : m[g];     // nothing seen yet: z is -inf too
+                p[g] = __builtin_amdgcn_exp2f(z[g] - ref);
+                l[g] += p[g];
+            }
         }
 #pragma unroll
         for (int j = 0; j < VPL; ++j) {
@@ -352,7 +406,34 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
         }
     };
     // raise every head's reference max to cover z (rare)
-    auto rescale = [&](const float (&z)[HG]) {
+    auto rescale = [&](float (&z)[HG]) {
+        if constexpr (TRANS) {
+            // every head's logit of the row, for the wavefront maxima below
+            z[0] = dpp<DPP_NEWBCAST + 0>(z_lane);
+            z[1] = dpp<DPP_NEWBCAST + 8>(z_lane);
+            z[2] = dpp<DPP_NEWBCAST + 4>(z_lane);
+            z[3] = dpp<DPP_NEWBCAST + 12>(z_lane);
+            z[4] = dpp<DPP_NEWBCAST + 2>(z_lane);
+            z[5] = dpp<DPP_NEWBCAST + 10>(z_lane);
+            z[6] = dpp<DPP_NEWBCAST + 6>(z_lane);
+            z[7] = dpp<DPP_NEWBCAST + 14>(z_lane);
+            float al = 1.f, ml = m_lane;
+#pragma unroll
+            for (int g = 0; g < HG; ++g) {
+                const float mn = fmaxf(m[g], wave_max(z[g]));
+                const float alpha = mn == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m[g] - mn);
+#pragma unroll
+                for (int j = 0; j < VPL; ++j)
+#pragma unroll
+                    for (int e = 0; e < PER16; ++e) o[g][j][e] *= alpha;
+                m[g] = mn;
+                al = hd == g ? alpha : al;
+                ml = hd == g ? mn : ml;
+            }
+            l_lane *= al;
+            m_lane = ml;
+            return;
+        }
 #pragma unroll
         for (int g = 0; g < HG; ++g) {
             const float mn = fmaxf(m[g], wave_max(z[g]));
@@ -399,6 +480,17 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
         wait_vmem<0>();     // the ring is reused below
     }
 
+    if constexpr (TRANS) {
+        // each head's sum from the first lane holding it, for the whole row
+        l[0] = dpp<DPP_NEWBCAST + 0>(l_lane);
+        l[1] = dpp<DPP_NEWBCAST + 8>(l_lane);
+        l[2] = dpp<DPP_NEWBCAST + 4>(l_lane);
+        l[3] = dpp<DPP_NEWBCAST + 12>(l_lane);
+        l[4] = dpp<DPP_NEWBCAST + 2>(l_lane);
+        l[5] = dpp<DPP_NEWBCAST + 10>(l_lane);
+        l[6] = dpp<DPP_NEWBCAST + 6>(l_lane);
+        l[7] = dpp<DPP_NEWBCAST + 14>(l_lane);
+    }
     // The wavefront's partial state.  First the row groups within each 16-lane
     // DPP row are summed (m is wavefront-uniform) ...
 #pragma unroll
