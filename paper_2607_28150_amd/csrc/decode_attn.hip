@@ -3,9 +3,10 @@
 // Grid: x = (sequence, KV head) unit, y = split of the unit's rows (one split
 // whenever the units fill the chip), z = group of up to 8 q heads of the KV
 // head.  Between one and four units per CU the grid is instead one-dimensional
-// over (shader engine, part): every unit is cut into four equal parts, one per
-// engine of its XCD, and each engine takes its parts longest first (the
-// equal-parts mode in the kernel).  A workgroup serves all the q heads of its
+// over (shader engine, slot): every unit is cut into two equal parts for the
+// two engines of one engine pair of its XCD, the units are dealt to the pairs
+// in snake order of length, and each engine takes its units longest first
+// (the equal-parts mode in the kernel).  A workgroup serves all the q heads of its
 // group, so each K/V row is read from HBM once per step (twice for 16-head
 // groups).
 //
@@ -104,6 +105,7 @@ constexpr int64_t DEC_CAP_ROWS = 1024;    // split length when units number one 
 constexpr int DEC_XCDS = 8;
 constexpr int DEC_ENGINES = 4;
 constexpr int DEC_BIN_MAX = 128;          // units of one XCD in the equal-parts mode
+constexpr int DEC_PARTS = 2;              // parts per unit; units go to DEC_ENGINES / DEC_PARTS engine groups
 constexpr float DEC_LAZY = 16.f;    // log2 headroom before the reference max is raised
 
 // partial state of one split: per head (m, l) then o[d]
@@ -177,11 +179,13 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
     // Which rows this workgroup reads: [r0, rend) of unit `unit`.
     //   split mode: unit blockIdx.x, fixed split blockIdx.y of split_rows rows;
     //   equal-parts mode (parts > 0, a one-dimensional grid): workgroup L
-    //     belongs to the engine bin (x, k) = (L mod 8, (L / 8) mod 4) and
-    //     takes part k of the (L / 32)-th longest unit among the bin's units
-    //     x, x + 8, ..., each unit cut into `parts` equal parts.  Every engine
-    //     so receives the same share of every unit, and each engine's queue
-    //     runs longest first.
+    //     belongs to engine k = (L / 8) mod 4 of XCD x = L mod 8, whose units
+    //     are x, x + 8, ...  Those units, ranked by length, are dealt to the
+    //     XCD's engine groups (4 / parts engines each) in snake order (ranks
+    //     0, 3, 4, 7, ... to the first of two groups, 1, 2, 5, 6, ... to the
+    //     second), so the groups carry nearly equal rows; each unit is cut
+    //     into `parts` equal parts, one per engine of its group, and slot
+    //     L / 32 of an engine takes its group's units longest first.
     int64_t unit, n, r0, rend;
     int split, nsplit;
     if (parts > 0) {
@@ -191,7 +195,12 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
         const int L = (int)blockIdx.x;
         const int bx = L % DEC_XCDS, bk = (L / DEC_XCDS) % DEC_ENGINES, bj = L / (DEC_XCDS * DEC_ENGINES);
         const int members = (nunits - bx + DEC_XCDS - 1) / DEC_XCDS;
-        if (bj >= members) return;          // uniform: the bins' last slots past the units
+        // engine group of bk and the rank (by length) of the unit its bj-th
+        // workgroup takes: ranks are dealt to the groups in snake order
+        constexpr int NGRP = DEC_ENGINES / DEC_PARTS;
+        const int grp = bk / parts, part = bk % parts;
+        const int target = 2 * NGRP * (bj / 2) + ((bj & 1) ? 2 * NGRP - 1 - grp : grp);
+        if (target >= members) return;      // uniform: the bins' last slots past the units
         if (tid < DEC_BIN_MAX)
             bin_n[tid] = tid < members
                              ? (int32_t)max<int64_t>(0, min<int64_t>(n_rows[bx + (int64_t)DEC_XCDS * tid], max_rows))
@@ -217,16 +226,16 @@ __global__ __launch_bounds__((64 * DecodeShape<T, D, HG>::WAVES)) void decode_ke
             }
             cnt += __builtin_amdgcn_update_dpp(0, cnt, DPP_XOR1, 0xf, 0xf, false);
             cnt += __builtin_amdgcn_update_dpp(0, cnt, DPP_XOR2, 0xf, 0xf, false);
-            if (qtr == 0 && m < members && cnt == bj) chosen = m;
+            if (qtr == 0 && m < members && cnt == target) chosen = m;
         }
         __syncthreads();
         const int sel = min(max((int)chosen, 0), members - 1);   // the ranks are a permutation: one match
         unit = bx + (int64_t)DEC_XCDS * sel;
         n = bin_n[sel];
-        split = bk;
+        split = part;
         nsplit = parts;
-        r0 = n * bk / parts;
-        rend = n * (bk + 1) / parts;
+        r0 = n * part / parts;
+        rend = n * (part + 1) / parts;
     } else {
         unit = blockIdx.x;
         split = blockIdx.y;
@@ -680,7 +689,8 @@ static int64_t max_splits(int64_t max_rows) { return std::max<int64_t>(1, ceil_d
 //     the 64-request workload, one launch per layer: 0.67 of HBM peak against
 //     0.61 with one split per unit).  The equal-parts mode, which also
 //     balances the shader engines and orders each engine's work longest
-//     first, reached 0.70 there;
+//     first, reached 0.68-0.70 there (and 0.45 against 0.39 for the 80-layer
+//     8-head launch);
 //   - more units: one split per unit (the workgroups balance by themselves,
 //     and extra splits only add merge work).
 // A split never spans more page entries than the LDS stage holds and starts
@@ -708,10 +718,10 @@ static int launch_decode(const char *fn, hipStream_t s, int B, int Hq, int Hkv, 
     // engines (see the kernel), where the unit counts and sizes allow it
     const int64_t wgs = units * NHG;
     const bool parts = NHG == 1 && wgs > device_cus() && wgs < 4 * (int64_t)device_cus() &&
-                       ceil_div(units, DEC_XCDS) <= DEC_BIN_MAX && max_rows >= DEC_ENGINES * DEC_MIN_SPLIT_ROWS &&
-                       ceil_div(ceil_div(max_rows, DEC_ENGINES), page_size) + 1 <= DEC_PT_CAP;
+                       ceil_div(units, DEC_XCDS) <= DEC_BIN_MAX && max_rows >= DEC_PARTS * DEC_MIN_SPLIT_ROWS &&
+                       ceil_div(ceil_div(max_rows, DEC_PARTS), page_size) + 1 <= DEC_PT_CAP;
     const int64_t split_rows = parts ? 0 : plan_split_rows(wgs, max_rows, page_size);
-    const int64_t nsplit = parts ? DEC_ENGINES : ceil_div(max_rows, split_rows);
+    const int64_t nsplit = parts ? DEC_PARTS : ceil_div(max_rows, split_rows);
     if (nsplit > 65535 || nsplit > max_splits(max_rows)) {
         set_error("%s: %lld splits of %lld rows are not supported", fn, (long long)nsplit, (long long)split_rows);
         return SG_EUNSUPPORTED;
@@ -730,11 +740,13 @@ static int launch_decode(const char *fn, hipStream_t s, int B, int Hq, int Hkv, 
     const int page_shift = 30 + lg;
     const uint32_t page_mul = (uint32_t)(((1ull << page_shift) + (uint64_t)page_size - 1) / (uint64_t)page_size);
     dim3 grid((unsigned)units, (unsigned)nsplit, (unsigned)NHG);
-    if (parts) grid = dim3((unsigned)(DEC_XCDS * DEC_ENGINES * ceil_div(units, DEC_XCDS)), 1, 1);
+    if (parts)
+        grid = dim3((unsigned)(DEC_XCDS * DEC_ENGINES *
+                               ceil_div(ceil_div(units, DEC_XCDS), DEC_ENGINES / DEC_PARTS)), 1, 1);
     decode_kernel<T, D, HG><<<grid, 64 * WAVES, 0, s>>>(
         Hq, Hkv, scale_log2, reinterpret_cast<const T *>(q), reinterpret_cast<const v4u *>(k_pool),
         reinterpret_cast<const v4u *>(v_pool), pool_rows, page_table, n_rows, page_size, page_mul, page_shift,
-        max_pages, split_rows, out, ws, (int)units, parts ? DEC_ENGINES : 0);
+        max_pages, split_rows, out, ws, (int)units, parts ? DEC_PARTS : 0);
     if (nsplit > 1)
         decode_merge_kernel<D, G><<<(unsigned)units, 256, 0, s>>>(Hq, Hkv, (int)nsplit, n_rows, max_rows, split_rows, ws,
                                                                   out);

@@ -281,7 +281,7 @@ def test_decode_parity(gpu_lib, dtype, d, G, nmax, P, B):
 
 def test_decode_equal_parts_tiny_units(gpu_lib):
     """Equal-parts launches where most units hold 0 to 3 rows: parts of such
-    units are empty or one row long, and all four still meet in the merge."""
+    units are empty or one row long, and both still meet in the merge."""
     say("decode equal parts, tiny units")
     g = np.random.default_rng(4242)
     B, Hkv, G, d, P = 140, 2, 4, 128, 16
