@@ -228,6 +228,18 @@ class Path:
                                   dtype=torch.uint8, device=dev)
         self.kv_index = []
         self.graphs = []
+        # the select region in request groups: pairs of consecutive requests,
+        # the longest pairs first, each pair's top-k and pack on a second
+        # stream beside the next pair's score.  Used only when every pair's
+        # score call keeps full-length key chunks (enough workgroups), so the
+        # outputs are bit-identical to one call over the whole batch.
+        full_chunks = lambda b0, b1: (b1 - b0) * L * Hkv * -(-max(lens[b0:b1]) // 2048) >= 1024  # noqa: E731
+        pairs = [(b, min(B, b + 2)) for b in range(0, B, 2)]
+        self.select_groups = []
+        if B >= 4 and all(full_chunks(a, b) for a, b in pairs):
+            pairs.sort(key=lambda ab: -sum(lens[ab[0]:ab[1]]))
+            self.select_groups = [dict(a=a, b=b, nmax=max(lens[a:b]), maxk=max(self.kb[a:b])) for a, b in pairs]
+        self.sel_stream = torch.cuda.Stream(device=dev)
 
     # ---- the calls of a step
     def score(self, lse_in=None):
@@ -241,6 +253,33 @@ class Path:
     def pack(self):
         self.sg.sg_pack(self.pre["k"], self.pre["v"], self.idx, self.cus, self.T, self.cuk, self.K_total,
                         max(self.kb), self.tbuf, L=self.cfg.L, Hkv=self.cfg.Hkv)
+
+    def select(self):
+        """score -> top-k -> pack over the batch; in request groups when
+        `select_groups` is set (see the constructor)."""
+        import torch
+        if not self.select_groups:
+            self.score()
+            self.topk()
+            self.pack()
+            return
+        c = self.cfg
+        main = torch.cuda.current_stream()
+        side = self.sel_stream
+        side.wait_stream(main)
+        for g in self.select_groups:
+            a, b = g["a"], g["b"]
+            self.sg.sg_score(self.pre["q_win"][a:b], self.pre["k"], self.cus[a:b + 1], self.T, g["nmax"], c.Hkv,
+                             self.scores, ws=self.ws_score)
+            done = torch.cuda.Event()
+            done.record(main)
+            side.wait_event(done)
+            with torch.cuda.stream(side):
+                self.sg.sg_topk(self.scores, self.cus[a:b + 1], self.T, g["nmax"], self.cuk[a:b + 1], self.K_total,
+                                self.idx)
+                self.sg.sg_pack(self.pre["k"], self.pre["v"], self.idx, self.cus[a:b + 1], self.T,
+                                self.cuk[a:b + 1], self.K_total, g["maxk"], self.tbuf, L=c.L, Hkv=c.Hkv)
+        main.wait_stream(side)
 
     def receive(self, rep=0):
         kp, vp = self.pools[rep]
@@ -418,6 +457,15 @@ def path_ops(p: Path, lse=False):
     else:
         ops["pack"] = {"ms": r4(t), "gbs": round(gbs(pb, t), 1), "frac_hbm_peak": r4(gbs(pb, t) / HBM_PEAK_GBS),
                        "mb_algorithmic": round(pb / 1e6, 1)}
+    kvb = p.kv_cache_bytes()
+    t = median_ms(lambda i: (p.score(), p.topk(), p.pack()))
+    ops["select_one_call"] = {"ms": r4(t), "gbs_kv_cache": round(gbs(kvb, t), 1),
+                              "note": "score, top-k and pack over the whole batch, one call each on one stream"}
+    if p.select_groups:
+        t = median_ms(lambda i: p.select())
+        ops["select_request_pairs"] = {"ms": r4(t), "gbs_kv_cache": round(gbs(kvb, t), 1), "groups": len(p.select_groups),
+                                       "note": "the timed form: pairs of requests, each pair's top-k and pack on a "
+                                               "second stream beside the next pair's score"}
     t = median_ms(lambda i: p.receive(i % p.reps))
     rb = p.receive_bytes()
     ops["receive"] = {"ms": r4(t), "mb_algorithmic": round(rb / 1e6, 1)}
@@ -449,6 +497,65 @@ def path_ops(p: Path, lse=False):
         "tokens_per_s": round(p.B / (t * 1e-3), 1),
         "note": "all layers in one launch as L x B sequences: a kernel-bandwidth ceiling, not a model order"}
     return ops
+
+
+def select_per_layer_kv(sg, cfg):
+    """The select region of `cfg` with a K/V source per layer instead of one
+    shared by the layers (the headline workload shares one to keep its decode
+    side in memory): no layer finds another layer's keys in the last-level
+    cache.  Both forms, one call and request pairs; outputs compared."""
+    import torch
+    from datagen import inputs
+    c = cfg.with_(kv_shared_layers=False)
+    pre = inputs.make_prefill(c, device="cuda")
+    lens, T, B, L, Hkv, d = pre["seqlens"], pre["T"], c.B, c.L, c.Hkv, c.d
+    bud = inputs.make_budget(c, lens)
+    kb, K_total = bud["k"], bud["K_total"]
+    i32 = dict(dtype=torch.int32, device="cuda")
+    cus, cuk = torch.tensor(pre["cu_seqlens"], **i32), torch.tensor(bud["cu_k"], **i32)
+    scores = torch.empty((L, Hkv, T), device="cuda")
+    idx = torch.empty((L, Hkv, K_total), **i32)
+    ws = torch.empty(sg.score_workspace_size(B, L, c.Hq, Hkv, d, c.W, max(lens)), dtype=torch.uint8, device="cuda")
+    tbuf = torch.empty(sg.pack_bytes(pre["k"].dtype, L, Hkv, d, K_total), dtype=torch.uint8, device="cuda")
+    side = torch.cuda.Stream()
+
+    def one_call():
+        sg.sg_score(pre["q_win"], pre["k"], cus, T, max(lens), Hkv, scores, ws=ws)
+        sg.sg_topk(scores, cus, T, max(lens), cuk, K_total, idx)
+        sg.sg_pack(pre["k"], pre["v"], idx, cus, T, cuk, K_total, max(kb), tbuf, L=L, Hkv=Hkv)
+
+    pairs = sorted([(b, min(B, b + 2)) for b in range(0, B, 2)], key=lambda ab: -sum(lens[ab[0]:ab[1]]))
+
+    def pairs_call():
+        main = torch.cuda.current_stream()
+        side.wait_stream(main)
+        for a, b in pairs:
+            sg.sg_score(pre["q_win"][a:b], pre["k"], cus[a:b + 1], T, max(lens[a:b]), Hkv, scores, ws=ws)
+            done = torch.cuda.Event()
+            done.record(main)
+            side.wait_event(done)
+            with torch.cuda.stream(side):
+                sg.sg_topk(scores, cus[a:b + 1], T, max(lens[a:b]), cuk[a:b + 1], K_total, idx)
+                sg.sg_pack(pre["k"], pre["v"], idx, cus[a:b + 1], T, cuk[a:b + 1], K_total, max(kb[a:b]), tbuf,
+                           L=L, Hkv=Hkv)
+        main.wait_stream(side)
+
+    kvb = 2 * L * Hkv * T * d * pre["k"].element_size()
+    one_call()
+    torch.cuda.synchronize()
+    ref = (scores.clone(), idx.clone())
+    t1 = median_ms(lambda i: one_call(), reps=5, warm=1)
+    pairs_call()
+    torch.cuda.synchronize()
+    same = bool(torch.equal(scores, ref[0]) and torch.equal(idx, ref[1]))
+    t2 = median_ms(lambda i: pairs_call(), reps=5, warm=1)
+    res = {"one_call_ms": r4(t1), "one_call_gbs": round(gbs(kvb, t1), 1), "request_pairs_ms": r4(t2),
+           "request_pairs_gbs": round(gbs(kvb, t2), 1), "pairs_identical_to_one_call": same,
+           "note": "K/V source per layer (159 GB): no cross-layer cache reuse; 5 repetitions each"}
+    del pre, scores, idx, ws, tbuf, ref
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
 
 
 def window_lse(q_win, k, lens, Hkv, W, d, shared):
@@ -551,26 +658,22 @@ def main():
     setup_s = time.time() - t0
     print(f"[bench] {cfg.name}: set-up done in {setup_s:.1f} s", file=sys.stderr, flush=True)
 
-    NE = 5 + 3 * D
+    NE = 3 + 3 * D
 
     def step(e):
         rec = (lambda i: e[i].record()) if e is not None else (lambda i: None)
         rec(0)
-        p.score()
+        p.select()
         rec(1)
-        p.topk()
-        rec(2)
-        p.pack()
-        rec(3)
         p.receive()
-        rec(4)
+        rec(2)
         for s in range(D):
             p.split(s)
-            rec(5 + 3 * s)
+            rec(3 + 3 * s)
             p.fetch(s)
-            rec(6 + 3 * s)
+            rec(4 + 3 * s)
             p.attn_graph(s)
-            rec(7 + 3 * s)
+            rec(5 + 3 * s)
 
     for _ in range(args.warmup):
         step(None)
@@ -588,13 +691,12 @@ def main():
         return float(np.median([e[i].elapsed_time(e[j]) for e in evs]))
 
     def seg_dec(part):
-        # decode step s: split from the previous mark to 5 + 3s, fetch to 6 + 3s, attention to 7 + 3s
+        # decode step s: split from the previous mark to 3 + 3s, fetch to 4 + 3s, attention to 5 + 3s
         def one(e, s):
-            return e[4 + 3 * s + part].elapsed_time(e[5 + 3 * s + part])
+            return e[2 + 3 * s + part].elapsed_time(e[3 + 3 * s + part])
         return float(np.median([np.mean([one(e, s) for s in range(D)]) for e in evs]))
 
-    t_select = seg(0, 3)
-    t_score, t_topk, t_pack, t_recv = seg(0, 1), seg(1, 2), seg(2, 3), seg(3, 4)
+    t_select, t_recv = seg(0, 1), seg(1, 2)
     t_split, t_fetch, t_attn = seg_dec(0), seg_dec(1), seg_dec(2)
     ms_per_step = wall * 1e3 / args.steps
     value = gbs(p.kv_cache_bytes(), t_select)
@@ -624,6 +726,11 @@ def main():
                    "seed": cfg.seed},
         "select_ms": r4(t_select),
         "value_note": "bytes of the KV cache of every layer and head turned into a transfer buffer per second of "
+                      "score + top-k + pack time (medians over the timed steps); the select region runs in pairs "
+                      "of requests, each pair's top-k and pack beside the next pair's score (outputs bit-identical "
+                      "to one call over the batch); the layers share one K/V source, whose keys the last-level "
+                      "cache serves to later layers: ops.select_per_layer_kv times a source per layer" if p.select_groups else
+                      "bytes of the KV cache of every layer and head turned into a transfer buffer per second of "
                       "score + top-k + pack time (medians over the timed steps)",
         "decode_tokens_per_s": round(tokens_per_s, 1),
         "decode_tokens_per_s_note": "requests per second of decode attention, one launch per layer in model order "
@@ -631,7 +738,7 @@ def main():
         "decode_step_tokens_per_s": round(step_tok_s, 1),
         "decode_step_tokens_per_s_note": "requests per second of whole decode steps: Algorithm 1 + on-demand "
                                          "fetch over the host link + attention",
-        "step_ms": {"score": r4(t_score), "topk": r4(t_topk), "pack": r4(t_pack), "receive": r4(t_recv),
+        "step_ms": {"select": r4(t_select), "receive": r4(t_recv),
                     "split_per_decode_step": r4(t_split), "fetch_per_decode_step": r4(t_fetch),
                     "attention_per_decode_step": r4(t_attn)},
         "roofline": {"kernel": "sg_decode_attn", "bound": "hbm", "achieved": round(dec_gbs, 1),
@@ -666,6 +773,10 @@ def main():
         cpu_in = cpu_inputs(p)
     p.free()
     del p
+    if not args.no_ops and cfg.kv_shared_layers and cfg.B >= 4:
+        print("[bench] select with a K/V source per layer", file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+        line["ops"]["select_per_layer_kv"] = select_per_layer_kv(sg, cfg)
     if not args.no_ops and not args.no_workloads:
         wl = {}
         for name in ("llama8b_8k", "llama8b_32k", "llama70b_16k"):

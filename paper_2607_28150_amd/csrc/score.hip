@@ -522,9 +522,17 @@ static ScorePlan score_plan(int B, int L, int Hkv, int max_seqlen) {
     constexpr int64_t MIN_WG = 1024;                      // two rounds of two workgroups per CU
     constexpr int TILE = 128;                             // chunk granularity (keys)
     const int64_t units = (int64_t)B * L * Hkv;
-    const int64_t want = std::max<int64_t>(1, ceil_div(MIN_WG, units));       // chunks per unit
     ScorePlan p;
-    p.chunk_keys = (int)std::min<int64_t>(SC_CHUNK, std::max<int64_t>(TILE, ceil_div(ceil_div(max_seqlen, want), TILE) * TILE));
+    if (units * ceil_div(max_seqlen, SC_CHUNK) >= MIN_WG) {
+        // full-length chunks already fill the chip: keep them, so that the
+        // chunk boundaries (and the rounding of every score) do not depend on
+        // how many requests one call covers
+        p.chunk_keys = SC_CHUNK;
+    } else {
+        const int64_t want = std::max<int64_t>(1, ceil_div(MIN_WG, units));   // chunks per unit
+        p.chunk_keys = (int)std::min<int64_t>(
+            SC_CHUNK, std::max<int64_t>(TILE, ceil_div(ceil_div(max_seqlen, want), TILE) * TILE));
+    }
     p.nchunk = (int)ceil_div(max_seqlen, p.chunk_keys);
     return p;
 }

@@ -33,6 +33,22 @@ def test_batched64_headline_step(gpu_lib, seed):
         cfg = cfg.with_(seed=seed)
     say("headline batched64: inputs, seed", cfg.seed)
     p = bench.Path(gpu_lib, cfg, decode_steps=1)
+    # the bench's select region runs in request pairs; it must give exactly
+    # what one call over the batch gives (same launch plans per request)
+    say("headline batched64: select region, one call and request pairs")
+    assert p.select_groups, "the 64-request workload runs its select region in request pairs"
+    p.score()
+    p.topk()
+    p.pack()
+    torch.cuda.synchronize()
+    ref = (p.scores.clone(), p.idx.clone(), p.tbuf.clone())
+    p.scores.fill_(float("nan"))
+    p.idx.fill_(-7)
+    p.tbuf.zero_()
+    p.select()
+    torch.cuda.synchronize()
+    assert torch.equal(p.scores, ref[0]) and torch.equal(p.idx, ref[1]) and torch.equal(p.tbuf, ref[2])
+    del ref
     sel = inputs.random_selection(cfg, p.lens, p.kb, device="cuda", tag_extra=5)
     say("headline batched64: prepare (pack, receive, mask, index, graph)")
     p.prepare(selection=sel)
