@@ -1,7 +1,8 @@
 """sg_decode_attn_noalloc (the entry point for callers that cannot allocate)
 against sg_decode_attn with a caller workspace, through the C ABI: the same
 kernels, so outputs must be bit-identical; both within the decode tolerance of
-the oracle.  Two calls in a row, the second smaller, share the static scratch."""
+the oracle.  Calls in a row, each smaller than the one before, share the
+static scratch."""
 import numpy as np
 import pytest
 import torch
@@ -28,10 +29,12 @@ def _case(B, Hq, Hkv, d, rows, P, seed):
 
 @pytest.mark.parametrize("order", ["large_then_small"])
 def test_noalloc_matches_workspace_entry_point(gpu_lib, order):
-    # the first call splits every unit's rows over several workgroups (16 units
-    # on a 256-CU chip), so the split states go through the scratch array; the
-    # second is smaller and reuses it
-    cases = [(2, 32, 8, 128, [3000 + 37 * i for i in range(16)], 16, 1),
+    # the first call cuts 320 units into equal parts over the shader engines;
+    # the second splits every unit's rows over several workgroups (16 units on
+    # a 256-CU chip); the third is smaller still.  Each one's states go through
+    # the scratch array the previous call left behind
+    cases = [(40, 32, 8, 128, [400 + (97 * i) % 1200 for i in range(320)], 16, 3),
+             (2, 32, 8, 128, [3000 + 37 * i for i in range(16)], 16, 1),
              (1, 32, 8, 128, [700 + 5 * i for i in range(8)], 16, 2)]
     assert gpu_lib.decode_noalloc_scratch_bytes() == 16 << 20
     for (B, Hq, Hkv, d, rows, P, seed) in cases:
