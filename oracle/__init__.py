@@ -52,11 +52,13 @@ def _load():
                                    _vp, _vp, _l, _i64p, _vp, _vp, _l, _i8p, _l, _i64p, _i32p]
     lib.sgo_score_count.argtypes = [_i, _i, _i, _i, _i, _i, _i32p, _l, _f32p, _f32p, _l, ctypes.c_double,
                                     ctypes.c_double, _i32p, _i32p]
+    lib.sgo_score_topshare.argtypes = [_i, _i, _i, _i, _i, _i, _i32p, _l, _f32p, _f32p, _l, _i, ctypes.c_double,
+                                       _i32p, _i32p]
     lib.sgo_decode_select.argtypes = [_i, _i, _i, _i, _i, _f32p, _i32p, _l, _f32p, _l, _i32p, _l, ctypes.c_double,
                                       ctypes.c_double, _i32p, _i32p, _f64p]
     for f in ("sgo_score", "sgo_topk", "sgo_pack", "sgo_split", "sgo_fetch", "sgo_decode_attn", "sgo_threads",
               "sgo_block_importance", "sgo_pack_blocks", "sgo_spec_push", "sgo_fetch_keep", "sgo_score_count",
-              "sgo_decode_select"):
+              "sgo_decode_select", "sgo_score_topshare"):
         getattr(lib, f).restype = ctypes.c_int
     lib.sgo_set_threads.argtypes = [_i]
     lib.sgo_set_threads.restype = None
@@ -333,6 +335,27 @@ def score_count(q_win, k, cu_seqlens, Hkv, alpha, k_layer_rows=None, eps=None):
                                  int(k_layer_rows), float(alpha), float(eps or 0.0), _p(out, _i32p),
                                  None if near is None else _p(near, _i32p))
     _check(rc, "score_count")
+    return out if eps is None else (out, near)
+
+
+def score_topshare(q_win, k, cu_seqlens, Hkv, ratio_bp, k_layer_rows=None, eps=None):
+    """Selection counts [L][Hkv][T] int32 when every window row picks its top
+    ratio_bp / 10000 of the keys it sees (ties with the row's threshold all
+    picked); with eps also the per-key number of decisions within eps of a
+    row's threshold: (counts, near)."""
+    q = _c(q_win, np.float32)
+    kk = _c(k, np.float32)
+    B, L, Hq, W, d = q.shape
+    T = kk.shape[2]
+    if k_layer_rows is None:
+        k_layer_rows = 0 if kk.shape[0] == 1 and L > 1 else Hkv * T
+    cu = _c(cu_seqlens, np.int32)
+    out = np.zeros((L, Hkv, T), dtype=np.int32)
+    near = np.zeros((L, Hkv, T), dtype=np.int32) if eps is not None else None
+    rc = _load().sgo_score_topshare(B, L, Hq, Hkv, d, W, _p(cu, _i32p), T, _p(q, _f32p), _p(kk, _f32p),
+                                    int(k_layer_rows), int(ratio_bp), float(eps or 0.0), _p(out, _i32p),
+                                    None if near is None else _p(near, _i32p))
+    _check(rc, "score_topshare")
     return out if eps is None else (out, near)
 
 

@@ -592,6 +592,75 @@ int sgo_score_count(int B, int L, int Hq, int Hkv, int d, int W,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Selection-frequency score under a top-share selector (Section 4.1 defines a
+ * KV entry's importance as how often the selector picks it; Section 5.1 sets a
+ * maximum selection ratio of 20%).  Window row w of q head g sees the
+ * n = p + 1 keys j <= p = N - W + w and picks its top share of them:
+ *     k   = max(1, min(n, floor(n * ratio_bp / 10000)))
+ *     thr = the k-th largest of z_0 .. z_p   (z as in sgo_score_count)
+ *     count_j += [z_j >= thr]                (every key tied with thr is picked)
+ * an integer in [0, G*W].  `near` counts the rows with |z_j - thr| <= eps.
+ */
+static int cmp_desc(const void *a, const void *b) {
+    const double x = *(const double *)a, y = *(const double *)b;
+    return (x < y) - (x > y);
+}
+
+int sgo_score_topshare(int B, int L, int Hq, int Hkv, int d, int W,
+                       const int32_t *cu_seqlens, int64_t T,
+                       const float *q_win, const float *k, int64_t k_layer_rows,
+                       int ratio_bp, double eps, int32_t *counts, int32_t *near)
+{
+    if (B <= 0 || L <= 0 || Hkv <= 0 || Hq % Hkv != 0 || d <= 0 || W <= 0 || ratio_bp < 1 || ratio_bp > 10000)
+        return SGO_EINVAL;
+    const int G = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)d);
+    for (int b = 0; b < B; ++b)
+        if (cu_seqlens[b + 1] - cu_seqlens[b] < W) return SGO_EINVAL;
+    const int nunits = L * Hkv * B;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int u = 0; u < nunits; ++u) {
+        const int b = u % B;
+        const int h = (u / B) % Hkv;
+        const int l = u / (B * Hkv);
+        const int64_t N = cu_seqlens[b + 1] - cu_seqlens[b];
+        const float *K = k + ((int64_t)l * k_layer_rows + (int64_t)h * T + cu_seqlens[b]) * d;
+        int32_t *C = counts + ((int64_t)l * Hkv + h) * T + cu_seqlens[b];
+        int32_t *E = near ? near + ((int64_t)l * Hkv + h) * T + cu_seqlens[b] : NULL;
+        double *z = (double *)malloc(sizeof(double) * (size_t)N);
+        double *sorted = (double *)malloc(sizeof(double) * (size_t)N);
+        for (int64_t j = 0; j < N; ++j) {
+            C[j] = 0;
+            if (E) E[j] = 0;
+        }
+        for (int g = h * G; g < (h + 1) * G; ++g)
+            for (int w = 0; w < W; ++w) {
+                const float *q = q_win + ((((int64_t)b * L + l) * Hq + g) * W + w) * d;
+                const int64_t p = N - W + w;
+                const int64_t n = p + 1;
+                for (int64_t j = 0; j <= p; ++j) {
+                    double acc = 0.0;
+                    for (int c = 0; c < d; ++c) acc += (double)q[c] * (double)K[j * d + c];
+                    z[j] = acc * scale;
+                    sorted[j] = z[j];
+                }
+                int64_t kk = n * (int64_t)ratio_bp / 10000;
+                if (kk < 1) kk = 1;
+                if (kk > n) kk = n;
+                qsort(sorted, (size_t)n, sizeof(double), cmp_desc);
+                const double thr = sorted[kk - 1];
+                for (int64_t j = 0; j <= p; ++j) {
+                    if (z[j] >= thr) C[j] += 1;
+                    if (E && fabs(z[j] - thr) <= eps) E[j] += 1;
+                }
+            }
+        free(sorted);
+        free(z);
+    }
+    return SGO_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Decode-time dynamic selection (Section 2.3: the selector picks each step's
  * KV entries from the decode query; Section 5.1: alpha = 5 and a maximum KV
  * selection ratio of 20%).  For request b, layer l and KV head h, with the G q

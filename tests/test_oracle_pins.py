@@ -787,6 +787,64 @@ def test_score_count_limits():
     np.testing.assert_array_equal(near[0, 0], seen)
 
 
+def test_score_topshare_worked_examples():
+    for c in _golden("selector_worked.json")["topshare"]:
+        k = np.array(c["k"], np.float32).reshape(1, 1, -1, 1)
+        q = np.array(c["q"], np.float32).reshape(1, 1, 1, c["W"], 1)
+        got = oracle.score_topshare(q, k, [0, len(c["k"])], 1, c["ratio_bp"])
+        np.testing.assert_array_equal(got[0, 0], c["expect"], err_msg=c["name"])
+
+
+def _brute_topshare(q, k, N, W, G, ratio_bp):
+    d = k.shape[-1]
+    out = np.zeros(N, np.int64)
+    picked = 0
+    for g in range(G):
+        for w in range(W):
+            n = N - W + w + 1
+            z = (k[:n].astype(np.float64) @ q[g, w].astype(np.float64)) / math.sqrt(d)
+            kk = min(n, max(1, n * ratio_bp // 10000))
+            order = np.argsort(-z, kind="stable")
+            thr = z[order[kk - 1]]
+            out[:n] += z >= thr
+            picked += kk
+    return out, picked
+
+
+@pytest.mark.parametrize("ratio_bp", [100, 2000, 5000])
+def test_score_topshare_brute_force(ratio_bp):
+    G, W, d, N = 3, 5, 8, 60
+    q = _rand((1, 1, G, W, d), 31)
+    k = _rand((1, 1, N, d), 32)
+    got = oracle.score_topshare(q, k, [0, N], 1, ratio_bp)[0, 0]
+    want, picked = _brute_topshare(q[0, 0], k[0, 0], N, W, G, ratio_bp)
+    np.testing.assert_array_equal(got, want)
+    assert got.sum() == picked                       # distinct logits: each row picks exactly its k
+
+
+def test_score_topshare_limits():
+    G, W, d, N = 2, 6, 4, 30
+    q = _rand((1, 1, G, W, d), 33)
+    k = _rand((1, 1, N, d), 34)
+    seen = np.array([G * sum(1 for w in range(W) if N - W + w >= j) for j in range(N)])
+    # the whole share: every row picks all it sees
+    np.testing.assert_array_equal(oracle.score_topshare(q, k, [0, N], 1, 10000)[0, 0], seen)
+    # equal keys all tie with the threshold: the same closed form at any share
+    keq = np.repeat(k[:, :, :1], N, axis=2)
+    np.testing.assert_array_equal(oracle.score_topshare(q, keq, [0, N], 1, 500)[0, 0], seen)
+    # a share below one key: each row picks its argmax, as the alpha rule at alpha = 0
+    np.testing.assert_array_equal(oracle.score_topshare(q, k, [0, N], 1, 100)[0, 0],
+                                  oracle.score_count(q, k, [0, N], 1, 0.0)[0, 0])
+    # two requests and a shared-layer source address like the single-request calls
+    k2 = _rand((1, 1, 2 * N, d), 35)
+    q2 = _rand((2, 3, G, W, d), 36)
+    both = oracle.score_topshare(q2, k2, [0, N, 2 * N], 1, 3000)
+    for b in range(2):
+        for l in range(3):
+            one = oracle.score_topshare(q2[b:b + 1, l:l + 1], k2[:, :, b * N:(b + 1) * N], [0, N], 1, 3000)
+            np.testing.assert_array_equal(both[l, 0, b * N:(b + 1) * N], one[0, 0])
+
+
 def test_decode_select_worked_examples():
     for c in _golden("selector_worked.json")["select"]:
         k = np.array(c["k"], np.float32).reshape(1, 1, -1, 1)
