@@ -22,6 +22,8 @@
  *                   is sg_topk over one row of L * M importances per request
  *   sg_score_count  selection-frequency importance under the alpha-threshold
  *                   selector (Section 4.1, Section 5.1)
+ *   sg_score_topshare  selection-frequency importance when each row picks a
+ *                   fixed share of its keys (Section 4.1, Section 5.1)
  *   sg_decode_select  decode-time dynamic selection: alpha rule, capped
  *                   (Section 2.3, Section 5.1)
  *   sg_fetch_keep   on-demand fetch that keeps fetched rows in the decode
@@ -140,6 +142,37 @@ int sg_score_count(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int
                    const int32_t *cu_seqlens, int64_t T, int max_seqlen,
                    const void *q_win, const void *k, int64_t k_layer_rows,
                    float alpha, float *counts, void *ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------- sg_score_topshare
+ * Selection-frequency importance under the top-share selector (Section 4.1
+ * counts how often the selector picks an entry; Section 5.1 gives the other
+ * selector setting as the top 20% of the entries).  The window rows stand in
+ * for decode queries as in sg_score.  Row w (position p_w = N - W + w) sees
+ * n_w = p_w + 1 keys:
+ *
+ *   z_j  = q_w . k_j / sqrt(d)  (j <= p_w)
+ *   k_w  = floor(n_w * ratio_bp / 10000), clamped to [1, n_w]
+ *   t_w  = the k_w-th largest z_j of the row
+ *   counts[l][h][s0 + j] = number of (q head, window row) pairs with z_j >= t_w
+ *
+ * so a row picks its k_w largest logits and every key tied with the k_w-th
+ * (the threshold is exact: a radix select over the fp32 logits; the decisions
+ * are taken in fp32 on the raw products q . k_j, whose order the positive
+ * scale keeps; -0 equals +0).  Counts are integers in [0, G * W] stored as
+ * float, as in sg_score_count.
+ *   ratio_bp  the share in basis points, 1 .. 10000 (2000 = 20%).
+ *   ws        device workspace of at least sg_score_topshare_workspace_size
+ *             bytes (16-byte aligned): per-row thresholds and histograms;
+ *             its contents need no initialisation.
+ * Arguments and layout as sg_score (lse_in does not apply); max_seqlen must be
+ * at least every N_b.  A request with N_b < W gets all-zero counts.
+ * Calls that share a workspace must be ordered (same stream, or an event).
+ */
+size_t sg_score_topshare_workspace_size(int B, int L, int Hq, int Hkv, int d, int W, int max_seqlen);
+int sg_score_topshare(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
+                      const int32_t *cu_seqlens, int64_t T, int max_seqlen,
+                      const void *q_win, const void *k, int64_t k_layer_rows,
+                      int ratio_bp, float *counts, void *ws, size_t ws_bytes);
 
 /* ---------------------------------------------------------------- sg_topk
  * Exact top-k of every unit row (Section 2.3: each head of each request keeps

@@ -1,0 +1,412 @@
+// sg_score_topshare: selection-frequency importance when every window row
+// picks a fixed share of the keys it sees.
+//
+// Row w of q head g (prompt position p = N - W + w) sees the n = p + 1 keys
+// j <= p and picks those whose logit z_j = q . k_j / sqrt(d) is at or above
+// its k-th largest, k = floor(n * ratio_bp / 10000) clamped to [1, n]; keys
+// tied with the k-th largest are all picked.  counts[j] is the number of
+// (q head, window row) pairs of the unit that pick key j.
+//
+// The k-th largest logit of every row is found exactly by a radix select,
+// most significant digit first, over the logits' bit patterns.  A float maps
+// to an unsigned key of the same order (sign bit set for non-negative values,
+// every bit flipped for negative ones); each pass resolves one digit of DB
+// bits of every row's threshold key:
+//
+//   hist  : recompute the logits with the MFMA engine of sg_score in the
+//           C = K Q^T layout (a lane's values of a block belong to one row)
+//           and, for each value whose key matches its row's resolved prefix,
+//           add one to the row's bin of the next digit (LDS atomics, bins x
+//           rows); the chunk's nonzero bins go into the unit's global
+//           histogram with global atomics (integer adds: the result does not
+//           depend on their order);
+//   digit : per row, walk the bins from the top until the remaining rank is
+//           reached: that bin's digit extends the prefix, the rank drops by
+//           the keys above the bin, and the bins are cleared for the next
+//           pass.
+//
+// After 32 bits the prefix is the key of the row's k-th largest value.  The
+// count pass recomputes the logits in the same layout, so each row compares
+// exactly the values its threshold came from (the same MFMA operands in the
+// same order), and counts each key's picks with one wavefront ballot per
+// value (one bit per row) and population counts.
+//
+// The passes work on the raw products q . k_j: the positive scale 1/sqrt(d)
+// keeps their order.  -0 sorts just below +0 as a key, but the threshold is a
+// value that occurs and the picks compare floats, so -0 and +0 are picked
+// together, as for any other tie.
+#include <algorithm>
+
+#include "score_tiles.h"
+
+namespace sg {
+
+constexpr int TS_MAXBINS = 64;     // bins per row of the global histogram (digits of at most 6 bits)
+
+// Digit width: 6 bits (6 passes) while the bins of up to 256 rows fit in
+// LDS beside the two K tiles; 5 bits (7 passes) for 512 rows.
+template <int NW>
+struct TsDigits {
+    static constexpr int DB = NW == 8 ? 5 : 6;
+    static constexpr int NB = 1 << DB;
+};
+
+__device__ __forceinline__ uint32_t order_key(float f) {
+    const uint32_t x = __float_as_uint(f);
+    return x ^ ((uint32_t)((int32_t)x >> 31) | 0x80000000u);
+}
+
+__device__ __forceinline__ float key_value(uint32_t key) {
+    return __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
+}
+
+// One block of the histogram pass.  FIRST: the first digit, every value
+// counts.  Later passes: c = prefix ^ (the sign flip of the prefix's sign), so
+// for a value x of the prefix's sign, x ^ c = key(x) ^ prefix, whose bits
+// above the digit are zero exactly when the key matches the prefix; a value of
+// the other sign sets the top bit (the prefix always covers the sign bit).
+template <typename T, int D, int NW, bool FIRST, bool MASK>
+struct HistStep {
+    static constexpr int NRB = QFrags<T, D>::NRB;
+    uint32_t *hist;                 // LDS [bins][64 * NW]
+    const uint32_t (&c)[NRB];
+    const int (&pos)[NRB];          // window position of the lane's row (-1: padded row)
+    int lane, wave, key0, sh;
+    uint32_t lim;                   // bins of this pass
+    __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
+        using M = MT<T, D>;
+        uint32_t *h = hist + wave * 64 + rb * M::BM + lane % M::BM;      // bin 0 of the lane's row
+#pragma unroll
+        for (int v = 0; v < M::NV; ++v) {
+            const uint32_t t = FIRST ? order_key(acc[v]) >> sh : (__float_as_uint(acc[v]) ^ c[rb]) >> sh;
+            bool take = FIRST || t < lim;
+            if (MASK) take = take && key0 + kb * M::BM + M::crow(v, lane) <= pos[rb];
+            if (take) __hip_atomic_fetch_add(h + t * (64 * NW), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+    }
+};
+
+template <typename T, int D, int NW, bool FIRST>
+__global__ __launch_bounds__(64 * NW) void ts_hist_kernel(
+    int B, int L, int Hq, int Hkv, int W, const int32_t *__restrict__ cu_seqlens, int64_t T_,
+    const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, int nchunk, int chunk_keys,
+    int sh, int width, const uint32_t *__restrict__ pre, uint32_t *__restrict__ ghist) {
+    using M = MT<T, D>;
+    using KT = KTile<T, D>;
+    constexpr int NRB = QFrags<T, D>::NRB, ROWS = 64 * NW, NB = TsDigits<NW>::NB;
+    __shared__ __attribute__((aligned(16))) char kbA[KT::BYTES];
+    __shared__ __attribute__((aligned(16))) char kbB[KT::BYTES];
+    __shared__ __attribute__((aligned(16))) uint32_t hist[NB * ROWS];
+    int64_t u;
+    int chunk;
+    unit_chunk((int64_t)L * Hkv * B, nchunk, u, chunk);
+    const UnitGeom g = unit_geom(u, B, Hkv, cu_seqlens, T_);
+    const int G = Hq / Hkv, R = G * W;
+    const int N = (int)g.N;
+    const int key_begin = chunk * chunk_keys;
+    if (N < W || key_begin >= N) return;
+    const int lane = threadIdx.x % 64;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    const T *qunit = q_win + (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * W * D;
+    const T *kunit = k + ((int64_t)g.l * k_layer_rows + (int64_t)g.h * T_ + g.s0) * D;
+    const int key_end = min(N, key_begin + chunk_keys);
+    const int ntile = (int)ceil_div(key_end - key_begin, KT::TK);
+    KT::template load<NW>(kbA, kunit, key_begin, N, wave, lane);
+    QFrags<T, D> q;
+    q.load(qunit, R, wave, lane);
+    const int nbins = 1 << width;
+    for (int i = threadIdx.x; i < nbins * ROWS / 4; i += 64 * NW)
+        reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0u, 0u, 0u, 0u);
+    uint32_t c[NRB];
+    int pos[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+        const int row = wave * 64 + rb * M::BM + lane % M::BM;
+        pos[rb] = row < R ? N - W + row % W : -1;
+        const uint32_t p = (!FIRST && row < R) ? pre[u * R + row] : 0u;
+        c[rb] = p ^ ((p & 0x80000000u) ? 0x80000000u : 0xffffffffu);
+    }
+    TC<T, D> zero[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) zero[rb] = M::zero();
+    auto step = [&](int t, char *cur, char *nxt, auto mask) {
+        constexpr bool MASK = decltype(mask)::value;
+        barrier_after_loads();      // tile t landed (and the bins are clear); tile t - 1 done everywhere
+        const int key0 = key_begin + t * KT::TK;
+        if (t + 1 < ntile) KT::template load<NW>(nxt, kunit, key0 + KT::TK, N, wave, lane);
+        const HistStep<T, D, NW, FIRST, MASK> f{hist, c, pos, lane, wave, key0, sh, (uint32_t)nbins};
+        if (MASK) tile_sweep_plain<T, D, true>(cur, q, zero, lane, f);
+        else tile_sweep<T, D, true>(cur, q, zero, lane, f);
+    };
+    const int nfull = full_tiles(key_begin, ntile, KT::TK, N, W);
+    int t = 0;
+    for (; t + 1 < nfull; t += 2) {
+        step(t, kbA, kbB, std::false_type{});
+        step(t + 1, kbB, kbA, std::false_type{});
+    }
+    for (; t < ntile; ++t) {
+        if (t & 1) step(t, kbB, kbA, std::true_type{});
+        else step(t, kbA, kbB, std::true_type{});
+    }
+    barrier_after_loads();      // every bin final, no load in flight
+    uint32_t *gh = ghist + u * NB * (int64_t)R;
+    for (int i = threadIdx.x; i < nbins * ROWS; i += 64 * NW) {
+        const int row = i % ROWS;
+        const uint32_t v = hist[i];
+        if (row < R && v != 0u)
+            __hip_atomic_fetch_add(gh + (int64_t)(i / ROWS) * R + row, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// One thread per (unit, row): the start of the select.  need = k, the rank
+// (from the top) of the wanted key; prefix = 0; the unit's bins cleared.
+__global__ __launch_bounds__(256) void ts_init_kernel(int64_t nrows, int R, int W, int B, int Hkv,
+                                                      const int32_t *__restrict__ cu_seqlens, int64_t T_,
+                                                      int ratio_bp, uint32_t *__restrict__ pre,
+                                                      uint32_t *__restrict__ need, uint32_t *__restrict__ ghist,
+                                                      int nb) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= nrows) return;
+    const int64_t u = i / R;
+    const int r = (int)(i % R);
+    const UnitGeom g = unit_geom(u, B, Hkv, cu_seqlens, T_);
+    const int64_t n = g.N - W + r % W + 1;                 // keys the row sees
+    const int64_t kk = std::min<int64_t>(std::max<int64_t>(n, 1), std::max<int64_t>(1, n * ratio_bp / 10000));
+    pre[i] = 0u;
+    need[i] = (uint32_t)kk;
+    uint32_t *h = ghist + u * nb * (int64_t)R + r;
+    for (int b = 0; b < nb; ++b) h[(int64_t)b * R] = 0u;
+}
+
+// One thread per (unit, row): pick this pass's digit of the threshold key.
+// The bins of a row are R words apart, so a wavefront's 64 rows read each bin
+// as one contiguous run.
+__global__ __launch_bounds__(256) void ts_digit_kernel(int64_t nrows, int R, int nb, int sh, int width,
+                                                       uint32_t *__restrict__ pre, uint32_t *__restrict__ need,
+                                                       uint32_t *__restrict__ ghist) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= nrows) return;
+    const int64_t u = i / R;
+    const int r = (int)(i % R);
+    uint32_t *h = ghist + u * nb * (int64_t)R + r;
+    const uint32_t nd = need[i];
+    uint32_t above = 0u, digit = 0u, rest = nd;
+    bool found = false;
+    for (int b = (1 << width) - 1; b >= 0; --b) {
+        const uint32_t cnt = h[(int64_t)b * R];
+        h[(int64_t)b * R] = 0u;
+        if (!found && above + cnt >= nd) {
+            found = true;
+            digit = (uint32_t)b;
+            rest = nd - above;
+        }
+        above += cnt;
+    }
+    pre[i] |= digit << sh;
+    need[i] = rest;
+}
+
+// One block of the count pass: a ballot per value (bit = lane = row), whose
+// lane groups hold different keys; a key's picks in the block are the
+// population count of its lane group.  Four consecutive keys' counts go to
+// LDS in one write (lane 0), one slot per row block.
+template <typename T, int D, bool MASK>
+struct TsCountStep {
+    static constexpr int NRB = QFrags<T, D>::NRB, GR = 64 / MT<T, D>::BM;
+    uint32_t *cs;                          // LDS [NRB][tile keys]: this wavefront's picks
+    const float (&thr)[NRB];               // the lane's row's threshold (+inf: padded row)
+    const int (&pos)[NRB];
+    int lane, key0;
+    __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
+        using M = MT<T, D>;
+        constexpr uint32_t GMASK = (uint32_t)((1ull << M::BM) - 1);
+#pragma unroll
+        for (int v4 = 0; v4 < M::NV / 4; ++v4) {
+            uint32_t n[GR][4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int v = 4 * v4 + i;
+                bool pick = acc[v] >= thr[rb];
+                if (MASK) pick = pick && key0 + kb * M::BM + M::crow(v, lane) <= pos[rb];
+                const uint64_t m = __ballot(pick);
+#pragma unroll
+                for (int gi = 0; gi < GR; ++gi) n[gi][i] = (uint32_t)__popc((uint32_t)(m >> (gi * M::BM)) & GMASK);
+            }
+            // keys crow(4 v4 + i, gi * BM), i = 0..3, are consecutive
+            if (lane == 0) {
+#pragma unroll
+                for (int gi = 0; gi < GR; ++gi)
+                    *reinterpret_cast<uint4 *>(cs + rb * KTile<T, D>::TK + kb * M::BM + M::crow(4 * v4, gi * M::BM)) =
+                        make_uint4(n[gi][0], n[gi][1], n[gi][2], n[gi][3]);
+            }
+        }
+    }
+};
+
+template <typename T, int D, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void ts_count_kernel(
+    int B, int L, int Hq, int Hkv, int W, const int32_t *__restrict__ cu_seqlens, int64_t T_,
+    const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, int nchunk, int chunk_keys,
+    const uint32_t *__restrict__ pre, float *__restrict__ counts) {
+    using M = MT<T, D>;
+    using KT = KTile<T, D>;
+    constexpr int NRB = QFrags<T, D>::NRB;
+    __shared__ __attribute__((aligned(16))) char kbA[KT::BYTES];
+    __shared__ __attribute__((aligned(16))) char kbB[KT::BYTES];
+    __shared__ __attribute__((aligned(16))) uint32_t csum[2][NW][NRB][KT::TK];
+    int64_t u;
+    int chunk;
+    unit_chunk((int64_t)L * Hkv * B, nchunk, u, chunk);
+    const UnitGeom g = unit_geom(u, B, Hkv, cu_seqlens, T_);
+    const int G = Hq / Hkv, R = G * W;
+    const int N = (int)g.N;
+    const int key_begin = chunk * chunk_keys;
+    const int key_end = min(N, key_begin + chunk_keys);
+    float *orow = counts + ((int64_t)g.l * Hkv + g.h) * T_ + g.s0;
+    if (N < W) {  // documented fallback: zero counts
+        for (int j = key_begin + (int)threadIdx.x; j < key_end; j += blockDim.x) orow[j] = 0.f;
+        return;
+    }
+    if (key_begin >= N) return;
+    const int lane = threadIdx.x % 64;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    const T *qunit = q_win + (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * W * D;
+    const T *kunit = k + ((int64_t)g.l * k_layer_rows + (int64_t)g.h * T_ + g.s0) * D;
+    const int ntile = (int)ceil_div(key_end - key_begin, KT::TK);
+    KT::template load<NW>(kbA, kunit, key_begin, N, wave, lane);
+    QFrags<T, D> q;
+    q.load(qunit, R, wave, lane);
+    float thr[NRB];
+    int pos[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+        const int row = wave * 64 + rb * M::BM + lane % M::BM;
+        pos[rb] = row < R ? N - W + row % W : -1;
+        thr[rb] = row < R ? key_value(pre[u * R + row]) : INFINITY;
+    }
+    TC<T, D> zero[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) zero[rb] = M::zero();
+    // the wavefronts' picks of tile t sit in csum[t & 1]; they are added and
+    // stored after the next barrier
+    auto flush = [&](int t) {
+        const int key0 = key_begin + t * KT::TK;
+        for (int j = threadIdx.x; j < KT::TK; j += 64 * NW) {
+            uint32_t v = 0u;
+            for (int w = 0; w < NW; ++w)
+                for (int rb = 0; rb < NRB; ++rb) v += csum[t & 1][w][rb][j];
+            if (key0 + j < N) orow[key0 + j] = (float)v;
+        }
+    };
+    auto step = [&](int t, char *cur, char *nxt, auto mask) {
+        constexpr bool MASK = decltype(mask)::value;
+        barrier_after_loads();      // tile t landed; tile t - 1 finished everywhere
+        if (t > 0) flush(t - 1);
+        const int key0 = key_begin + t * KT::TK;
+        if (t + 1 < ntile) KT::template load<NW>(nxt, kunit, key0 + KT::TK, N, wave, lane);
+        const TsCountStep<T, D, MASK> f{&csum[t & 1][wave][0][0], thr, pos, lane, key0};
+        if (MASK) tile_sweep_plain<T, D, true>(cur, q, zero, lane, f);
+        else tile_sweep<T, D, true>(cur, q, zero, lane, f);
+    };
+    const int nfull = full_tiles(key_begin, ntile, KT::TK, N, W);
+    int t = 0;
+    for (; t + 1 < nfull; t += 2) {
+        step(t, kbA, kbB, std::false_type{});
+        step(t + 1, kbB, kbA, std::false_type{});
+    }
+    for (; t < ntile; ++t) {
+        if (t & 1) step(t, kbB, kbA, std::true_type{});
+        else step(t, kbA, kbB, std::true_type{});
+    }
+    barrier_after_loads();
+    flush(ntile - 1);
+}
+
+template <typename T, int D, int NW>
+static void launch_topshare(hipStream_t s, const ScorePlan &p, int B, int L, int Hq, int Hkv, int W,
+                            const int32_t *cu_seqlens, int64_t ntok, const void *q_win, const void *k,
+                            int64_t k_layer_rows, int ratio_bp, float *counts, void *ws) {
+    constexpr int DB = TsDigits<NW>::DB, NB = TsDigits<NW>::NB;
+    const int R = (Hq / Hkv) * W;
+    const int64_t units = (int64_t)L * Hkv * B, nrows = units * R;
+    uint32_t *pre = reinterpret_cast<uint32_t *>(ws);
+    uint32_t *need = pre + nrows;
+    uint32_t *gh = need + nrows;
+    const T *q = reinterpret_cast<const T *>(q_win);
+    const T *kk = reinterpret_cast<const T *>(k);
+    const dim3 rgrid((unsigned)ceil_div(nrows, 256));
+    const dim3 grid((unsigned)(units * p.nchunk));
+    ts_init_kernel<<<rgrid, 256, 0, s>>>(nrows, R, W, B, Hkv, cu_seqlens, ntok, ratio_bp, pre, need, gh, NB);
+    for (int hi = 32; hi > 0;) {
+        const int sh = std::max(0, hi - DB), width = hi - sh;
+        if (hi == 32)
+            ts_hist_kernel<T, D, NW, true><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                                  k_layer_rows, p.nchunk, p.chunk_keys, sh, width,
+                                                                  pre, gh);
+        else
+            ts_hist_kernel<T, D, NW, false><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                                   k_layer_rows, p.nchunk, p.chunk_keys, sh, width,
+                                                                   pre, gh);
+        ts_digit_kernel<<<rgrid, 256, 0, s>>>(nrows, R, NB, sh, width, pre, need, gh);
+        hi = sh;
+    }
+    ts_count_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk, k_layer_rows,
+                                                      p.nchunk, p.chunk_keys, pre, counts);
+}
+
+template <typename T, int D>
+static int topshare_dispatch(hipStream_t s, int B, int L, int Hq, int Hkv, int W, const int32_t *cu_seqlens,
+                             int64_t ntok, int max_seqlen, const void *q_win, const void *k, int64_t k_layer_rows,
+                             int ratio_bp, float *counts, void *ws) {
+    const int R = (Hq / Hkv) * W;
+    const int nw = (int)ceil_div(R, 64);
+    const ScorePlan p = score_plan(B, L, Hkv, max_seqlen);
+    if (nw <= 1) launch_topshare<T, D, 1>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, ratio_bp, counts, ws);
+    else if (nw <= 2) launch_topshare<T, D, 2>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, ratio_bp, counts, ws);
+    else if (nw <= 4) launch_topshare<T, D, 4>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, ratio_bp, counts, ws);
+    else launch_topshare<T, D, 8>(s, p, B, L, Hq, Hkv, W, cu_seqlens, ntok, q_win, k, k_layer_rows, ratio_bp, counts, ws);
+    return launch_status("sg_score_topshare");
+}
+
+}  // namespace sg
+
+using namespace sg;
+
+extern "C" size_t sg_score_topshare_workspace_size(int B, int L, int Hq, int Hkv, int d, int W, int max_seqlen) {
+    if (B <= 0 || L <= 0 || Hkv <= 0 || Hq <= 0 || W <= 0 || max_seqlen <= 0 || d <= 0) return 0;
+    const int64_t rows = (int64_t)L * Hkv * B * (Hq / Hkv) * W;
+    return (size_t)(rows * (2 + TS_MAXBINS)) * sizeof(uint32_t);
+}
+
+extern "C" int sg_score_topshare(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
+                                 const int32_t *cu_seqlens, int64_t T, int max_seqlen, const void *q_win,
+                                 const void *k, int64_t k_layer_rows, int ratio_bp, float *counts, void *ws,
+                                 size_t ws_bytes) {
+    const char *name = "sg_score_topshare";
+    SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "%s: unknown dtype %d", name, (int)dt);
+    SG_REQUIRE(B >= 1 && L >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0, SG_EINVAL,
+               "%s: need B, L, Hq, Hkv >= 1 and Hq %% Hkv == 0", name);
+    SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "%s: head dimension %d not supported (64 or 128)", name, d);
+    SG_REQUIRE(W >= 1, SG_EINVAL, "%s: window must be >= 1", name);
+    SG_REQUIRE((int64_t)(Hq / Hkv) * W <= SC_MAXR, SG_EUNSUPPORTED, "%s: G*W = %d above %d", name, (Hq / Hkv) * W,
+               SC_MAXR);
+    SG_REQUIRE(ratio_bp >= 1 && ratio_bp <= 10000, SG_EINVAL, "%s: ratio_bp %d outside [1, 10000]", name, ratio_bp);
+    SG_REQUIRE(T >= 0 && max_seqlen >= 0 && k_layer_rows >= 0, SG_EINVAL, "%s: negative size", name);
+    SG_REQUIRE(max_seqlen <= (1 << 30), SG_EINVAL, "%s: max_seqlen too large", name);
+    if (T == 0 || max_seqlen == 0) return SG_OK;
+    SG_REQUIRE(cu_seqlens && q_win && k && counts, SG_EINVAL, "%s: null pointer", name);
+    SG_REQUIRE(aligned16(q_win) && aligned16(k), SG_EINVAL, "%s: q_win and k must be 16-byte aligned", name);
+    const int64_t units = (int64_t)L * Hkv * B;
+    SG_REQUIRE(units * ceil_div(max_seqlen, 128) <= 0x7fffffff, SG_EINVAL, "%s: grid too large", name);
+    SG_REQUIRE(units * (Hq / Hkv) * W <= (int64_t)0x7fffffff, SG_EINVAL, "%s: too many rows", name);
+    const size_t need = sg_score_topshare_workspace_size(B, L, Hq, Hkv, d, W, max_seqlen);
+    SG_REQUIRE(ws && ws_bytes >= need, SG_EWORKSPACE, "%s: workspace %zu < %zu", name, ws_bytes, need);
+    SG_REQUIRE(aligned16(ws), SG_EINVAL, "%s: workspace must be 16-byte aligned", name);
+    hipStream_t s = as_stream(stream);
+    if (dt == SG_BF16) {
+        if (d == 128) return topshare_dispatch<uint16_t, 128>(s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, ratio_bp, counts, ws);
+        return topshare_dispatch<uint16_t, 64>(s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, ratio_bp, counts, ws);
+    }
+    if (d == 128) return topshare_dispatch<float, 128>(s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, ratio_bp, counts, ws);
+    return topshare_dispatch<float, 64>(s, B, L, Hq, Hkv, W, cu_seqlens, T, max_seqlen, q_win, k, k_layer_rows, ratio_bp, counts, ws);
+}

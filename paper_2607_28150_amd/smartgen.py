@@ -32,6 +32,7 @@ EXPORTS = [
     "sg_block_importance", "sg_block_budget", "sg_pack_blocks_bytes", "sg_pack_blocks",
     "sg_fetch_keep", "sg_spec_quota", "sg_spec_push", "sg_spec_commit", "sg_score_count",
     "sg_decode_select_workspace_size", "sg_decode_select",
+    "sg_score_topshare_workspace_size", "sg_score_topshare",
 ]
 
 
@@ -80,6 +81,9 @@ def load() -> ctypes.CDLL:
     lib.sg_fetch_keep.argtypes = [_vp, _i, _i, _i, _vp, _l, _vp, _vp, _vp, _l, _vp, _vp, _vp, _i, _i, _vp, _vp, _vp,
                                   _l, _vp, _vp, _vp, _l, _vp, _l, _vp, _vp]
     lib.sg_score_count.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _l, _i, _vp, _vp, _l, _f, _vp, _vp, _sz]
+    lib.sg_score_topshare_workspace_size.argtypes = [_i] * 7
+    lib.sg_score_topshare_workspace_size.restype = _sz
+    lib.sg_score_topshare.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _l, _i, _vp, _vp, _l, _i, _vp, _vp, _sz]
     lib.sg_decode_select_workspace_size.argtypes = [_i, _i, _i, _i]
     lib.sg_decode_select_workspace_size.restype = _sz
     lib.sg_decode_select.argtypes = [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _l, _i, _vp, _l, _f, _f, _vp, _l, _vp,
@@ -91,7 +95,7 @@ def load() -> ctypes.CDLL:
     for f in ("sg_score", "sg_topk", "sg_pack", "sg_split", "sg_fetch", "sg_decode_attn", "sg_decode_attn_noalloc",
               "sg_block_importance",
               "sg_pack_blocks", "sg_fetch_keep", "sg_spec_push", "sg_spec_commit", "sg_score_count",
-              "sg_decode_select"):
+              "sg_decode_select", "sg_score_topshare"):
         getattr(lib, f).restype = _i
     _lib = lib
     return lib
@@ -194,6 +198,29 @@ def sg_score_count(q_win, k, cu_seqlens, T, max_seqlen, Hkv, counts, alpha, ws, 
                                int(max_seqlen), _ptr(q_win), _ptr(k), int(k_layer_rows), float(alpha), _ptr(counts),
                                _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size())
     _check("sg_score_count", rc)
+    return counts
+
+
+def score_topshare_workspace_size(B, L, Hq, Hkv, d, W, max_seqlen) -> int:
+    return int(load().sg_score_topshare_workspace_size(B, L, Hq, Hkv, d, W, max_seqlen))
+
+
+def sg_score_topshare(q_win, k, cu_seqlens, T, max_seqlen, Hkv, counts, ratio_bp, ws, k_layer_rows=None,
+                      stream=None):
+    """counts[L][Hkv][T] (float32 integers, written): how many (q head, window row)
+    pairs pick each key when every row picks its top ratio_bp / 10000 of the
+    keys it sees (ties with the row's threshold included)."""
+    B, L, Hq, W, d = q_win.shape
+    _need(k.dtype == q_win.dtype, "q_win and k must share a dtype")
+    _need(counts.dtype == torch.float32 and counts.numel() >= L * Hkv * T, "counts must be float32 [L][Hkv][T]")
+    _need(cu_seqlens.dtype == torch.int32 and cu_seqlens.numel() == B + 1, "cu_seqlens must be int32 [B+1]")
+    if k_layer_rows is None:
+        k_layer_rows = 0 if (k.dim() == 4 and k.shape[0] == 1 and L > 1) else Hkv * T
+    _need(k.numel() >= ((L - 1) * k_layer_rows + Hkv * T) * d, "k is smaller than its layout needs")
+    rc = load().sg_score_topshare(_stream(stream), _dtype_code(q_win), B, L, Hq, Hkv, d, W, _ptr(cu_seqlens),
+                                  int(T), int(max_seqlen), _ptr(q_win), _ptr(k), int(k_layer_rows), int(ratio_bp),
+                                  _ptr(counts), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size())
+    _check("sg_score_topshare", rc)
     return counts
 
 
