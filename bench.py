@@ -1049,13 +1049,13 @@ def decode_side(sg, nsteps=12, long_steps=256, ratio_bp=1000, M=1024):
 
 def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=5.0, cap_bp=2000):
     """Selector variants on the request of the 8B 8K workload: the alpha-rule
-    selection-frequency score (Section 4.1 importance under the Section 5.1
-    selector) and decode-time dynamic selection (Section 2.3; alpha 5, at most
-    20% of the tokens), each timed on its own; then the on-demand ratio
-    (Section 3: entries the decode step selects that were not sent at prefill)
-    seen by that decode-time selector over `nsteps` steps, for four proactive
-    choices of the same budget: top-k of the window score, top-k of the
-    alpha-rule counts, the first tokens, and a random set."""
+    and top-20% selection-frequency scores (Section 4.1 importance under either
+    Section 5.1 selector) and decode-time dynamic selection (Section 2.3; alpha
+    5, at most 20% of the tokens), each timed on its own; then the on-demand
+    ratio (Section 3: entries the decode step selects that were not sent at
+    prefill) seen by that decode-time selector over `nsteps` steps, for five
+    proactive choices of the same budget: top-k of the window score, top-k of
+    either selector's counts, the first tokens, and a random set."""
     import numpy as np
     import torch
     from datagen import inputs
@@ -1069,6 +1069,13 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     t_count = median_ms(lambda i: sg.sg_score_count(pre["q_win"], pre["k"], cus, T, N, Hkv, counts, alpha, ws))
     idx_count = torch.empty_like(idx_score)
     sg.sg_topk(counts, cus, T, N, cuk, K_total, idx_count)
+    # the other Section 5.1 selector: each window row picks its top 20%
+    ts_counts = torch.empty((L, Hkv, T), device=dev)
+    ws_ts = torch.empty(sg.score_topshare_workspace_size(1, L, Hq, Hkv, d, W, N), dtype=torch.uint8, device=dev)
+    t_ts = median_ms(lambda i: sg.sg_score_topshare(pre["q_win"], pre["k"], cus, T, N, Hkv, ts_counts, cap_bp, ws_ts))
+    idx_ts = torch.empty_like(idx_score)
+    sg.sg_topk(ts_counts, cus, T, N, cuk, K_total, idx_ts)
+    ts_passes = 1 + (6 if cfg.G * W <= 256 else 7)       # one logit recompute per digit, then the count pass
     cap = N * cap_bp // 10000
     cu_cap = torch.tensor([0, cap], dtype=torch.int32, device=dev)
     ws_sel = torch.empty(sg.decode_select_workspace_size(1, L, Hq, N), dtype=torch.uint8, device=dev)
@@ -1102,6 +1109,7 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     ratios = {}
     sel_frac = []
     for name, sel, partial in (("score", idx_score, False), ("count", idx_count, False),
+                               ("topshare_count", idx_ts, False),
                                ("sequential", seq, False), ("random", rnd, False),
                                ("score_partial_selector", idx_score, True)):
         mask = torch.full((units, N), 2, dtype=torch.int8, device=dev)
@@ -1121,6 +1129,10 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     return {"alpha": alpha, "count_score": {"ms": r4(t_count), "tflops": round(score_flops / (t_count * 1e-3) / 1e12, 1),
                                             "frac_mfma_peak": r4(score_flops / (t_count * 1e-3) / 1e12
                                                                  / BF16_MFMA_PEAK_TFLOPS)},
+            "topshare_score": {"ratio_bp": cap_bp, "ms": r4(t_ts), "logit_passes": ts_passes,
+                               "tflops_all_passes": round(ts_passes * score_flops / (t_ts * 1e-3) / 1e12, 1),
+                               "frac_mfma_peak_all_passes": r4(ts_passes * score_flops / (t_ts * 1e-3) / 1e12
+                                                               / BF16_MFMA_PEAK_TFLOPS)},
             "decode_select": {"ms": r4(t_sel), "cap": cap, "k_read_gbs": round(gbs(k_bytes, t_sel), 1),
                               "frac_hbm_peak": r4(gbs(k_bytes, t_sel) / HBM_PEAK_GBS),
                               "selected_fraction": r4(np.mean(sel_frac))},

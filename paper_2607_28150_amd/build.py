@@ -24,13 +24,21 @@ CFLAGS = [
     "-I", os.path.join(_ROOT, "include"),
 ]
 
+# Per-file additions.  topshare.hip: its histogram kernels hold 130 KB of LDS,
+# so one workgroup per CU and a register budget above 256, where the compiler
+# would put the MFMA accumulators in AGPRs and copy every value out before the
+# vector work; the VGPR form fits the bf16 kernels in 256 VGPRs without spills.
+FILE_FLAGS = {
+    "topshare.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
 
 def _hipcc() -> str:
     return os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "bin", "hipcc")
 
 
 def _compile(src: str, obj: str, verbose: bool) -> None:
-    cmd = [_hipcc(), *CFLAGS, "-c", src, "-o", obj]
+    cmd = [_hipcc(), *CFLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

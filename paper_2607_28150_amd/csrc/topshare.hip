@@ -25,16 +25,23 @@
 //           the keys above the bin, and the bins are cleared for the next
 //           pass.
 //
-// After 32 bits the prefix is the key of the row's k-th largest value.  The
-// count pass recomputes the logits in the same layout, so each row compares
-// exactly the values its threshold came from (the same MFMA operands in the
-// same order), and counts each key's picks with one wavefront ballot per
-// value (one bit per row) and population counts.
+// After 32 bits the prefix is the key of the row's k-th largest value.  A row
+// settles earlier when its chosen bin holds exactly the keys it still needs:
+// then every key at or above the bin's lower edge is picked and nothing below
+// it.  Once every row of a unit has settled, the unit's remaining passes
+// return at once (real-valued logits settle after about 30 bits).  The count
+// pass recomputes the logits in the same layout, so each row compares exactly
+// the values its threshold came from (the same MFMA operands in the same
+// order), and counts each key's picks with one wavefront ballot per value (one
+// bit per row) and population counts.
 //
 // The passes work on the raw products q . k_j: the positive scale 1/sqrt(d)
-// keeps their order.  -0 sorts just below +0 as a key, but the threshold is a
-// value that occurs and the picks compare floats, so -0 and +0 are picked
-// together, as for any other tie.
+// keeps their order.  The picks compare floats against the threshold: the
+// row's k-th largest value, or a settled bin's lower edge (the float of the
+// smallest key in the bin's range, -inf below the keys of -inf), which picks
+// exactly the keys at or above the edge.  -0 sorts just below +0 as a key; as
+// floats they are equal and picked together, as for any other tie, so a bin
+// whose lower edge is +0 does not settle early (-0 would tie it).
 #include <algorithm>
 
 #include "score_tiles.h"
@@ -42,6 +49,7 @@
 namespace sg {
 
 constexpr int TS_MAXBINS = 64;     // bins per row of the global histogram (digits of at most 6 bits)
+constexpr int TS_MAXPASS = 8;      // per-unit flag words per call (7 passes at most)
 
 // Digit width: 6 bits (6 passes) while the bins of up to 256 rows fit in
 // LDS beside the two K tiles; 5 bits (7 passes) for 512 rows.
@@ -60,6 +68,12 @@ __device__ __forceinline__ float key_value(uint32_t key) {
     return __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
 }
 
+// The float threshold of a row whose picks are the keys >= key.
+__device__ __forceinline__ float threshold_value(uint32_t key) {
+    constexpr uint32_t NEG_INF_KEY = 0x007fffffu;         // order_key(-inf); keys below it are NaN patterns
+    return key < NEG_INF_KEY ? -INFINITY : key_value(key);
+}
+
 // One block of the histogram pass.  FIRST: the first digit, every value
 // counts.  Later passes: c = prefix ^ (the sign flip of the prefix's sign), so
 // for a value x of the prefix's sign, x ^ c = key(x) ^ prefix, whose bits
@@ -72,34 +86,38 @@ struct HistStep {
     const uint32_t (&c)[NRB];
     const int (&pos)[NRB];          // window position of the lane's row (-1: padded row)
     int lane, wave, key0, sh;
-    uint32_t lim;                   // bins of this pass
+    uint32_t lim;                   // bins of this pass (bin lim takes the values that do not count)
     __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
         using M = MT<T, D>;
         uint32_t *h = hist + wave * 64 + rb * M::BM + lane % M::BM;      // bin 0 of the lane's row
+        // no branch per value (it would split the block and undo the MFMA /
+        // vector interleave): a value that does not count goes to bin lim,
+        // which is never read
 #pragma unroll
         for (int v = 0; v < M::NV; ++v) {
-            const uint32_t t = FIRST ? order_key(acc[v]) >> sh : (__float_as_uint(acc[v]) ^ c[rb]) >> sh;
-            bool take = FIRST || t < lim;
-            if (MASK) take = take && key0 + kb * M::BM + M::crow(v, lane) <= pos[rb];
-            if (take) __hip_atomic_fetch_add(h + t * (64 * NW), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            uint32_t t = FIRST ? order_key(acc[v]) >> sh : min((__float_as_uint(acc[v]) ^ c[rb]) >> sh, lim);
+            if (MASK) t = key0 + kb * M::BM + M::crow(v, lane) <= pos[rb] ? t : lim;
+            __hip_atomic_fetch_add(h + t * (64 * NW), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
     }
 };
 
 template <typename T, int D, int NW, bool FIRST>
-__global__ __launch_bounds__(64 * NW) void ts_hist_kernel(
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void ts_hist_kernel(
     int B, int L, int Hq, int Hkv, int W, const int32_t *__restrict__ cu_seqlens, int64_t T_,
     const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, int nchunk, int chunk_keys,
-    int sh, int width, const uint32_t *__restrict__ pre, uint32_t *__restrict__ ghist) {
+    int sh, int width, const uint32_t *__restrict__ busy, const uint32_t *__restrict__ pre,
+    uint32_t *__restrict__ ghist) {
     using M = MT<T, D>;
     using KT = KTile<T, D>;
     constexpr int NRB = QFrags<T, D>::NRB, ROWS = 64 * NW, NB = TsDigits<NW>::NB;
     __shared__ __attribute__((aligned(16))) char kbA[KT::BYTES];
     __shared__ __attribute__((aligned(16))) char kbB[KT::BYTES];
-    __shared__ __attribute__((aligned(16))) uint32_t hist[NB * ROWS];
+    __shared__ __attribute__((aligned(16))) uint32_t hist[(NB + 1) * ROWS];
     int64_t u;
     int chunk;
     unit_chunk((int64_t)L * Hkv * B, nchunk, u, chunk);
+    if (!FIRST && busy[u] == 0u) return;        // every row of the unit has settled
     const UnitGeom g = unit_geom(u, B, Hkv, cu_seqlens, T_);
     const int G = Hq / Hkv, R = G * W;
     const int N = (int)g.N;
@@ -159,12 +177,13 @@ __global__ __launch_bounds__(64 * NW) void ts_hist_kernel(
 }
 
 // One thread per (unit, row): the start of the select.  need = k, the rank
-// (from the top) of the wanted key; prefix = 0; the unit's bins cleared.
+// (from the top) of the wanted key; prefix = 0; the unit's bins and its
+// per-pass flags cleared.
 __global__ __launch_bounds__(256) void ts_init_kernel(int64_t nrows, int R, int W, int B, int Hkv,
                                                       const int32_t *__restrict__ cu_seqlens, int64_t T_,
                                                       int ratio_bp, uint32_t *__restrict__ pre,
                                                       uint32_t *__restrict__ need, uint32_t *__restrict__ ghist,
-                                                      int nb) {
+                                                      int nb, uint32_t *__restrict__ busy, int64_t units) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= nrows) return;
     const int64_t u = i / R;
@@ -176,34 +195,53 @@ __global__ __launch_bounds__(256) void ts_init_kernel(int64_t nrows, int R, int 
     need[i] = (uint32_t)kk;
     uint32_t *h = ghist + u * nb * (int64_t)R + r;
     for (int b = 0; b < nb; ++b) h[(int64_t)b * R] = 0u;
+    if (r == 0)
+        for (int k = 0; k < TS_MAXPASS; ++k) busy[k * units + u] = 0u;
 }
 
 // One thread per (unit, row): pick this pass's digit of the threshold key.
 // The bins of a row are R words apart, so a wavefront's 64 rows read each bin
-// as one contiguous run.
+// as one contiguous run; eight bins are read before any is used.  need = 0
+// marks a settled row (its bins are only cleared).  busy_in: the flags the
+// previous pass set (a unit without one did not run this pass); busy_out: set
+// for the unit of every row that has not settled (NULL after the last digit).
 __global__ __launch_bounds__(256) void ts_digit_kernel(int64_t nrows, int R, int nb, int sh, int width,
-                                                       uint32_t *__restrict__ pre, uint32_t *__restrict__ need,
-                                                       uint32_t *__restrict__ ghist) {
+                                                       const uint32_t *__restrict__ busy_in,
+                                                       uint32_t *__restrict__ busy_out, uint32_t *__restrict__ pre,
+                                                       uint32_t *__restrict__ need, uint32_t *__restrict__ ghist) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= nrows) return;
     const int64_t u = i / R;
     const int r = (int)(i % R);
+    if (busy_in && busy_in[u] == 0u) return;        // settled unit: its pass did not run, the bins are clear
     uint32_t *h = ghist + u * nb * (int64_t)R + r;
     const uint32_t nd = need[i];
-    uint32_t above = 0u, digit = 0u, rest = nd;
+    uint32_t above = 0u, digit = 0u, rest = nd, in_bin = 0u;
     bool found = false;
-    for (int b = (1 << width) - 1; b >= 0; --b) {
-        const uint32_t cnt = h[(int64_t)b * R];
-        h[(int64_t)b * R] = 0u;
-        if (!found && above + cnt >= nd) {
-            found = true;
-            digit = (uint32_t)b;
-            rest = nd - above;
+    for (int b0 = (1 << width) - 1; b0 >= 0; b0 -= 8) {          // bins come in fours: 4, 32 or 64
+        uint32_t c[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) c[j] = b0 - j >= 0 ? h[(int64_t)(b0 - j) * R] : 0u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (b0 - j >= 0) h[(int64_t)(b0 - j) * R] = 0u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (!found && b0 - j >= 0 && above + c[j] >= nd) {
+                found = true;
+                digit = (uint32_t)(b0 - j);
+                rest = nd - above;
+                in_bin = c[j];
+            }
+            above += c[j];
         }
-        above += cnt;
     }
-    pre[i] |= digit << sh;
-    need[i] = rest;
+    if (nd == 0u) return;
+    const uint32_t p = pre[i] | (digit << sh);
+    pre[i] = p;
+    const bool settled = rest == in_bin && p != 0x80000000u;      // +0 edge: -0 would tie it
+    need[i] = settled ? 0u : rest;
+    if (!settled && busy_out) busy_out[u] = 1u;       // every writer stores the same value
 }
 
 // One block of the count pass: a ballot per value (bit = lane = row), whose
@@ -282,7 +320,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
     for (int rb = 0; rb < NRB; ++rb) {
         const int row = wave * 64 + rb * M::BM + lane % M::BM;
         pos[rb] = row < R ? N - W + row % W : -1;
-        thr[rb] = row < R ? key_value(pre[u * R + row]) : INFINITY;
+        thr[rb] = row < R ? threshold_value(pre[u * R + row]) : INFINITY;
     }
     TC<T, D> zero[NRB];
 #pragma unroll
@@ -332,22 +370,27 @@ static void launch_topshare(hipStream_t s, const ScorePlan &p, int B, int L, int
     uint32_t *pre = reinterpret_cast<uint32_t *>(ws);
     uint32_t *need = pre + nrows;
     uint32_t *gh = need + nrows;
+    uint32_t *busy = gh + nrows * TS_MAXBINS;               // [TS_MAXPASS][units]
     const T *q = reinterpret_cast<const T *>(q_win);
     const T *kk = reinterpret_cast<const T *>(k);
     const dim3 rgrid((unsigned)ceil_div(nrows, 256));
     const dim3 grid((unsigned)(units * p.nchunk));
-    ts_init_kernel<<<rgrid, 256, 0, s>>>(nrows, R, W, B, Hkv, cu_seqlens, ntok, ratio_bp, pre, need, gh, NB);
-    for (int hi = 32; hi > 0;) {
+    static_assert((32 + DB - 1) / DB <= TS_MAXPASS, "flag words");
+    ts_init_kernel<<<rgrid, 256, 0, s>>>(nrows, R, W, B, Hkv, cu_seqlens, ntok, ratio_bp, pre, need, gh, NB, busy,
+                                         units);
+    for (int pass = 0, hi = 32; hi > 0; ++pass) {
         const int sh = std::max(0, hi - DB), width = hi - sh;
-        if (hi == 32)
+        const uint32_t *busy_in = pass > 0 ? busy + (pass - 1) * units : nullptr;
+        uint32_t *busy_out = sh > 0 ? busy + pass * units : nullptr;
+        if (pass == 0)
             ts_hist_kernel<T, D, NW, true><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
                                                                   k_layer_rows, p.nchunk, p.chunk_keys, sh, width,
-                                                                  pre, gh);
+                                                                  busy_in, pre, gh);
         else
             ts_hist_kernel<T, D, NW, false><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
                                                                    k_layer_rows, p.nchunk, p.chunk_keys, sh, width,
-                                                                   pre, gh);
-        ts_digit_kernel<<<rgrid, 256, 0, s>>>(nrows, R, NB, sh, width, pre, need, gh);
+                                                                   busy_in, pre, gh);
+        ts_digit_kernel<<<rgrid, 256, 0, s>>>(nrows, R, NB, sh, width, busy_in, busy_out, pre, need, gh);
         hi = sh;
     }
     ts_count_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk, k_layer_rows,
@@ -374,8 +417,8 @@ using namespace sg;
 
 extern "C" size_t sg_score_topshare_workspace_size(int B, int L, int Hq, int Hkv, int d, int W, int max_seqlen) {
     if (B <= 0 || L <= 0 || Hkv <= 0 || Hq <= 0 || W <= 0 || max_seqlen <= 0 || d <= 0) return 0;
-    const int64_t rows = (int64_t)L * Hkv * B * (Hq / Hkv) * W;
-    return (size_t)(rows * (2 + TS_MAXBINS)) * sizeof(uint32_t);
+    const int64_t units = (int64_t)L * Hkv * B, rows = units * (Hq / Hkv) * W;
+    return (size_t)(rows * (2 + TS_MAXBINS) + units * TS_MAXPASS) * sizeof(uint32_t);
 }
 
 extern "C" int sg_score_topshare(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,
