@@ -1129,10 +1129,10 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     return {"alpha": alpha, "count_score": {"ms": r4(t_count), "tflops": round(score_flops / (t_count * 1e-3) / 1e12, 1),
                                             "frac_mfma_peak": r4(score_flops / (t_count * 1e-3) / 1e12
                                                                  / BF16_MFMA_PEAK_TFLOPS)},
-            "topshare_score": {"ratio_bp": cap_bp, "ms": r4(t_ts), "logit_passes": ts_passes,
-                               "tflops_all_passes": round(ts_passes * score_flops / (t_ts * 1e-3) / 1e12, 1),
-                               "frac_mfma_peak_all_passes": r4(ts_passes * score_flops / (t_ts * 1e-3) / 1e12
-                                                               / BF16_MFMA_PEAK_TFLOPS)},
+            "topshare_score": {"ratio_bp": cap_bp, "ms": r4(t_ts), "logit_passes_at_most": ts_passes,
+                               "tflops_one_contraction": round(score_flops / (t_ts * 1e-3) / 1e12, 1),
+                               "note": "each histogram pass recomputes the logits; a unit whose rows have "
+                                       "all settled skips its remaining passes"},
             "decode_select": {"ms": r4(t_sel), "cap": cap, "k_read_gbs": round(gbs(k_bytes, t_sel), 1),
                               "frac_hbm_peak": r4(gbs(k_bytes, t_sel) / HBM_PEAK_GBS),
                               "selected_fraction": r4(np.mean(sel_frac))},
