@@ -25,7 +25,12 @@
 //           the keys above the bin, and the bins are cleared for the next
 //           pass.
 //
-// After 32 bits the prefix is the key of the row's k-th largest value.  A row
+// After 32 bits the prefix is the key of the row's k-th largest value.  Long
+// before that a row's bin holds only a few keys: once 18 bits are resolved,
+// a row whose bin holds at most TS_CMAX keys gathers them (one more logit
+// pass: each such value is appended to its row's list, in LDS, then in the
+// workspace) and a small kernel picks the exact k-th largest among them.
+// Rows with larger bins (many ties) keep the radix passes.  A row
 // settles earlier when its chosen bin holds exactly the keys it still needs:
 // then every key at or above the bin's lower edge is picked and nothing below
 // it.  Once every row of a unit has settled, the unit's remaining passes
@@ -50,6 +55,9 @@ namespace sg {
 
 constexpr int TS_MAXBINS = 64;     // bins per row of the global histogram (digits of at most 6 bits)
 constexpr int TS_MAXPASS = 8;      // per-unit flag words per call (7 passes at most)
+constexpr int TS_CMAX = 32;        // keys a row may gather
+constexpr int TS_GATHER_BITS = 18; // resolved bits before a row may gather
+constexpr uint32_t TS_GATHER = 0x80000000u;   // need flag: the row gathers its bin
 
 // Digit width: 6 bits (6 passes) while the bins of up to 256 rows fit in
 // LDS beside the two K tiles; 5 bits (7 passes) for 512 rows.
@@ -183,7 +191,8 @@ __global__ __launch_bounds__(256) void ts_init_kernel(int64_t nrows, int R, int 
                                                       const int32_t *__restrict__ cu_seqlens, int64_t T_,
                                                       int ratio_bp, uint32_t *__restrict__ pre,
                                                       uint32_t *__restrict__ need, uint32_t *__restrict__ ghist,
-                                                      int nb, uint32_t *__restrict__ busy, int64_t units) {
+                                                      int nb, uint32_t *__restrict__ busy, int64_t units,
+                                                      uint32_t *__restrict__ gcount, uint32_t *__restrict__ gflag) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= nrows) return;
     const int64_t u = i / R;
@@ -195,8 +204,11 @@ __global__ __launch_bounds__(256) void ts_init_kernel(int64_t nrows, int R, int 
     need[i] = (uint32_t)kk;
     uint32_t *h = ghist + u * nb * (int64_t)R + r;
     for (int b = 0; b < nb; ++b) h[(int64_t)b * R] = 0u;
-    if (r == 0)
+    gcount[i] = 0u;
+    if (r == 0) {
         for (int k = 0; k < TS_MAXPASS; ++k) busy[k * units + u] = 0u;
+        gflag[u] = 0u;
+    }
 }
 
 // One thread per (unit, row): pick this pass's digit of the threshold key.
@@ -205,10 +217,14 @@ __global__ __launch_bounds__(256) void ts_init_kernel(int64_t nrows, int R, int 
 // marks a settled row (its bins are only cleared).  busy_in: the flags the
 // previous pass set (a unit without one did not run this pass); busy_out: set
 // for the unit of every row that has not settled (NULL after the last digit).
+// gflag (the digit after which rows may gather, else NULL): a row whose bin
+// holds at most TS_CMAX keys is flagged to gather them (need | TS_GATHER) and
+// sets gflag of its unit instead of busy_out.
 __global__ __launch_bounds__(256) void ts_digit_kernel(int64_t nrows, int R, int nb, int sh, int width,
                                                        const uint32_t *__restrict__ busy_in,
                                                        uint32_t *__restrict__ busy_out, uint32_t *__restrict__ pre,
-                                                       uint32_t *__restrict__ need, uint32_t *__restrict__ ghist) {
+                                                       uint32_t *__restrict__ need, uint32_t *__restrict__ ghist,
+                                                       uint32_t *__restrict__ gflag) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= nrows) return;
     const int64_t u = i / R;
@@ -240,8 +256,174 @@ __global__ __launch_bounds__(256) void ts_digit_kernel(int64_t nrows, int R, int
     const uint32_t p = pre[i] | (digit << sh);
     pre[i] = p;
     const bool settled = rest == in_bin && p != 0x80000000u;      // +0 edge: -0 would tie it
-    need[i] = settled ? 0u : rest;
-    if (!settled && busy_out) busy_out[u] = 1u;       // every writer stores the same value
+    const bool gather = !settled && gflag && in_bin <= (uint32_t)TS_CMAX;
+    need[i] = settled ? 0u : gather ? (rest | TS_GATHER) : rest;
+    // every writer of a flag stores the same value
+    if (gather) gflag[u] = 1u;
+    else if (!settled && busy_out) busy_out[u] = 1u;
+}
+
+// One block of the gather pass: the values of gathering rows whose key
+// matches the row's prefix (all bits above sh) are appended to the row's list
+// in LDS.  A value matches when (bits ^ c) < lim, where lim is 2^sh for a
+// gathering row and 0 otherwise: one compare per value, whose wavefront mask
+// (one bit per lane) is kept.  Matches are rare (a few per row over the whole
+// prompt), so they are handled behind one wavefront-uniform test per block.
+// The lanes holding one row (lane % BM) keep the row's count in step: a
+// value's mask gives every lane its slot (the count plus the set bits of its
+// row's lanes below it) and the count's increase, so no atomics are needed.
+template <typename T, int D, int NW, bool MASK>
+struct GatherStep {
+    static constexpr int NRB = QFrags<T, D>::NRB;
+    uint32_t *lcand;                // LDS [64 * NW][TS_CMAX]
+    uint32_t (&cnt)[NRB];           // values gathered so far for the lane's row
+    const uint32_t (&c)[NRB];       // as in HistStep
+    const uint32_t (&lim)[NRB];
+    const int (&pos)[NRB];
+    uint64_t rowmask, below;        // the lanes of the lane's row; those of them below the lane
+    int lane, wave, key0;
+    __device__ __forceinline__ void operator()(TC<T, D> &acc, int kb, int rb) const {
+        using M = MT<T, D>;
+        uint64_t m[M::NV], any = 0u;
+#pragma unroll
+        for (int v = 0; v < M::NV; ++v) {
+            bool h = (__float_as_uint(acc[v]) ^ c[rb]) < lim[rb];
+            if (MASK) h = h && key0 + kb * M::BM + M::crow(v, lane) <= pos[rb];
+            m[v] = __ballot(h);
+            any |= m[v];
+        }
+        if (__builtin_expect(any != 0u, 0)) {
+            const int row = wave * 64 + rb * M::BM + lane % M::BM;
+#pragma unroll
+            for (int v = 0; v < M::NV; ++v) {
+                if (m[v] == 0u) continue;           // wavefront-uniform
+                const uint32_t slot = cnt[rb] + (uint32_t)__popcll(m[v] & below);
+                if (((m[v] >> lane) & 1u) && slot < (uint32_t)TS_CMAX)
+                    lcand[row * TS_CMAX + slot] = __float_as_uint(acc[v]);
+                cnt[rb] += (uint32_t)__popcll(m[v] & rowmask);
+            }
+        }
+    }
+};
+
+template <typename T, int D, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void ts_gather_kernel(
+    int B, int L, int Hq, int Hkv, int W, const int32_t *__restrict__ cu_seqlens, int64_t T_,
+    const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, int nchunk, int chunk_keys,
+    int sh, const uint32_t *__restrict__ gflag, const uint32_t *__restrict__ pre, const uint32_t *__restrict__ need,
+    uint32_t *__restrict__ gcount, uint32_t *__restrict__ gcand) {
+    using M = MT<T, D>;
+    using KT = KTile<T, D>;
+    constexpr int NRB = QFrags<T, D>::NRB, ROWS = 64 * NW;
+    __shared__ __attribute__((aligned(16))) char kbA[KT::BYTES];
+    __shared__ __attribute__((aligned(16))) char kbB[KT::BYTES];
+    __shared__ uint32_t lcand[ROWS * TS_CMAX];
+    int64_t u;
+    int chunk;
+    unit_chunk((int64_t)L * Hkv * B, nchunk, u, chunk);
+    if (gflag[u] == 0u) return;                 // no row of the unit gathers
+    const UnitGeom g = unit_geom(u, B, Hkv, cu_seqlens, T_);
+    const int G = Hq / Hkv, R = G * W;
+    const int N = (int)g.N;
+    const int key_begin = chunk * chunk_keys;
+    if (N < W || key_begin >= N) return;
+    const int lane = threadIdx.x % 64;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    const T *qunit = q_win + (((int64_t)g.b * L + g.l) * Hq + (int64_t)g.h * G) * W * D;
+    const T *kunit = k + ((int64_t)g.l * k_layer_rows + (int64_t)g.h * T_ + g.s0) * D;
+    const int key_end = min(N, key_begin + chunk_keys);
+    const int ntile = (int)ceil_div(key_end - key_begin, KT::TK);
+    KT::template load<NW>(kbA, kunit, key_begin, N, wave, lane);
+    QFrags<T, D> q;
+    q.load(qunit, R, wave, lane);
+    uint32_t c[NRB], cnt[NRB], lim[NRB];
+    int pos[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+        const int row = wave * 64 + rb * M::BM + lane % M::BM;
+        pos[rb] = row < R ? N - W + row % W : -1;
+        const uint32_t p = row < R ? pre[u * R + row] : 0u;
+        const bool on = row < R && (need[u * R + row] & TS_GATHER) != 0u;
+        lim[rb] = on ? 1u << sh : 0u;
+        c[rb] = p ^ ((p & 0x80000000u) ? 0x80000000u : 0xffffffffu);
+        cnt[rb] = 0u;
+    }
+    // lanes holding the same row: lane % BM, one per lane group
+    uint64_t rowmask = 0u;
+#pragma unroll
+    for (int gi = 0; gi < 64 / M::BM; ++gi) rowmask |= 1ull << (gi * M::BM + lane % M::BM);
+    const uint64_t below = rowmask & ((1ull << lane) - 1u);
+    TC<T, D> zero[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) zero[rb] = M::zero();
+    auto step = [&](int t, char *cur, char *nxt, auto mask) {
+        constexpr bool MASK = decltype(mask)::value;
+        barrier_after_loads();      // tile t landed; tile t - 1 done everywhere
+        const int key0 = key_begin + t * KT::TK;
+        if (t + 1 < ntile) KT::template load<NW>(nxt, kunit, key0 + KT::TK, N, wave, lane);
+        const GatherStep<T, D, NW, MASK> f{lcand, cnt, c, lim, pos, rowmask, below, lane, wave, key0};
+        if (MASK) tile_sweep_plain<T, D, true>(cur, q, zero, lane, f);
+        else tile_sweep<T, D, true>(cur, q, zero, lane, f);
+    };
+    const int nfull = full_tiles(key_begin, ntile, KT::TK, N, W);
+    int t = 0;
+    for (; t + 1 < nfull; t += 2) {
+        step(t, kbA, kbB, std::false_type{});
+        step(t + 1, kbB, kbA, std::false_type{});
+    }
+    for (; t < ntile; ++t) {
+        if (t & 1) step(t, kbB, kbA, std::true_type{});
+        else step(t, kbA, kbB, std::true_type{});
+    }
+    barrier_after_loads();      // every list final, no load in flight
+    // the chunk's values go after those of the unit's other chunks (their order
+    // does not matter: the pick below ranks them); the first lane group of each
+    // row block writes its rows' lists
+    if (lane < M::BM) {
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+            const int row = wave * 64 + rb * M::BM + lane;
+            const uint32_t n = min(cnt[rb], (uint32_t)TS_CMAX);
+            if (row >= R || n == 0u) continue;
+            const int64_t i = u * R + row;
+            const uint32_t base = __hip_atomic_fetch_add(gcount + i, n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (uint32_t j = 0; j < n && base + j < (uint32_t)TS_CMAX; ++j)
+                gcand[i * TS_CMAX + base + j] = lcand[row * TS_CMAX + j];
+        }
+    }
+}
+
+// One thread per gathering row: the exact key of rank `need` (from the top)
+// among the gathered values; the row then settles on it.  The values wait in
+// LDS, so the loops run over the row's own count.
+__global__ __launch_bounds__(256) void ts_pick_kernel(int64_t nrows, const uint32_t *__restrict__ gcount,
+                                                      const uint32_t *__restrict__ gcand, uint32_t *__restrict__ pre,
+                                                      uint32_t *__restrict__ need) {
+    __shared__ uint32_t keys[TS_CMAX][256];
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= nrows) return;
+    const uint32_t nd = need[i];
+    if ((nd & TS_GATHER) == 0u) return;
+    const uint32_t rank = nd & ~TS_GATHER;
+    const int n = (int)min(gcount[i], (uint32_t)TS_CMAX);
+    uint32_t *kk = &keys[0][threadIdx.x];             // this thread's column: entries 256 words apart
+    for (int a = 0; a < n; ++a) {
+        const uint32_t x = gcand[i * TS_CMAX + a];
+        kk[a * 256] = x ^ ((uint32_t)((int32_t)x >> 31) | 0x80000000u);
+    }
+    uint32_t best = pre[i];          // kept only if the values disagreed with the counts
+    for (int a = 0; a < n; ++a) {
+        const uint32_t ka = kk[a * 256];
+        uint32_t above = 0u, atleast = 0u;
+        for (int b = 0; b < n; ++b) {
+            const uint32_t kb = kk[b * 256];
+            above += kb > ka ? 1u : 0u;
+            atleast += kb >= ka ? 1u : 0u;
+        }
+        if (above < rank && rank <= atleast) best = ka;
+    }
+    pre[i] = best;
+    need[i] = 0u;
 }
 
 // One block of the count pass: a ballot per value (bit = lane = row), whose
@@ -371,13 +553,16 @@ static void launch_topshare(hipStream_t s, const ScorePlan &p, int B, int L, int
     uint32_t *need = pre + nrows;
     uint32_t *gh = need + nrows;
     uint32_t *busy = gh + nrows * TS_MAXBINS;               // [TS_MAXPASS][units]
+    uint32_t *gflag = busy + TS_MAXPASS * units;            // [units]
+    uint32_t *gcount = gflag + units;                       // [rows]
+    uint32_t *gcand = gcount + nrows;                       // [rows][TS_CMAX]
     const T *q = reinterpret_cast<const T *>(q_win);
     const T *kk = reinterpret_cast<const T *>(k);
     const dim3 rgrid((unsigned)ceil_div(nrows, 256));
     const dim3 grid((unsigned)(units * p.nchunk));
     static_assert((32 + DB - 1) / DB <= TS_MAXPASS, "flag words");
     ts_init_kernel<<<rgrid, 256, 0, s>>>(nrows, R, W, B, Hkv, cu_seqlens, ntok, ratio_bp, pre, need, gh, NB, busy,
-                                         units);
+                                         units, gcount, gflag);
     for (int pass = 0, hi = 32; hi > 0; ++pass) {
         const int sh = std::max(0, hi - DB), width = hi - sh;
         const uint32_t *busy_in = pass > 0 ? busy + (pass - 1) * units : nullptr;
@@ -390,7 +575,15 @@ static void launch_topshare(hipStream_t s, const ScorePlan &p, int B, int L, int
             ts_hist_kernel<T, D, NW, false><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
                                                                    k_layer_rows, p.nchunk, p.chunk_keys, sh, width,
                                                                    busy_in, pre, gh);
-        ts_digit_kernel<<<rgrid, 256, 0, s>>>(nrows, R, NB, sh, width, busy_in, busy_out, pre, need, gh);
+        const bool gather = 32 - sh >= TS_GATHER_BITS && 32 - hi < TS_GATHER_BITS;   // first digit past 18 bits
+        ts_digit_kernel<<<rgrid, 256, 0, s>>>(nrows, R, NB, sh, width, busy_in, busy_out, pre, need, gh,
+                                              gather ? gflag : nullptr);
+        if (gather) {
+            ts_gather_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk,
+                                                               k_layer_rows, p.nchunk, p.chunk_keys, sh, gflag, pre,
+                                                               need, gcount, gcand);
+            ts_pick_kernel<<<rgrid, 256, 0, s>>>(nrows, gcount, gcand, pre, need);
+        }
         hi = sh;
     }
     ts_count_kernel<T, D, NW><<<grid, 64 * NW, 0, s>>>(B, L, Hq, Hkv, W, cu_seqlens, ntok, q, kk, k_layer_rows,
@@ -418,7 +611,7 @@ using namespace sg;
 extern "C" size_t sg_score_topshare_workspace_size(int B, int L, int Hq, int Hkv, int d, int W, int max_seqlen) {
     if (B <= 0 || L <= 0 || Hkv <= 0 || Hq <= 0 || W <= 0 || max_seqlen <= 0 || d <= 0) return 0;
     const int64_t units = (int64_t)L * Hkv * B, rows = units * (Hq / Hkv) * W;
-    return (size_t)(rows * (2 + TS_MAXBINS) + units * TS_MAXPASS) * sizeof(uint32_t);
+    return (size_t)(rows * (3 + TS_MAXBINS + TS_CMAX) + units * (TS_MAXPASS + 1)) * sizeof(uint32_t);
 }
 
 extern "C" int sg_score_topshare(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int d, int W,

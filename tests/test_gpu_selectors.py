@@ -221,6 +221,24 @@ def test_score_topshare_exact(gpu_lib, dtype, G, W, d, lens, bp, span):
     assert got.min() >= 0 and got.max() <= G * W
 
 
+def test_score_topshare_mixed_rows(gpu_lib):
+    """One unit whose rows take both ways to their threshold: keys in {-1, 0, 1};
+    window rows w < 32 with queries in [-40, 40] see a few keys per logit value
+    (their last bins are gathered and ranked), rows w >= 32 with queries in
+    {-1, 0, 1} see dozens of keys tied at every value (their bins stay too large
+    to gather and the radix passes go on).  Integer logits: exact."""
+    G, W, d, L, Hkv, lens = 4, 64, 64, 2, 2, (3000, 2100)
+    say("score topshare mixed rows", lens)
+    T = sum(lens)
+    q = _ints((len(lens), L, Hkv * G, W, d), -40, 40, 81, "bf16")
+    q[..., 32:, :] = _ints((len(lens), L, Hkv * G, W - 32, d), -1, 1, 82, "bf16")
+    k = _ints((L, Hkv, T, d), -1, 1, 83, "bf16")
+    for bp in (2000, 500):
+        got, cus = _topshare(gpu_lib, q, k, lens, Hkv, bp)
+        ref = oracle.score_topshare(q.float().numpy(), k.float().numpy(), cus, Hkv, bp)
+        np.testing.assert_array_equal(got, ref.astype(np.float32))
+
+
 def test_score_topshare_all_keys_closed_form(gpu_lib):
     """ratio 100%: each row picks every key it sees, so key j's count is G times
     the number of window rows at or after it, whatever the values."""
