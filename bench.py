@@ -1075,7 +1075,11 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     t_ts = median_ms(lambda i: sg.sg_score_topshare(pre["q_win"], pre["k"], cus, T, N, Hkv, ts_counts, cap_bp, ws_ts))
     idx_ts = torch.empty_like(idx_score)
     sg.sg_topk(ts_counts, cus, T, N, cuk, K_total, idx_ts)
-    ts_passes = 1 + (6 if cfg.G * W <= 256 else 7)       # one logit recompute per digit, then the count pass
+    # logit passes: one per digit (6 bits, 5 above 256 rows) until 18 bits, the
+    # gather, the count; rows with large bins (ties) take the remaining digits
+    db = 6 if cfg.G * W <= 256 else 5
+    ts_gather_after = -(-18 // db)
+    ts_passes = {"when_every_row_gathers": ts_gather_after + 2, "at_most": -(-32 // db) + 2}
     cap = N * cap_bp // 10000
     cu_cap = torch.tensor([0, cap], dtype=torch.int32, device=dev)
     ws_sel = torch.empty(sg.decode_select_workspace_size(1, L, Hq, N), dtype=torch.uint8, device=dev)
@@ -1129,10 +1133,10 @@ def selectors(sg, cfg, pre, cus, cuk, T, N, K_total, idx_score, nsteps=8, alpha=
     return {"alpha": alpha, "count_score": {"ms": r4(t_count), "tflops": round(score_flops / (t_count * 1e-3) / 1e12, 1),
                                             "frac_mfma_peak": r4(score_flops / (t_count * 1e-3) / 1e12
                                                                  / BF16_MFMA_PEAK_TFLOPS)},
-            "topshare_score": {"ratio_bp": cap_bp, "ms": r4(t_ts), "logit_passes_at_most": ts_passes,
+            "topshare_score": {"ratio_bp": cap_bp, "ms": r4(t_ts), "logit_passes": ts_passes,
                                "tflops_one_contraction": round(score_flops / (t_ts * 1e-3) / 1e12, 1),
-                               "note": "each histogram pass recomputes the logits; a unit whose rows have "
-                                       "all settled skips its remaining passes"},
+                               "note": "each pass recomputes the logits; a unit with no row left to resolve "
+                                       "returns at the start of the remaining radix passes"},
             "decode_select": {"ms": r4(t_sel), "cap": cap, "k_read_gbs": round(gbs(k_bytes, t_sel), 1),
                               "frac_hbm_peak": r4(gbs(k_bytes, t_sel) / HBM_PEAK_GBS),
                               "selected_fraction": r4(np.mean(sel_frac))},
