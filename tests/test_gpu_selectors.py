@@ -239,6 +239,24 @@ def test_score_topshare_mixed_rows(gpu_lib):
         np.testing.assert_array_equal(got, ref.astype(np.float32))
 
 
+def test_score_topshare_shared_layer_source(gpu_lib):
+    """One K source read by every layer (k_layer_rows = 0, as the batched
+    workload stores it), three requests; integer inputs: exact."""
+    G, W, d, L, Hkv, lens = 2, 32, 64, 3, 2, (900, 2300, 32)
+    say("score topshare shared layer source", lens)
+    T = sum(lens)
+    q = _ints((len(lens), L, Hkv * G, W, d), -40, 40, 91, "bf16")
+    k = _ints((1, Hkv, T, d), -40, 40, 92, "bf16")
+    cus = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    ws = torch.empty(gpu_lib.score_topshare_workspace_size(len(lens), L, Hkv * G, Hkv, d, W, max(lens)),
+                     dtype=torch.uint8, device="cuda")
+    out = torch.full((L, Hkv, T), -1.0, device="cuda")
+    gpu_lib.sg_score_topshare(q.cuda(), k.cuda(), cu(cus), T, max(lens), Hkv, out, 2000, ws, k_layer_rows=0)
+    torch.cuda.synchronize()
+    ref = oracle.score_topshare(q.float().numpy(), k.float().numpy(), cus, Hkv, 2000, k_layer_rows=0)
+    np.testing.assert_array_equal(out.cpu().numpy(), ref.astype(np.float32))
+
+
 def test_score_topshare_all_keys_closed_form(gpu_lib):
     """ratio 100%: each row picks every key it sees, so key j's count is G times
     the number of window rows at or after it, whatever the values."""
