@@ -156,14 +156,15 @@ int sg_score_count(void *stream, sg_dtype dt, int B, int L, int Hq, int Hkv, int
  *   counts[l][h][s0 + j] = number of (q head, window row) pairs with z_j >= t_w
  *
  * so a row picks its k_w largest logits and every key tied with the k_w-th
- * (the threshold is exact: a radix select over the fp32 logits; the decisions
- * are taken in fp32 on the raw products q . k_j, whose order the positive
- * scale keeps; -0 equals +0).  Counts are integers in [0, G * W] stored as
- * float, as in sg_score_count.
+ * (the threshold is exact: a radix select over the fp32 logits, finished by
+ * ranking the few values left in a row's last bin; the decisions are taken in
+ * fp32 on the raw products q . k_j, whose order the positive scale keeps; -0
+ * equals +0).  Counts are integers in [0, G * W] stored as float, as in
+ * sg_score_count.
  *   ratio_bp  the share in basis points, 1 .. 10000 (2000 = 20%).
  *   ws        device workspace of at least sg_score_topshare_workspace_size
- *             bytes (16-byte aligned): per-row thresholds and histograms;
- *             its contents need no initialisation.
+ *             bytes (16-byte aligned): per-row thresholds, histograms and
+ *             gathered values; its contents need no initialisation.
  * Arguments and layout as sg_score (lse_in does not apply); max_seqlen must be
  * at least every N_b.  A request with N_b < W gets all-zero counts.
  * Calls that share a workspace must be ordered (same stream, or an event).
