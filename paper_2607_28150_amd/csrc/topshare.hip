@@ -25,20 +25,22 @@
 //           the keys above the bin, and the bins are cleared for the next
 //           pass.
 //
-// After 32 bits the prefix is the key of the row's k-th largest value.  Long
-// before that a row's bin holds only a few keys: once 18 bits are resolved,
-// a row whose bin holds at most TS_CMAX keys gathers them (one more logit
-// pass: each such value is appended to its row's list, in LDS, then in the
-// workspace) and a small kernel picks the exact k-th largest among them.
-// Rows with larger bins (many ties) keep the radix passes.  A row
-// settles earlier when its chosen bin holds exactly the keys it still needs:
-// then every key at or above the bin's lower edge is picked and nothing below
-// it.  Once every row of a unit has settled, the unit's remaining passes
-// return at once (real-valued logits settle after about 30 bits).  The count
-// pass recomputes the logits in the same layout, so each row compares exactly
-// the values its threshold came from (the same MFMA operands in the same
-// order), and counts each key's picks with one wavefront ballot per value (one
-// bit per row) and population counts.
+// After 32 bits the prefix is the key of the row's k-th largest value.  Two
+// shortcuts end most rows much earlier:
+//   settle : a row whose chosen bin holds exactly the keys it still needs is
+//            done (every key at or above the bin's lower edge is picked and
+//            nothing below it);
+//   gather : once 18 bits are resolved a row's bin holds only a few keys
+//            (with real-valued logits); a row whose bin holds at most TS_CMAX
+//            keys gathers their values (one more logit pass appends each to
+//            the row's list, in LDS, then in the workspace) and a small kernel
+//            picks the exact k-th largest among them.  Rows with larger bins
+//            (many ties) keep the radix passes.
+// A unit with no row left to resolve returns at the start of the remaining
+// passes.  The count pass recomputes the logits in the same layout, so each
+// row compares exactly the values its threshold came from (the same MFMA
+// operands in the same order), and counts each key's picks with one wavefront
+// ballot per value (one bit per row) and population counts.
 //
 // The passes work on the raw products q . k_j: the positive scale 1/sqrt(d)
 // keeps their order.  The picks compare floats against the threshold: the
@@ -59,8 +61,8 @@ constexpr int TS_CMAX = 32;        // keys a row may gather
 constexpr int TS_GATHER_BITS = 18; // resolved bits before a row may gather
 constexpr uint32_t TS_GATHER = 0x80000000u;   // need flag: the row gathers its bin
 
-// Digit width: 6 bits (6 passes) while the bins of up to 256 rows fit in
-// LDS beside the two K tiles; 5 bits (7 passes) for 512 rows.
+// Digit width: 6 bits (at most 6 histogram passes) while the bins of up to
+// 256 rows fit in LDS beside the two K tiles; 5 bits (at most 7) for 512 rows.
 template <int NW>
 struct TsDigits {
     static constexpr int DB = NW == 8 ? 5 : 6;
