@@ -70,7 +70,7 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
 def build_host_sanitized(out_path: str, jobs: int = 8) -> str:
     """The library with its host code (argument checks, dispatch) built with
     AddressSanitizer and UndefinedBehaviorSanitizer (device code unoptimised:
-    this build is for CPU-only checks of the host side).  Load it with the
+    the sanitized library is for CPU-only checks of the host side).  Load it with the
     clang ASan runtime preloaded."""
     srcs = sorted(glob.glob(os.path.join(_HERE, "csrc", "*.hip")))
     bdir = os.path.join(os.path.dirname(os.path.abspath(out_path)), "objs")
