@@ -103,6 +103,12 @@ __device__ __forceinline__ UnitGeom unit_geom(int64_t u, int B, int Hkv, const i
     return g;
 }
 
+// Direct global->LDS load as dma16, addressed by a wavefront-uniform base in
+// scalar registers and a 32-bit per-lane offset.
+__device__ __forceinline__ void dma16_sbase(const char *base, unsigned off, unsigned lds) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
+}
+
 // K tiles in LDS.  A tile is TK keys of D elements, stored without padding;
 // the 16-byte vector v of key j sits at slot j * VPR + (v ^ (j % VPR)), so the
 // 32 (or 16) lanes reading one fragment column hit distinct banks.  Tiles
@@ -128,6 +134,32 @@ struct KTile {
         asm volatile("" : "+v"(lane));
         const unsigned kl = (unsigned)lane / VPR, vl = (unsigned)lane % VPR;
         const char *tb = reinterpret_cast<const char *>(kunit) + (int64_t)key0 * (VPR * 16);   // wavefront-uniform
+        if constexpr (sizeof(T) == 2) {
+            // A whole bf16 tile: every wavefront's first key is a multiple of VPR
+            // and the swizzle repeats every PER instructions, so the lane's 32-bit
+            // offsets of PER instructions serve them all, each instruction taking
+            // a wavefront-uniform base in scalar registers (no 64-bit address
+            // arithmetic per lane and instruction).
+            static_assert(KPW % VPR == 0 && (VPR % KPI == 0 || KPI % VPR == 0), "swizzle period");
+            constexpr int NI = KPW / KPI, PER0 = VPR % KPI == 0 ? VPR / KPI : 1, PER = PER0 < NI ? PER0 : NI;
+            if (key0 + TK <= N) {
+                unsigned off[PER];
+#pragma unroll
+                for (int p = 0; p < PER; ++p)
+                    off[p] = (p * KPI + kl) * (VPR * 16) + ((vl ^ ((p * KPI + kl) % VPR)) << 4);
+                // the base is uniform by construction; readfirstlane puts it in the
+                // scalar registers the instruction form requires
+                const uint64_t b0 = reinterpret_cast<uint64_t>(tb + (int64_t)wave * KPW * (VPR * 16));
+                const uint64_t sb = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b0 >> 32)) << 32) |
+                                    (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b0);
+#pragma unroll
+                for (int j = 0; j < NI; ++j) {
+                    const char *base = reinterpret_cast<const char *>(sb + (uint64_t)((j / PER) * PER * KPI * VPR * 16));
+                    dma16_sbase(base, off[j % PER], lds_addr(buf + (wave * KPW + j * KPI) * VPR * 16));
+                }
+                return;
+            }
+        }
         // the last key of the prompt relative to key0: keys past it read it instead
         const unsigned last = (unsigned)max(0, min(TK - 1, N - 1 - key0));
         const bool whole = key0 + TK <= N;
