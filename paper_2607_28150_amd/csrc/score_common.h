@@ -104,7 +104,15 @@ __device__ __forceinline__ UnitGeom unit_geom(int64_t u, int B, int Hkv, const i
 }
 
 // Direct global->LDS load as dma16, addressed by a wavefront-uniform base in
-// scalar registers and a 32-bit per-lane offset.
+// scalar registers and a 32-bit per-lane offset.  The base reaches the
+// instruction in scalar registers only in an optimising compile (readfirstlane
+// results stay scalar there); an unoptimised device compile (the sanitised
+// library for host-side checks) keeps the 64-bit form.
+#if defined(__OPTIMIZE__)
+constexpr bool SC_SCALAR_BASE = true;
+#else
+constexpr bool SC_SCALAR_BASE = false;
+#endif
 __device__ __forceinline__ void dma16_sbase(const char *base, unsigned off, unsigned lds) {
     asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
 }
@@ -134,7 +142,7 @@ struct KTile {
         asm volatile("" : "+v"(lane));
         const unsigned kl = (unsigned)lane / VPR, vl = (unsigned)lane % VPR;
         const char *tb = reinterpret_cast<const char *>(kunit) + (int64_t)key0 * (VPR * 16);   // wavefront-uniform
-        if constexpr (sizeof(T) == 2) {
+        if constexpr (sizeof(T) == 2 && SC_SCALAR_BASE) {
             // A whole bf16 tile: every wavefront's first key is a multiple of VPR
             // and the swizzle repeats every PER instructions, so the lane's 32-bit
             // offsets of PER instructions serve them all, each instruction taking
