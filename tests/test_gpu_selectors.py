@@ -206,6 +206,8 @@ def _topshare(gpu_lib, q, k, lens, Hkv, ratio_bp, ws=None):
     ("f32", 8, 16, 64, (1300,), 5000, 40),           # 128 rows
     ("bf16", 4, 20, 64, (2222, 999), 333, 3),        # 80 rows: padded wavefront rows
     ("f32", 2, 8, 128, (777, 130), 2000, 3),         # a single wavefront, short prompts
+    ("f32", 8, 64, 128, (700,), 2000, 40),           # fp32 at 512 rows (8 wavefronts, 5-bit digits)
+    ("f32", 8, 64, 64, (1100, 64), 1500, 3),
 ])
 def test_score_topshare_exact(gpu_lib, dtype, G, W, d, lens, bp, span):
     """Integer inputs: every logit is exact in fp32 and fp64, so the thresholds,
