@@ -176,3 +176,21 @@ def test_selector_host_checks(lib):
     assert rc == smartgen.SG_EINVAL and "scale" in _err(lib)
     rc = lib.sg_decode_select(None, 1, 1, 1, 32, 8, 128, P, P, 100, 100, P, 0, 0.0, 5.0, P, 10, P, P, P, 64)
     assert rc == smartgen.SG_EWORKSPACE
+
+
+def test_topshare_host_checks(lib):
+    # rows x (prefix, rank, gathered count, 64 bins, 32 gathered values) + units x (8 pass flags, gather flag)
+    rows, units = 1 * 32 * 8 * 4 * 64, 1 * 32 * 8
+    assert smartgen.score_topshare_workspace_size(1, 32, 32, 8, 128, 64, 8192) == (rows * 99 + units * 9) * 4
+    assert smartgen.score_topshare_workspace_size(0, 32, 32, 8, 128, 64, 8192) == 0
+    for bp in (0, 10001, -5):
+        rc = lib.sg_score_topshare(None, 1, 1, 1, 8, 8, 64, 32, P, 100, 100, P, P, 0, bp, P, P, 1 << 20)
+        assert rc == smartgen.SG_EINVAL and "ratio_bp" in _err(lib)
+    rc = lib.sg_score_topshare(None, 1, 1, 1, 8, 8, 96, 32, P, 100, 100, P, P, 0, 2000, P, P, 1 << 20)
+    assert rc == smartgen.SG_EUNSUPPORTED and "head dimension" in _err(lib)
+    rc = lib.sg_score_topshare(None, 1, 1, 1, 64, 8, 128, 65, P, 100, 100, P, P, 0, 2000, P, P, 1 << 20)
+    assert rc == smartgen.SG_EUNSUPPORTED and "G*W" in _err(lib)
+    rc = lib.sg_score_topshare(None, 1, 1, 1, 8, 8, 64, 32, P, 4096, 4096, P, P, 0, 2000, P, P, 16)
+    assert rc == smartgen.SG_EWORKSPACE
+    rc = lib.sg_score_topshare(None, 1, 1, 1, 8, 8, 64, 32, P, 0, 0, P, P, 0, 2000, P, P, 0)
+    assert rc == smartgen.SG_OK                                             # nothing to do
