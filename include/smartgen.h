@@ -209,8 +209,14 @@ int sg_topk(void *stream, int B, int L, int Hkv, const int32_t *cu_seqlens, int6
  *   idx     device int32 [L][Hkv][K_total].
  *   dst     device memory or pinned host memory (then the kernel writes over
  *           the host link); 16-byte aligned; dst_bytes >= sg_pack_bytes(...).
- *   max_k   host bound of every k_b: it only sizes the launch (any k_b is
- *           covered), so a tight bound gives the best grid.
+ *   max_k   host bound of every k_b (>= 0): it sizes the launch (at most
+ *           B * max_k slots per row), any k_b is covered, so a tight bound
+ *           gives the best grid.
+ * The call writes the slots [cu_k[0], cu_k[B]) of each (layer, KV head) row,
+ * so a group of requests (cu_seqlens and cu_k pointing into the whole batch's
+ * arrays, K_total the whole batch's) fills its part of a shared buffer.  A slot
+ * in that range that no request's [cu_k[b], cu_k[b+1]) covers (bad offsets)
+ * is left unwritten.
  */
 size_t sg_pack_bytes(sg_dtype dt, int L, int Hkv, int d, int64_t K_total);
 int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,

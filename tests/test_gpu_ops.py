@@ -44,7 +44,7 @@ def test_pack_bit_exact(gpu_lib, dtype, d, lens, ks):
 
 @pytest.mark.parametrize("max_k", [0, 1])
 def test_pack_small_launch_bound_covers_every_row(gpu_lib, max_k):
-    """max_k only sizes the launch: a bound of 0 or 1 still packs every k_b."""
+    """max_k does not shape the launch: a bound of 0 or 1 still packs every k_b."""
     cfg = _cfg(dtype="bf16", d=128, seqlens=(900, 300), B=2, W=4)
     say("pack launch bound", max_k)
     pre = inputs.make_prefill(cfg, device="cuda")
@@ -56,6 +56,45 @@ def test_pack_small_launch_bound_covers_every_row(gpu_lib, max_k):
     gpu_lib.sg_pack(pre["k"], pre["v"], idx, cu(pre["cu_seqlens"]), pre["T"], cu(cuk), cuk[-1], max_k, dst)
     torch.cuda.synchronize()
     ref = oracle.pack(raw(pre["k"]), raw(pre["v"]), raw(idx), pre["cu_seqlens"], cuk)
+    assert np.array_equal(dst.cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("d,dtype,groups", [(128, torch.bfloat16, 1), (64, torch.bfloat16, 1),
+                                            (128, torch.float32, 1), (128, torch.bfloat16, 3)])
+def test_pack_many_requests_chunks_across_boundaries(gpu_lib, d, dtype, groups):
+    """Chunks that span request boundaries, requests without selected rows, a
+    request without tokens (its rows are zero) and invalid indices, over two
+    layers; with groups > 1 the requests are packed in calls over consecutive
+    groups of them into one buffer (offsets into the whole batch)."""
+    lens = [50, 0, 7, 300, 33, 1, 0, 64, 129, 5, 2, 40, 31, 90, 17]
+    ks = [9, 4, 7, 61, 0, 1, 0, 32, 33, 0, 2, 40, 1, 45, 3]
+    say("pack across request boundaries", d, dtype)
+    g = torch.Generator().manual_seed(77)
+    L, Hkv, T = 2, 3, sum(lens)
+    k = torch.randn((L, Hkv, T, d), generator=g).to(dtype).cuda()
+    v = torch.randn((L, Hkv, T, d), generator=g).to(dtype).cuda()
+    cuk = inputs.cu_from_lengths(ks)
+    idx = torch.empty((L, Hkv, cuk[-1]), dtype=torch.int32)
+    for l in range(L):
+        for h in range(Hkv):
+            for b, (n, kb) in enumerate(zip(lens, ks)):
+                if kb == 0:
+                    continue
+                sel = torch.randperm(max(n, 1), generator=g)[:kb].sort().values if n >= kb else \
+                    torch.randint(-3, 5, (kb,), generator=g)
+                idx[l, h, cuk[b]:cuk[b + 1]] = sel.to(torch.int32)
+    idx[0, 1, 5] = -1                 # invalid entries inside a valid request
+    idx[1, 2, cuk[3] + 7] = lens[3]
+    idx = idx.cuda()
+    cus = inputs.cu_from_lengths(lens)
+    nbytes = gpu_lib.pack_bytes(dtype, L, Hkv, d, cuk[-1])
+    dst = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device="cuda")
+    cus_d, cuk_d = cu(cus), cu(cuk)
+    cuts = [len(lens) * g // groups for g in range(groups + 1)]
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        gpu_lib.sg_pack(k, v, idx, cus_d[a:b + 1], T, cuk_d[a:b + 1], cuk[-1], max(ks[a:b]), dst, L=L, Hkv=Hkv)
+    torch.cuda.synchronize()
+    ref = oracle.pack(raw(k), raw(v), raw(idx), cus, cuk)
     assert np.array_equal(dst.cpu().numpy(), ref)
 
 
