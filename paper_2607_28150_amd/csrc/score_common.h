@@ -122,10 +122,10 @@ __device__ __forceinline__ void dma16_sbase(const char *base, unsigned off, unsi
 // 32 (or 16) lanes reading one fragment column hit distinct banks.  Tiles
 // arrive through direct global->LDS loads (lane i of an instruction lands at
 // base + 16 i; the swizzle is applied to the global address each lane reads).
-template <typename T, int D>
+template <typename T, int D, int TKEYS = (sizeof(T) == 2 ? 128 : 64)>
 struct KTile {
     static constexpr int VPR = D * (int)sizeof(T) / 16;          // 16-byte vectors per key
-    static constexpr int TK = sizeof(T) == 2 ? 128 : 64;          // keys per tile
+    static constexpr int TK = TKEYS;                              // keys per tile
     static constexpr int BYTES = TK * VPR * 16;
     static constexpr int NKB = TK / MT<T, D>::BM;                 // key blocks per tile
 
@@ -142,7 +142,7 @@ struct KTile {
         asm volatile("" : "+v"(lane));
         const unsigned kl = (unsigned)lane / VPR, vl = (unsigned)lane % VPR;
         const char *tb = reinterpret_cast<const char *>(kunit) + (int64_t)key0 * (VPR * 16);   // wavefront-uniform
-        if constexpr (sizeof(T) == 2 && SC_SCALAR_BASE) {
+        if constexpr (sizeof(T) == 2 && SC_SCALAR_BASE && KPW % VPR == 0) {
             // A whole bf16 tile: every wavefront's first key is a multiple of VPR
             // and the swizzle repeats every PER instructions, so the lane's 32-bit
             // offsets of PER instructions serve them all, each instruction taking

@@ -75,10 +75,10 @@ __device__ __forceinline__ TC<T, D> block_mma_refill(const char *buf, int next, 
 // a key block refills them with the next key block's behind its own MFMAs.
 // Scheduling barriers keep the compiler from hoisting later loads, and group
 // barriers interleave each MFMA with a share of the vector work.
-template <typename T, int D, bool KEY_ROWS, typename F>
+template <typename T, int D, bool KEY_ROWS, int TKEYS = KTile<T, D>::TK, typename F>
 __device__ __forceinline__ void tile_sweep(const char *buf, const QFrags<T, D> &q,
                                            const TC<T, D> (&c0)[QFrags<T, D>::NRB], int lane, F &&valu) {
-    constexpr int NKB = KTile<T, D>::NKB, NRB = QFrags<T, D>::NRB, NB = NKB * NRB;
+    constexpr int NKB = KTile<T, D, TKEYS>::NKB, NRB = QFrags<T, D>::NRB, NB = NKB * NRB;
     // a block's vector work is about 3 instructions per output value
     constexpr int VALU_PER_MFMA = (3 * MT<T, D>::NV + MT<T, D>::KS - 1) / MT<T, D>::KS;
     TA<T, D> kf[MT<T, D>::KS];
@@ -110,10 +110,10 @@ __device__ __forceinline__ void tile_sweep(const char *buf, const QFrags<T, D> &
 // The same products without pipelining, for the few tiles at the end of a
 // prompt (keeps their masking work from raising the register needs of the
 // main loop).
-template <typename T, int D, bool KEY_ROWS, typename F>
+template <typename T, int D, bool KEY_ROWS, int TKEYS = KTile<T, D>::TK, typename F>
 __device__ __forceinline__ void tile_sweep_plain(const char *buf, const QFrags<T, D> &q,
                                                  const TC<T, D> (&c0)[QFrags<T, D>::NRB], int lane, F &&valu) {
-    constexpr int NKB = KTile<T, D>::NKB, NRB = QFrags<T, D>::NRB;
+    constexpr int NKB = KTile<T, D, TKEYS>::NKB, NRB = QFrags<T, D>::NRB;
 #pragma unroll 1
     for (int kb = 0; kb < NKB; ++kb) {
         TA<T, D> kf[MT<T, D>::KS];
