@@ -17,7 +17,8 @@
 // Both passes use one engine.  A workgroup owns one (unit, chunk) and has one
 // wavefront per 64 query rows; each wavefront keeps its rows in registers as
 // MFMA operand fragments.  The chunk's keys stream through LDS in tiles of 64
-// keys, double buffered: direct global->LDS loads of the
+// keys (stats) or 128 (colsum; 64 at fp32), double buffered: direct
+// global->LDS loads of the
 // next tile run while every wavefront multiplies its rows against the current
 // one with v_mfma_f32_32x32x16_bf16 (bf16) or v_mfma_f32_16x16x4_f32 (fp32),
 // fp32 accumulation; one workgroup barrier per tile.  Within a tile the
@@ -43,13 +44,18 @@
 
 namespace sg {
 
-// Keys per LDS tile.  64-key tiles (32 KB double buffered at bf16 d = 128)
-// let the stats pass hold three workgroups per CU, three wavefronts per SIMD
-// (168 VGPRs), where 128-key tiles allowed two: on the 8K workload the stats
-// pass took 166 against 178 us.  The colsum pass needs about 200 VGPRs and
-// stays at two wavefronts per SIMD (at three the compiler spills 50 or more
-// registers and the pass slows by half); the shorter tiles cost it nothing.
-constexpr int SC_TILE_KEYS = 64;
+// Keys per LDS tile.  The stats pass takes 64-key tiles (32 KB double
+// buffered at bf16 d = 128), so three workgroups fit a CU and the pass runs at
+// three wavefronts per SIMD (168 VGPRs), where 128-key tiles allowed two.  The
+// colsum pass needs about 200 VGPRs and stays at two wavefronts per SIMD (at
+// three the compiler spills 50 or more registers, even with the row
+// normalisers read from LDS, and the pass slows by half); it keeps 128-key
+// tiles, which measured 2-3% faster for it than 64 at the 64-request shape.
+// Same box, alternating builds: 64 requests, two passes 43.8 against 44.0 ms
+// and the request pairs 40.9 against 41.2 ms; 8K workload 325 against 331 us.
+constexpr int SC_STATS_TILE_KEYS = 64;
+template <typename T>
+constexpr int colsum_tile_keys() { return sizeof(T) == 2 ? 128 : 64; }
 
 // Wavefronts per SIMD the stats kernel is compiled for: three for the bf16
 // probability pass (168 VGPRs, 2 spilled); the count mode's max-only pass and
@@ -151,7 +157,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(stats_w
     const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, float c2, int nchunk, int chunk_keys,
     float2 *__restrict__ part) {
     using M = MT<T, D>;
-    using KT = KTile<T, D, SC_TILE_KEYS>;
+    using KT = KTile<T, D, SC_STATS_TILE_KEYS>;
     constexpr int NRB = QFrags<T, D>::NRB;
     // two tile buffers as separate objects: the compiler can then tell that the
     // direct loads into one never alias the fragment reads from the other
@@ -193,20 +199,20 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(stats_w
     };
     auto full = [&](const char *buf, int key0) {       // every row sees every key of the tile
         if constexpr (MAXONLY) {
-            tile_sweep<T, D, true, SC_TILE_KEYS>(buf, q, zero, lane, StatsMax<T, D, false>{m, lane, wave, key0, N, W, R});
+            tile_sweep<T, D, true, SC_STATS_TILE_KEYS>(buf, q, zero, lane, StatsMax<T, D, false>{m, lane, wave, key0, N, W, R});
         } else {
             unsigned need = 0u;
-            tile_sweep<T, D, true, SC_TILE_KEYS>(buf, q, zero, lane, StatsFast<T, D>{m, s, need, c2});
+            tile_sweep<T, D, true, SC_STATS_TILE_KEYS>(buf, q, zero, lane, StatsFast<T, D>{m, s, need, c2});
             if (__any(need != 0u))             // rare: those blocks again, exactly
-                tile_sweep<T, D, true, SC_TILE_KEYS>(buf, q, zero, lane,
+                tile_sweep<T, D, true, SC_STATS_TILE_KEYS>(buf, q, zero, lane,
                                        StatsExact<T, D, false>{m, s, need, lane, wave, key0, N, W, R, c2});
         }
     };
     auto masked = [&](const char *buf, int key0) {     // causal limit and prompt end (or a leftover full tile)
         if constexpr (MAXONLY)
-            tile_sweep_plain<T, D, true, SC_TILE_KEYS>(buf, q, zero, lane, StatsMax<T, D, true>{m, lane, wave, key0, N, W, R});
+            tile_sweep_plain<T, D, true, SC_STATS_TILE_KEYS>(buf, q, zero, lane, StatsMax<T, D, true>{m, lane, wave, key0, N, W, R});
         else
-            tile_sweep_plain<T, D, true, SC_TILE_KEYS>(buf, q, zero, lane,
+            tile_sweep_plain<T, D, true, SC_STATS_TILE_KEYS>(buf, q, zero, lane,
                                          StatsExact<T, D, true>{m, s, ~0u, lane, wave, key0, N, W, R, c2});
     };
     const int nfull = full_tiles(key_begin, ntile, KT::TK, N, W);
@@ -247,7 +253,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(stats_w
 // raw product units, and a key adds 1 where the row picks it (acc >= 0).
 template <typename T, int D, bool MASK, bool COUNT>
 struct ColsumStep {
-    float (&cs)[KTile<T, D, SC_TILE_KEYS>::NKB];
+    float (&cs)[KTile<T, D, colsum_tile_keys<T>()>::NKB];
     const int *poss;    // window position of every row of the unit (-1 for padded rows), LDS
     int lane, wave, key0;
     float c2;
@@ -279,7 +285,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
     const T *__restrict__ q_win, const T *__restrict__ k, int64_t k_layer_rows, float c2, int nchunk, int chunk_keys,
     const float2 *__restrict__ part, const float *__restrict__ lse_in, float thr_off, float *__restrict__ scores) {
     using M = MT<T, D>;
-    using KT = KTile<T, D, SC_TILE_KEYS>;
+    using KT = KTile<T, D, colsum_tile_keys<T>()>;
     constexpr int NRB = QFrags<T, D>::NRB, NKB = KT::NKB;
     __shared__ __attribute__((aligned(16))) char kbA[KT::BYTES];   // separate objects, see the stats kernel
     __shared__ __attribute__((aligned(16))) char kbB[KT::BYTES];
@@ -375,9 +381,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb) cs[kb] = 0.f;
         if (MASK)
-            tile_sweep_plain<T, D, false, SC_TILE_KEYS>(cur, q, c0, lane, ColsumStep<T, D, true, COUNT>{cs, poss, lane, wave, key0, c2});
+            tile_sweep_plain<T, D, false, colsum_tile_keys<T>()>(cur, q, c0, lane, ColsumStep<T, D, true, COUNT>{cs, poss, lane, wave, key0, c2});
         else
-            tile_sweep<T, D, false, SC_TILE_KEYS>(cur, q, c0, lane, ColsumStep<T, D, false, COUNT>{cs, poss, lane, wave, key0, c2});
+            tile_sweep<T, D, false, colsum_tile_keys<T>()>(cur, q, c0, lane, ColsumStep<T, D, false, COUNT>{cs, poss, lane, wave, key0, c2});
         // lanes holding the same key (different rows) add up; every such lane
         // then holds the total and stores it (same value, same address: no
         // branch, so the exponentials are not moved behind one)
