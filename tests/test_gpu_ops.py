@@ -98,6 +98,33 @@ def test_pack_many_requests_chunks_across_boundaries(gpu_lib, d, dtype, groups):
     assert np.array_equal(dst.cpu().numpy(), ref)
 
 
+def test_pack_bad_offsets_leave_slots_unwritten(gpu_lib):
+    """Offsets past K_total make a request's segment empty: its slots keep
+    their bytes, the valid request is packed as usual."""
+    say("pack bad offsets")
+    g = torch.Generator().manual_seed(5)
+    L, Hkv, d, T = 1, 2, 128, 90
+    k = torch.randn((L, Hkv, T, d), generator=g).to(torch.bfloat16).cuda()
+    v = torch.randn((L, Hkv, T, d), generator=g).to(torch.bfloat16).cuda()
+    K_total = 40
+    idx = torch.randint(0, 30, (L, Hkv, K_total), generator=g, dtype=torch.int32).cuda()
+    cus = [0, 30, 60, 90]
+    cuk_bad = [0, 20, 100, 40]          # requests 1 and 2 end or start past K_total
+    nbytes = gpu_lib.pack_bytes(torch.bfloat16, L, Hkv, d, K_total)
+    dst = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device="cuda")
+    gpu_lib.sg_pack(k, v, idx, cu(cus), T, cu(cuk_bad), K_total, 20, dst)
+    torch.cuda.synchronize()
+    # request 0 alone with the same slots, from the oracle
+    ref = oracle.pack(raw(k), raw(v), raw(idx), [0, 30, 30, 30], [0, 20, 20, 40])
+    got = dst.cpu().numpy()
+    S, rowb = L * Hkv * K_total, d * 2
+    for h in range(Hkv):
+        for region, width in ((0, rowb), (S * rowb, rowb), (2 * S * rowb, 4)):
+            lo = region + h * K_total * width
+            assert np.array_equal(got[lo:lo + 20 * width], ref[lo:lo + 20 * width])
+            assert (got[lo + 20 * width:lo + K_total * width] == 0xAB).all()
+
+
 def test_pack_to_pinned_host_and_full_selection(gpu_lib):
     cfg = _cfg(seqlens=(333,), L=1, W=4)
     say("pack pinned host full selection")
