@@ -1249,19 +1249,34 @@ def cpu_baseline(cfg, s, min_seconds):
     def decode_once():
         oracle.decode_attn(*s["dec"])
 
-    def timed(fn):
+    def timed(fn, seconds=min_seconds):
         reps = 0
         t0 = time.perf_counter()
         while True:
             fn()
             reps += 1
-            if time.perf_counter() - t0 >= min_seconds:
+            if time.perf_counter() - t0 >= seconds:
                 break
         return (time.perf_counter() - t0) / reps, reps
 
     dt, reps = timed(select_once)
     kv_bytes = 2 * units * s["n0"] * cfg.d * s["esize"]
     ddt, dreps = timed(decode_once)
+    # one thread, on a slice of the same samples: the select half for layer 0's
+    # KV heads, the decode half as above
+    q1, k1, kr1, vr1 = s["q0"][:, :1], s["k0"][:1], s["kraw0"][:1], s["vraw0"][:1]
+
+    def select_one_layer():
+        sc = oracle.score(q1, k1, cu, cfg.Hkv)
+        ix = oracle.topk(sc.astype(np.float32), cu, ck)
+        oracle.pack(kr1, vr1, ix, cu, ck)
+
+    oracle.set_threads(1)
+    try:
+        dt1, reps1 = timed(select_one_layer, min_seconds / 4)
+        ddt1, dreps1 = timed(decode_once, min_seconds / 4)
+    finally:
+        oracle.set_threads(threads)
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -1282,6 +1297,12 @@ def cpu_baseline(cfg, s, min_seconds):
                        "sample": f"decode attention of layer 0, decode step 0, all {B} requests x {cfg.Hkv} KV heads "
                                  f"({s['dec_rows']} rows: seeded selection + extras at the workload's sizes); "
                                  f"tokens/s = requests / (seconds per layer x {cfg.L} layers)"},
+            "single_thread": {"value": round(2 * cfg.Hkv * s["n0"] * cfg.d * s["esize"] / dt1 / 1e9, 4),
+                              "unit": "GB/s", "seconds_per_pass": round(dt1, 3), "passes": reps1,
+                              "decode_tokens_per_s": round(B / (ddt1 * cfg.L), 2),
+                              "decode_seconds_per_pass": round(ddt1, 3), "decode_passes": dreps1,
+                              "sample": f"select half: layer 0's {cfg.Hkv} KV heads of request 0; decode half: "
+                                        "the decode sample above; one OpenMP thread"},
             "cpu_model": cpu, "host": platform.node()}
 
 
