@@ -67,75 +67,75 @@ __global__ __launch_bounds__(PACK_THREADS) void pack_kernel(
         s0 = okt ? t0 : 0;
         nb = okt ? t1 - t0 : 0;
     };
-  for (int64_t i0 = first + ((int64_t)blockIdx.x % nchunk) * ROWS; i0 < last; i0 += nchunk * ROWS) {
-    const int64_t i1 = min<int64_t>(last, i0 + ROWS);     // slots [i0, i1) of the row
-    const int b0 = request_of_slot(cu_k, B, i0);
-    int64_t c0, kb, s0, nb;
-    segment(b0, c0, kb, s0, nb);
-    if (nb > 0 && i0 >= c0 && i1 <= c0 + kb) {
-        // Every row of the chunk belongs to request b0, which has tokens.
-        // Every load is issued before any result is used: the indices first,
-        // then the K and V rows (an invalid index reads row 0 of the request
-        // and is zeroed afterwards).  Loads behind branches would make each
-        // wait for all the loads before it.
-        int32_t t[PACK_UNROLL];
+    for (int64_t i0 = first + ((int64_t)blockIdx.x % nchunk) * ROWS; i0 < last; i0 += nchunk * ROWS) {
+        const int64_t i1 = min<int64_t>(last, i0 + ROWS);     // slots [i0, i1) of the row
+        const int b0 = request_of_slot(cu_k, B, i0);
+        int64_t c0, kb, s0, nb;
+        segment(b0, c0, kb, s0, nb);
+        if (nb > 0 && i0 >= c0 && i1 <= c0 + kb) {
+            // Every row of the chunk belongs to request b0, which has tokens.
+            // Every load is issued before any result is used: the indices first,
+            // then the K and V rows (an invalid index reads row 0 of the request
+            // and is zeroed afterwards).  Loads behind branches would make each
+            // wait for all the loads before it.
+            int32_t t[PACK_UNROLL];
 #pragma unroll
-        for (int j = 0; j < PACK_UNROLL; ++j) t[j] = idx[slot0 + min<int64_t>(i0 + rsub + j * RPI, i1 - 1)];
-        __builtin_amdgcn_sched_barrier(0);      // every index load ahead of the row loads
-        v4u kr[PACK_UNROLL], vr[PACK_UNROLL];
-        bool ok[PACK_UNROLL];
+            for (int j = 0; j < PACK_UNROLL; ++j) t[j] = idx[slot0 + min<int64_t>(i0 + rsub + j * RPI, i1 - 1)];
+            __builtin_amdgcn_sched_barrier(0);      // every index load ahead of the row loads
+            v4u kr[PACK_UNROLL], vr[PACK_UNROLL];
+            bool ok[PACK_UNROLL];
 #pragma unroll
-        for (int j = 0; j < PACK_UNROLL; ++j) {
-            ok[j] = t[j] >= 0 && t[j] < nb;
-            const int64_t src = (src_lh + s0 + (ok[j] ? t[j] : 0)) * CPR + lane;
-            kr[j] = __builtin_nontemporal_load(k + src);
-            vr[j] = __builtin_nontemporal_load(v + src);
-        }
-        __builtin_amdgcn_sched_barrier(0);      // every row load ahead of the stores
-#pragma unroll
-        for (int j = 0; j < PACK_UNROLL; ++j) {
-            const int64_t i = i0 + rsub + j * RPI;
-            if (i < i1) {
-                const int64_t dst = (slot0 + i) * CPR + lane;
-                __builtin_nontemporal_store(ok[j] ? kr[j] : v4u{0u, 0u, 0u, 0u}, dk + dst);
-                __builtin_nontemporal_store(ok[j] ? vr[j] : v4u{0u, 0u, 0u, 0u}, dv + dst);
+            for (int j = 0; j < PACK_UNROLL; ++j) {
+                ok[j] = t[j] >= 0 && t[j] < nb;
+                const int64_t src = (src_lh + s0 + (ok[j] ? t[j] : 0)) * CPR + lane;
+                kr[j] = __builtin_nontemporal_load(k + src);
+                vr[j] = __builtin_nontemporal_load(v + src);
             }
-        }
-        // the index table from the values already loaded (one lane per row);
-        // no second load, so nothing waits for the stores above to complete
+            __builtin_amdgcn_sched_barrier(0);      // every row load ahead of the stores
 #pragma unroll
+            for (int j = 0; j < PACK_UNROLL; ++j) {
+                const int64_t i = i0 + rsub + j * RPI;
+                if (i < i1) {
+                    const int64_t dst = (slot0 + i) * CPR + lane;
+                    __builtin_nontemporal_store(ok[j] ? kr[j] : v4u{0u, 0u, 0u, 0u}, dk + dst);
+                    __builtin_nontemporal_store(ok[j] ? vr[j] : v4u{0u, 0u, 0u, 0u}, dv + dst);
+                }
+            }
+            // the index table from the values already loaded (one lane per row);
+            // no second load, so nothing waits for the stores above to complete
+#pragma unroll
+            for (int j = 0; j < PACK_UNROLL; ++j) {
+                const int64_t i = i0 + rsub + j * RPI;
+                if (lane == 0 && i < i1) didx[slot0 + i] = t[j];
+            }
+            continue;
+        }
+        // A chunk across a request boundary, or of a request without tokens (zero
+        // rows) or with bad offsets: each row finds its own request, walking on
+        // from b0.  A slot that no valid request covers is left as it is.
+#pragma unroll 1
         for (int j = 0; j < PACK_UNROLL; ++j) {
             const int64_t i = i0 + rsub + j * RPI;
-            if (lane == 0 && i < i1) didx[slot0 + i] = t[j];
+            if (i >= i1) break;
+            int b = b0;
+            while (b + 1 < B && (int64_t)cu_k[b + 1] <= i) ++b;
+            int64_t rc0, rkb, rs0, rnb;
+            segment(b, rc0, rkb, rs0, rnb);
+            if (i < rc0 || i >= rc0 + rkb) continue;
+            const int32_t t = idx[slot0 + i];
+            const bool ok = t >= 0 && t < rnb;
+            v4u kr = v4u{0u, 0u, 0u, 0u}, vr = v4u{0u, 0u, 0u, 0u};
+            if (ok) {
+                const int64_t src = (src_lh + rs0 + t) * CPR + lane;
+                kr = __builtin_nontemporal_load(k + src);
+                vr = __builtin_nontemporal_load(v + src);
+            }
+            const int64_t dst = (slot0 + i) * CPR + lane;
+            __builtin_nontemporal_store(kr, dk + dst);
+            __builtin_nontemporal_store(vr, dv + dst);
+            if (lane == 0) didx[slot0 + i] = t;
         }
-        continue;
     }
-    // A chunk across a request boundary, or of a request without tokens (zero
-    // rows) or with bad offsets: each row finds its own request, walking on
-    // from b0.  A slot that no valid request covers is left as it is.
-#pragma unroll 1
-    for (int j = 0; j < PACK_UNROLL; ++j) {
-        const int64_t i = i0 + rsub + j * RPI;
-        if (i >= i1) break;
-        int b = b0;
-        while (b + 1 < B && (int64_t)cu_k[b + 1] <= i) ++b;
-        int64_t rc0, rkb, rs0, rnb;
-        segment(b, rc0, rkb, rs0, rnb);
-        if (i < rc0 || i >= rc0 + rkb) continue;
-        const int32_t t = idx[slot0 + i];
-        const bool ok = t >= 0 && t < rnb;
-        v4u kr = v4u{0u, 0u, 0u, 0u}, vr = v4u{0u, 0u, 0u, 0u};
-        if (ok) {
-            const int64_t src = (src_lh + rs0 + t) * CPR + lane;
-            kr = __builtin_nontemporal_load(k + src);
-            vr = __builtin_nontemporal_load(v + src);
-        }
-        const int64_t dst = (slot0 + i) * CPR + lane;
-        __builtin_nontemporal_store(kr, dk + dst);
-        __builtin_nontemporal_store(vr, dv + dst);
-        if (lane == 0) didx[slot0 + i] = t;
-    }
-  }
 }
 
 }  // namespace sg
