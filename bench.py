@@ -57,6 +57,11 @@ TRAFFIC_SUMMARY = os.path.join(_ROOT, "profiles", "decode_attn.batched64.hbm_tra
 TRACE_SUMMARY = os.path.join(_ROOT, "profiles", "all_kernels.batched64.kernel_trace.md")
 TRAFFIC_SOURCES = ("paper_2607_28150_amd/csrc/decode_attn.hip", "paper_2607_28150_amd/csrc/sg_internal.h")
 REPS, WARM = 20, 3
+# workgroup budget of a request pair's pack beside the next pair's score: it
+# finishes within that score and disturbs it less than the full-rate grid
+# (64-request workload, the select region: 47.6 ms at 1,024, 47.8 at 2,048,
+# 48.6 without a budget, 54.5 at 512)
+PAIR_PACK_WORKGROUPS = 1024
 
 
 def parse():
@@ -278,7 +283,8 @@ class Path:
                 self.sg.sg_topk(self.scores, self.cus[a:b + 1], self.T, g["nmax"], self.cuk[a:b + 1], self.K_total,
                                 self.idx)
                 self.sg.sg_pack(self.pre["k"], self.pre["v"], self.idx, self.cus[a:b + 1], self.T,
-                                self.cuk[a:b + 1], self.K_total, g["maxk"], self.tbuf, L=c.L, Hkv=c.Hkv)
+                                self.cuk[a:b + 1], self.K_total, g["maxk"], self.tbuf, L=c.L, Hkv=c.Hkv,
+                                max_workgroups=PAIR_PACK_WORKGROUPS)
         main.wait_stream(side)
 
     def receive(self, rep=0):

@@ -212,6 +212,12 @@ int sg_topk(void *stream, int B, int L, int Hkv, const int32_t *cu_seqlens, int6
  *   max_k   host bound of every k_b (>= 0): it sizes the launch (at most
  *           B * max_k slots per row), any k_b is covered, so a tight bound
  *           gives the best grid.
+ *   max_workgroups  0, or a budget of workgroups (64 threads each) for the
+ *           launch: the call then takes chunks of rows a grid stride apart, at
+ *           least one workgroup per (layer, KV head) row.  A pack that runs
+ *           beside compute kernels on another stream (the select region's
+ *           request groups) disturbs them less with a budget; alone it is
+ *           fastest without one.  < 0 -> SG_EINVAL.
  * The call writes the slots [cu_k[0], cu_k[B]) of each (layer, KV head) row,
  * so a group of requests (cu_seqlens and cu_k pointing into the whole batch's
  * arrays, K_total the whole batch's) fills its part of a shared buffer.  A slot
@@ -222,7 +228,7 @@ size_t sg_pack_bytes(sg_dtype dt, int L, int Hkv, int d, int64_t K_total);
 int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,
             const int32_t *cu_seqlens, int64_t T, const int32_t *cu_k, int64_t K_total,
             int max_k, const void *k, const void *v, int64_t kv_layer_rows, const int32_t *idx,
-            void *dst, size_t dst_bytes);
+            void *dst, size_t dst_bytes, int max_workgroups);
 
 /* ---------------------------------------------------------------- sg_split
  * Algorithm 1: KV index splitting and (optional) reordering.  Row r holds

@@ -151,12 +151,13 @@ extern "C" size_t sg_pack_bytes(sg_dtype dt, int L, int Hkv, int d, int64_t K_to
 extern "C" int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,
                        const int32_t *cu_seqlens, int64_t T, const int32_t *cu_k, int64_t K_total,
                        int max_k, const void *k, const void *v, int64_t kv_layer_rows,
-                       const int32_t *idx, void *dst, size_t dst_bytes) {
+                       const int32_t *idx, void *dst, size_t dst_bytes, int max_workgroups) {
     SG_REQUIRE(dt == SG_F32 || dt == SG_BF16, SG_EINVAL, "sg_pack: unknown dtype %d", (int)dt);
     SG_REQUIRE(B >= 1 && L >= 1 && Hkv >= 1, SG_EINVAL, "sg_pack: B, L, Hkv must be >= 1 (got %d, %d, %d)", B, L, Hkv);
     SG_REQUIRE(d == 64 || d == 128, SG_EUNSUPPORTED, "sg_pack: head dimension %d not supported (64 or 128)", d);
     SG_REQUIRE(T >= 0 && K_total >= 0 && max_k >= 0, SG_EINVAL, "sg_pack: negative size");
     SG_REQUIRE(kv_layer_rows >= 0, SG_EINVAL, "sg_pack: negative layer stride");
+    SG_REQUIRE(max_workgroups >= 0, SG_EINVAL, "sg_pack: negative workgroup budget");
     const size_t need = sg_pack_bytes(dt, L, Hkv, d, K_total);
     SG_REQUIRE(dst_bytes >= need, SG_EWORKSPACE, "sg_pack: destination holds %zu bytes, needs %zu", dst_bytes, need);
     if (K_total == 0) return SG_OK;
@@ -171,7 +172,11 @@ extern "C" int sg_pack(void *stream, sg_dtype dt, int B, int L, int Hkv, int d,
     const int rows_per_block = (PACK_THREADS / cpr) * PACK_UNROLL;
     // chunks per (layer, KV head) row: the slots [cu_k[0], cu_k[B]) number at
     // most K_total and, when max_k bounds every k_b, at most B * max_k
-    const int64_t nchunk = std::max<int64_t>(1, ceil_div(std::min<int64_t>(K_total, (int64_t)B * max_k), rows_per_block));
+    int64_t nchunk = std::max<int64_t>(1, ceil_div(std::min<int64_t>(K_total, (int64_t)B * max_k), rows_per_block));
+    // a workgroup budget: fewer workgroups, each taking chunks a grid stride
+    // apart (at least one per row)
+    if (max_workgroups > 0 && (int64_t)L * Hkv * nchunk > max_workgroups)
+        nchunk = std::max<int64_t>(1, max_workgroups / ((int64_t)L * Hkv));
     SG_REQUIRE((int64_t)L * Hkv * nchunk <= 0x7fffffff, SG_EINVAL, "sg_pack: too many rows for one launch");
     const dim3 grid((unsigned)((int64_t)L * Hkv * nchunk));
     hipStream_t s = as_stream(stream);

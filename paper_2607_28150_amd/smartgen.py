@@ -64,7 +64,7 @@ def load() -> ctypes.CDLL:
     lib.sg_topk.argtypes = [_vp, _i, _i, _i, _vp, _l, _i, _vp, _l, _vp, _vp]
     lib.sg_pack_bytes.argtypes = [_i, _i, _i, _i, _l]
     lib.sg_pack_bytes.restype = _sz
-    lib.sg_pack.argtypes = [_vp, _i, _i, _i, _i, _i, _vp, _l, _vp, _l, _i, _vp, _vp, _l, _vp, _vp, _sz]
+    lib.sg_pack.argtypes = [_vp, _i, _i, _i, _i, _i, _vp, _l, _vp, _l, _i, _vp, _vp, _l, _vp, _vp, _sz, _i]
     lib.sg_split.argtypes = [_vp, _i, _vp, _l, _vp, _vp, _l, _vp, _vp, _i, _vp, _vp, _vp, _vp, _vp, _vp]
     lib.sg_fetch.argtypes = [_vp, _i, _i, _i, _vp, _l, _vp, _vp, _vp, _l, _vp, _vp, _vp, _i, _i, _vp, _vp, _vp, _l]
     lib.sg_decode_attn_workspace_size.argtypes = [_i] * 6
@@ -273,8 +273,9 @@ def pack_bytes(dtype: torch.dtype, L, Hkv, d, K_total) -> int:
 
 
 def sg_pack(k, v, idx, cu_seqlens, T, cu_k, K_total, max_k, dst, L=None, Hkv=None, kv_layer_rows=None,
-            stream=None):
-    """Writes [K rows | V rows | idx] of every unit into ``dst`` (uint8, device or pinned host)."""
+            stream=None, max_workgroups=0):
+    """Writes [K rows | V rows | idx] of every unit into ``dst`` (uint8, device or pinned host).
+    max_workgroups > 0 caps the launch's workgroups (a pack beside other kernels)."""
     _need(k.dtype == v.dtype, "k and v must share a dtype")
     L = idx.shape[0] if L is None else L
     Hkv = idx.shape[1] if Hkv is None else Hkv
@@ -288,7 +289,7 @@ def sg_pack(k, v, idx, cu_seqlens, T, cu_k, K_total, max_k, dst, L=None, Hkv=Non
     _need(cu_k.numel() == B + 1, "cu_k must have B+1 entries")
     rc = load().sg_pack(_stream(stream), _dtype_code(k), B, L, Hkv, d, _ptr(cu_seqlens), int(T), _ptr(cu_k),
                         int(K_total), int(max_k), _ptr(k), _ptr(v), int(kv_layer_rows), _ptr(idx), _ptr(dst),
-                        dst.numel() * dst.element_size())
+                        dst.numel() * dst.element_size(), int(max_workgroups))
     _check("sg_pack", rc)
     return dst
 

@@ -88,12 +88,14 @@ def test_topk_rejections(lib):
 
 
 def test_pack_rejections(lib):
-    rc = lib.sg_pack(None, 1, 1, 1, 1, 128, P, 100, P, 10, 10, P, P, 100, P, P, 100)
+    rc = lib.sg_pack(None, 1, 1, 1, 1, 128, P, 100, P, 10, 10, P, P, 100, P, P, 100, 0)
     assert rc == smartgen.SG_EWORKSPACE
-    rc = lib.sg_pack(None, 1, 1, 1, 1, 80, P, 100, P, 10, 10, P, P, 100, P, P, 1 << 20)
+    rc = lib.sg_pack(None, 1, 1, 1, 1, 80, P, 100, P, 10, 10, P, P, 100, P, P, 1 << 20, 0)
     assert rc == smartgen.SG_EUNSUPPORTED
-    rc = lib.sg_pack(None, 1, 1, 1, 1, 128, P, 100, P, 10, 10, ctypes.c_void_p(18), P, 100, P, P, 1 << 20)
+    rc = lib.sg_pack(None, 1, 1, 1, 1, 128, P, 100, P, 10, 10, ctypes.c_void_p(18), P, 100, P, P, 1 << 20, 0)
     assert rc == smartgen.SG_EINVAL and "aligned" in _err(lib)
+    rc = lib.sg_pack(None, 1, 1, 1, 1, 128, P, 100, P, 10, 10, P, P, 100, P, P, 1 << 20, -1)
+    assert rc == smartgen.SG_EINVAL and "budget" in _err(lib)
 
 
 def test_split_fetch_decode_rejections(lib):

@@ -59,16 +59,18 @@ def test_pack_small_launch_bound_covers_every_row(gpu_lib, max_k):
     assert np.array_equal(dst.cpu().numpy(), ref)
 
 
-@pytest.mark.parametrize("d,dtype,groups", [(128, torch.bfloat16, 1), (64, torch.bfloat16, 1),
-                                            (128, torch.float32, 1), (128, torch.bfloat16, 3)])
-def test_pack_many_requests_chunks_across_boundaries(gpu_lib, d, dtype, groups):
+@pytest.mark.parametrize("d,dtype,groups,budget", [(128, torch.bfloat16, 1, 0), (64, torch.bfloat16, 1, 0),
+                                                   (128, torch.float32, 1, 0), (128, torch.bfloat16, 3, 0),
+                                                   (128, torch.bfloat16, 1, 8), (64, torch.bfloat16, 3, 7)])
+def test_pack_many_requests_chunks_across_boundaries(gpu_lib, d, dtype, groups, budget):
     """Chunks that span request boundaries, requests without selected rows, a
     request without tokens (its rows are zero) and invalid indices, over two
     layers; with groups > 1 the requests are packed in calls over consecutive
-    groups of them into one buffer (offsets into the whole batch)."""
+    groups of them into one buffer (offsets into the whole batch); a budget
+    of workgroups makes each take many chunks a grid stride apart."""
     lens = [50, 0, 7, 300, 33, 1, 0, 64, 129, 5, 2, 40, 31, 90, 17]
     ks = [9, 4, 7, 61, 0, 1, 0, 32, 33, 0, 2, 40, 1, 45, 3]
-    say("pack across request boundaries", d, dtype)
+    say("pack across request boundaries", d, dtype, groups, budget)
     g = torch.Generator().manual_seed(77)
     L, Hkv, T = 2, 3, sum(lens)
     k = torch.randn((L, Hkv, T, d), generator=g).to(dtype).cuda()
@@ -92,7 +94,8 @@ def test_pack_many_requests_chunks_across_boundaries(gpu_lib, d, dtype, groups):
     cus_d, cuk_d = cu(cus), cu(cuk)
     cuts = [len(lens) * g // groups for g in range(groups + 1)]
     for a, b in zip(cuts[:-1], cuts[1:]):
-        gpu_lib.sg_pack(k, v, idx, cus_d[a:b + 1], T, cuk_d[a:b + 1], cuk[-1], max(ks[a:b]), dst, L=L, Hkv=Hkv)
+        gpu_lib.sg_pack(k, v, idx, cus_d[a:b + 1], T, cuk_d[a:b + 1], cuk[-1], max(ks[a:b]), dst, L=L, Hkv=Hkv,
+                        max_workgroups=budget)
     torch.cuda.synchronize()
     ref = oracle.pack(raw(k), raw(v), raw(idx), cus, cuk)
     assert np.array_equal(dst.cpu().numpy(), ref)
