@@ -664,19 +664,6 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(int Hq, int Hkv, int 
     }
 }
 
-static int device_cus() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0, v = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-            cus = v;
-        else
-            cus = 256;
-    }
-    return cus;
-}
-
 // Most splits a call can use (the workspace is sized for it): splits are at
 // least DEC_MIN_SPLIT_ROWS rows long.
 static int64_t max_splits(int64_t max_rows) { return std::max<int64_t>(1, ceil_div(max_rows, DEC_MIN_SPLIT_ROWS)); }

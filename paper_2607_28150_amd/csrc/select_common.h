@@ -1,6 +1,6 @@
-// Exact top-k of a row held in registers by one 1024-thread workgroup:
-// wavefront-level radix select, shared by sg_topk and the decode-time
-// selection.
+// Exact top-k of a row held in registers by one workgroup of NT threads (1024
+// by default): wavefront-level radix select, shared by sg_topk and the
+// decode-time selection.
 //
 // Scores are mapped to order-preserving 32-bit keys (NaN -> 0, the lowest key;
 // -0 -> +0).  Four 8-bit digit passes, most significant first, narrow down the
@@ -30,8 +30,10 @@ __device__ __forceinline__ uint32_t order_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// inclusive scan over the 1024 threads of the block; `tot` receives the block total
+// inclusive scan over the NT threads of the block; `tot` receives the block total
+template <int NT = TOPK_THREADS>
 __device__ __forceinline__ int block_scan_incl(int x, int *wsum, int &tot) {
+    constexpr int NWV = NT / 64;
     const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -43,7 +45,7 @@ __device__ __forceinline__ int block_scan_incl(int x, int *wsum, int &tot) {
     int before = 0;
     tot = 0;
 #pragma unroll
-    for (int w = 0; w < TOPK_WAVES; ++w) {
+    for (int w = 0; w < NWV; ++w) {
         const int v = wsum[w];
         before += (w < wave) ? v : 0;
         tot += v;
@@ -52,27 +54,30 @@ __device__ __forceinline__ int block_scan_incl(int x, int *wsum, int &tot) {
     return x + before;
 }
 
-struct SelectSmem {
-    uint32_t hist[TOPK_WAVES][256];
-    int wsum[TOPK_WAVES];
-    int wsum2[TOPK_WAVES];
+template <int NT>
+struct SelectSmemT {
+    uint32_t hist[NT / 64][256];
+    int wsum[NT / 64];
+    int wsum2[NT / 64];
     uint32_t digit;
     int rem;
 };
+using SelectSmem = SelectSmemT<TOPK_THREADS>;
 
 // Thread t holds keys key[0 .. nv) of row entries first + i.  Writes the ids
 // of the kk largest keys (ties: lower id), ascending, to out[0 .. kk).
 // 0 < kk <= number of valid keys.  Every thread of the block must call it.
-template <int ITEMS>
+template <int ITEMS, int NT = TOPK_THREADS>
 __device__ __forceinline__ void select_top(const uint32_t (&key)[ITEMS], int nv, int first, int kk, int32_t *out,
-                                           SelectSmem &sm) {
+                                           SelectSmemT<NT> &sm) {
+    constexpr int NWV = NT / 64;
     const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
     uint32_t prefix = 0, pmask = 0;
     int rem = kk;
 #pragma unroll 1
     for (int pass = 0; pass < 4; ++pass) {
         const int shift = 24 - 8 * pass;
-        for (int i = tid; i < TOPK_WAVES * 256; i += TOPK_THREADS) (&sm.hist[0][0])[i] = 0;
+        for (int i = tid; i < NWV * 256; i += NT) (&sm.hist[0][0])[i] = 0;
         __syncthreads();
 #pragma unroll
         for (int i = 0; i < ITEMS; ++i) {
@@ -97,10 +102,10 @@ __device__ __forceinline__ void select_top(const uint32_t (&key)[ITEMS], int nv,
         if (tid < 256) {
             const int dg = 255 - tid;
 #pragma unroll
-            for (int w = 0; w < TOPK_WAVES; ++w) cnt += sm.hist[w][dg];
+            for (int w = 0; w < NWV; ++w) cnt += sm.hist[w][dg];
         }
         int tot;
-        const int incl = block_scan_incl(tid < 256 ? cnt : 0, sm.wsum, tot);
+        const int incl = block_scan_incl<NT>(tid < 256 ? cnt : 0, sm.wsum, tot);
         const int excl = incl - cnt;
         if (tid < 256 && cnt > 0 && excl < rem && rem <= incl) {
             sm.digit = 255 - tid;
@@ -122,8 +127,8 @@ __device__ __forceinline__ void select_top(const uint32_t (&key)[ITEMS], int nv,
         eq += (i < nv && key[i] == thr) ? 1 : 0;
     }
     int tot_gt, tot_eq;
-    const int gt_pre = block_scan_incl(gt, sm.wsum, tot_gt) - gt;
-    const int eq_pre = block_scan_incl(eq, sm.wsum2, tot_eq) - eq;
+    const int gt_pre = block_scan_incl<NT>(gt, sm.wsum, tot_gt) - gt;
+    const int eq_pre = block_scan_incl<NT>(eq, sm.wsum2, tot_eq) - eq;
     int pos = gt_pre + min(eq_pre, need);
     int eq_seen = eq_pre;
 #pragma unroll

@@ -1,19 +1,28 @@
 // sg_topk: exact budgeted top-k per unit row by wavefront-level radix select
 // (select_common.h).
 //
-// One 1024-thread workgroup owns one (request, layer, KV head) row (or, for
-// block selection, one request's row of L * M block importances).  The row is
-// held in registers, ITEMS consecutive keys per thread (up to 80).
+// One workgroup owns one (request, layer, KV head) row (or, for block
+// selection, one request's row of L * M block importances).  The row is held
+// in registers, ITEMS consecutive keys per thread (up to 80).  Rows of 8K to
+// 32K keys take 512 threads with 64 keys each (104 VGPRs, 8 KB of LDS) when
+// the call has at least two rows per CU: two workgroups then share a CU, and
+// one fits beside a score workgroup when the select region runs a request
+// pair's top-k beside the next pair's score, where 1024 threads with 32 keys
+// each (110 VGPRs, 84 KB of LDS for the staged row) held a whole CU.  64
+// requests (16,384 rows of 2.6K-32.6K keys): 2.04 against 2.75 ms alone, the
+// select region 46.1 against 46.7 ms.  With fewer rows the 1024-thread form
+// finishes each row sooner (256 rows of 32K keys: 0.050-0.058 against
+// 0.062 ms).
 #include "select_common.h"
 
 namespace sg {
 
-template <int ITEMS>
-__global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(int B, const int32_t *__restrict__ cu_seqlens,
+template <int ITEMS, int NT = TOPK_THREADS>
+__global__ __launch_bounds__(NT) void topk_kernel(int B, const int32_t *__restrict__ cu_seqlens,
                                                             int64_t T, const int32_t *__restrict__ cu_k,
                                                             int64_t K_total, const float *__restrict__ scores,
                                                             int32_t *__restrict__ idx) {
-    __shared__ SelectSmem sm;
+    __shared__ SelectSmemT<NT> sm;
     // long rows pass through LDS in chunks: coalesced loads, then each thread
     // reads its consecutive keys (one pad word per 32 keeps the reads free of
     // bank conflicts); reading them straight from memory would touch a new
@@ -31,13 +40,13 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(int B, const int32_t
     int32_t *out = idx + lh * K_total + c0;
     const int64_t kk = c1 - c0;
     const int64_t N = s1 - s0;
-    if (s0 < 0 || s1 < s0 || s1 > T || kk > N || N > (int64_t)ITEMS * TOPK_THREADS) {
-        for (int64_t i = tid; i < kk; i += TOPK_THREADS) out[i] = -1;
+    if (s0 < 0 || s1 < s0 || s1 > T || kk > N || N > (int64_t)ITEMS * NT) {
+        for (int64_t i = tid; i < kk; i += NT) out[i] = -1;
         return;
     }
     if (kk == 0) return;
     if (kk == N) {  // everything is selected
-        for (int64_t i = tid; i < kk; i += TOPK_THREADS) out[i] = (int32_t)i;
+        for (int64_t i = tid; i < kk; i += NT) out[i] = (int32_t)i;
         return;
     }
     const float *row = scores + lh * T + s0;
@@ -50,7 +59,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(int B, const int32_t
         for (int c0 = 0; c0 < (int)N; c0 += CH) {       // uniform
             const int cn = min<int64_t>(CH, N - c0);
 #pragma unroll 4
-            for (int j = tid; j < cn; j += TOPK_THREADS) stage[j + (j >> 5)] = row[c0 + j];
+            for (int j = tid; j < cn; j += NT) stage[j + (j >> 5)] = row[c0 + j];
             __syncthreads();
 #pragma unroll
             for (int i = 0; i < ITEMS; ++i) {
@@ -74,7 +83,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(int B, const int32_t
         for (int i = 0; i < ITEMS; ++i) key[i] = i < nv ? order_key(row[first + i]) : 0u;
     }
 
-    select_top<ITEMS>(key, nv, first, (int)kk, out, sm);
+    select_top<ITEMS, NT>(key, nv, first, (int)kk, out, sm);
 }
 
 }  // namespace sg
@@ -96,6 +105,8 @@ extern "C" int sg_topk(void *stream, int B, int L, int Hkv, const int32_t *cu_se
         topk_kernel<2><<<(unsigned)blocks, TOPK_THREADS, 0, s>>>(B, cu_seqlens, T, cu_k, K_total, scores, idx);
     else if (max_seqlen <= 8 * TOPK_THREADS)
         topk_kernel<8><<<(unsigned)blocks, TOPK_THREADS, 0, s>>>(B, cu_seqlens, T, cu_k, K_total, scores, idx);
+    else if (max_seqlen <= 32 * TOPK_THREADS && blocks >= 2 * (int64_t)device_cus())
+        topk_kernel<64, 512><<<(unsigned)blocks, 512, 0, s>>>(B, cu_seqlens, T, cu_k, K_total, scores, idx);
     else if (max_seqlen <= 32 * TOPK_THREADS)
         topk_kernel<32><<<(unsigned)blocks, TOPK_THREADS, 0, s>>>(B, cu_seqlens, T, cu_k, K_total, scores, idx);
     else if (max_seqlen <= 64 * TOPK_THREADS)
