@@ -192,6 +192,24 @@ def test_topk_bit_exact(gpu_lib, lens, ks, levels, specials):
     np.testing.assert_array_equal(idx.cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("lens,ks,levels,specials", [
+    ((12000, 32768), (1200, 3276), 0, True),
+    ((9000, 20000), (900, 19999), 25, False),     # heavy ties, k close to N
+])
+def test_topk_many_rows_bit_exact(gpu_lib, lens, ks, levels, specials):
+    """512 rows of 8K-32K keys: the calls with at least two rows per CU take
+    the 512-thread workgroups (64 keys per thread)."""
+    cfg, s = _topk_case(lens, ks, levels, seed=sum(lens) + levels, specials=specials, L=32, Hkv=8)
+    cus, cuk = inputs.cu_from_lengths(lens), inputs.cu_from_lengths(ks)
+    say("topk many rows", lens, ks, levels, specials)
+    sd = s.cuda()
+    idx = torch.full((cfg.L, cfg.Hkv, cuk[-1]), -7, dtype=torch.int32, device="cuda")
+    gpu_lib.sg_topk(sd, cu(cus), cus[-1], max(lens), cu(cuk), cuk[-1], idx)
+    torch.cuda.synchronize()
+    ref = oracle.topk(s.numpy(), cus, cuk)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref)
+
+
 def test_topk_all_equal_is_address_prefix(gpu_lib):
     say("topk all equal")
     s = torch.full((1, 2, 4000), 0.5, dtype=torch.float32, device="cuda")
