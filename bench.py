@@ -733,7 +733,8 @@ def main():
         "select_ms": r4(t_select),
         "value_note": "bytes of the KV cache of every layer and head turned into a transfer buffer per second of "
                       "score + top-k + pack time (medians over the timed steps); the select region runs in pairs "
-                      "of requests, each pair's top-k and pack beside the next pair's score (outputs bit-identical "
+                      "of requests, each pair's top-k and pack (under a budget of 1,024 workgroups) beside the next "
+                      "pair's score (outputs bit-identical "
                       "to one call over the batch); the layers share one K/V source, whose keys the last-level "
                       "cache serves to later layers: ops.select_per_layer_kv times a source per layer" if p.select_groups else
                       "bytes of the KV cache of every layer and head turned into a transfer buffer per second of "
