@@ -10,7 +10,10 @@
 // each of a K/V row, so 256/CPR entries are in flight per step, UNROLL steps
 // deep.  Eight steps (64 KB of a bf16 d = 128 row set per workgroup): scattered
 // single-row reads over the host link wait on its latency, and at four steps
-// the 16 host-source workgroups moved 47 GB/s where eight reach 55.
+// the 16 host-source workgroups moved 47 GB/s where eight reach 55.  Pool
+// pages are written with non-temporal stores (nothing reads them before the
+// whole call has landed): the 64-request receive of 31.8 GB into randomly
+// placed 16-row pages took 6.33 against 6.49 ms with plain stores.
 #include "sg_internal.h"
 
 namespace sg {
@@ -103,8 +106,8 @@ __device__ __forceinline__ void fetch_row(
 #pragma unroll
         for (int j = 0; j < FETCH_UNROLL; ++j) {
             if (dst[j] >= 0) {
-                k_pool[dst[j] * CPR + lane] = kr[j];
-                v_pool[dst[j] * CPR + lane] = vr[j];
+                __builtin_nontemporal_store(kr[j], k_pool + dst[j] * CPR + lane);
+                __builtin_nontemporal_store(vr[j], v_pool + dst[j] * CPR + lane);
             }
             if (KEEP) {
                 if (kdst[j] >= 0) {
