@@ -5,9 +5,11 @@
 // its entry (operator 1); three ballots give, for every lane, how many earlier
 // lanes carry each mask value, so the stable partitions (operators 2, 3) and
 // the stable descending sort by mask value (operators 4, 5) are all prefix
-// popcounts plus a running per-value count.  A first pass counts the remote
-// entries, which fixes where the local entries start in the reordered row.
-// Each pass takes four chunks at a time, issuing all their loads together.
+// popcounts plus a running per-value count.  For a reordered row a first pass
+// counts the remote and local entries, which fixes where the local and pad
+// blocks start; without reordering the row is read once (the 64-request
+// decode step's split: 37.3 M entries, 0.34 ms with both passes).  Each pass
+// takes four chunks at a time, issuing all their loads together.
 #include "sg_internal.h"
 
 namespace sg {
@@ -52,9 +54,10 @@ __global__ __launch_bounds__(64 * SPLIT_WAVES) void split_kernel(
             m[u] = ok && (x == 1 || x == 2) ? x : 0;
         }
     };
-    // pass 1: count remote entries (the start of the local block in the reordered row)
+    // pass 1 (reordered rows only): count remote and local entries, which fix
+    // where the local and pad blocks start in the reordered row
     int64_t n2 = 0, n1 = 0;
-    for (int64_t c = 0; c < n; c += 64 * SPLIT_GROUP) {
+    for (int64_t c = 0; reorder && c < n; c += 64 * SPLIT_GROUP) {
         int32_t t[SPLIT_GROUP];
         int m[SPLIT_GROUP];
         load_group(c, t, m);
@@ -97,6 +100,9 @@ __global__ __launch_bounds__(64 * SPLIT_WAVES) void split_kernel(
             c0 += __popcll(b0);
         }
     }
+    // the running counts are the totals (equal to pass 1's when it ran)
+    n1 = c1;
+    n2 = c2;
     // unused tails of the compacted outputs
     for (int64_t i = n1 + lane; i < n; i += 64) local[o + i] = -1;
     for (int64_t i = n2 + lane; i < n; i += 64) remote[o + i] = -1;
